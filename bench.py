@@ -1,0 +1,308 @@
+"""Benchmark of KV-cache retrieval from a bandwidth-striped KV pool on one MI355X.
+
+One step = one ``kv_pool_retrieve`` of a whole 128K-token LLaMA-3.1-8B-shaped
+request (8192 blocks of 16 tokens, 32 layers, 8 KV heads, head_dim 128, bf16:
+16 GiB) striped over 2 pinned host regions (weight 4 each) and 4 HBM staging
+regions standing in for SSDs (weight 1 each), gathered into a fragmented
+10240-slot paged cache.  Inputs are resident (pool filled by kv_pool_store)
+before the timed region starts.
+
+Prints one JSON line: retrieved GB/s (value), ms per retrieve, the two
+kernels' durations from HIP events recorded on the streams they run on, the
+measured copy peaks (HBM copy kernel / hipMemcpy D2D; host->GPU zero-copy
+kernel / hipMemcpy H2D) from the same process, and the CPU oracle timed on
+a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PCIE5_X16_GBPS = 64.0       # published per-direction rate of the MI355X host link (PCIe 5.0 x16)
+HBM_PEAK_GBPS = 8000.0      # published MI355X HBM3E bandwidth
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _events_ms(torch, fn, iters=3):
+    """Best and list of per-iteration ms of fn() on the current stream."""
+    out = []
+    for _ in range(iters):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn()
+        e.record()
+        e.synchronize()
+        out.append(s.elapsed_time(e))
+    return out
+
+
+def probes(torch, K, run, nbytes):
+    """Copy peaks in GB/s (1e9 B/s of copied bytes), measured on this GPU in this process."""
+    res = {}
+    cur = torch.cuda.current_stream()
+    a = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    best_k, best_grid = 0.0, 0
+    for grid in (1024, 2048, 4096, 8192):
+        ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(b.data_ptr(), a.data_ptr(), nbytes, grid, 0,
+                                                               cur.cuda_stream)))
+        gbps = nbytes / ms / 1e6
+        if gbps > best_k:
+            best_k, best_grid = gbps, grid
+    ms = min(_events_ms(torch, lambda: K.probe_memcpy(b.data_ptr(), a.data_ptr(), nbytes, cur.cuda_stream)))
+    res["hbm_copy_kernel_gbps"] = round(best_k, 1)
+    res["hbm_copy_kernel_grid"] = best_grid
+    res["hbm_memcpy_d2d_gbps"] = round(nbytes / ms / 1e6, 1)
+    res["hbm_copy_peak_gbps"] = max(res["hbm_copy_kernel_gbps"], res["hbm_memcpy_d2d_gbps"])
+    # host link: read from each pinned host region of the pool into HBM
+    link = []
+    for r in range(run.pool.n_regions):
+        info = run.pool.region_info(r)
+        if info["type"] != K.REGION_HOST:
+            continue
+        n = min(nbytes, info["capacity_bytes"]) // 4096 * 4096
+        src = info["device_ptr"]
+        best, bgrid = 0.0, 0
+        for grid in (32, 64, 128, 256, 512):
+            ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(b.data_ptr(), src, n, grid, 0, cur.cuda_stream),
+                                iters=2))
+            if n / ms / 1e6 > best:
+                best, bgrid = n / ms / 1e6, grid
+        ms = min(_events_ms(torch, lambda: K.probe_memcpy(b.data_ptr(), info["host_ptr"], n, cur.cuda_stream),
+                            iters=2))
+        link.append({"region": r, "numa_node": info["numa_node_actual"], "kernel_gbps": round(best, 2),
+                     "kernel_grid": bgrid, "memcpy_h2d_gbps": round(n / ms / 1e6, 2)})
+    res["host_link"] = link
+    res["host_link_peak_gbps"] = max([max(x["kernel_gbps"], x["memcpy_h2d_gbps"]) for x in link] or [0.0])
+    del a, b
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(run, wl, budget_s=12.0, max_blocks=1024):
+    """The oracle's gather (memcpy per chunk, one thread) on a bounded sample of the same request."""
+    import numpy as np
+    import oracle
+    sh = wl.shape
+    q = wl.requests[0]
+    m = run.maps[q.request_id]
+    n = min(max_blocks, q.n_present)
+    sample = m[:n].copy()
+    # host regions are read where they are (pinned host memory); staging regions
+    # (HBM) are mirrored to host memory for the sampled blocks only
+    mem = []
+    for r in range(len(wl.regions)):
+        info = run.pool.region_info(r)
+        if info["type"] == 0:
+            mem.append(info["host_ptr"])
+        else:
+            mem.append(None)
+    mirrors = []
+    for i in range(n):
+        r = int(sample["region"][i])
+        if mem[r] is None:
+            buf = run.pool.region_read(r, int(sample["offset"][i]), sh.block_bytes)
+            mirrors.append(buf)
+            sample["region"][i] = len(wl.regions) + len(mirrors) - 1
+            sample["offset"][i] = 0
+    regions = [m_ if m_ is not None else 0 for m_ in mem] + [b.ctypes.data for b in mirrors]
+    L = sh.layers
+    dst = np.zeros((L, 2, n, sh.kv_heads, sh.block_size, sh.head_dim), np.uint16)
+    slots = np.arange(n, dtype=np.int32)          # destination slots renumbered 0..n-1
+    shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
+    oracle.gather(sample, slots, regions, [dst[l, 0] for l in range(L)], [dst[l, 1] for l in range(L)],
+                  shape, wl.layout)                # warm: touch the destination pages
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        oracle.gather(sample, slots, regions, [dst[l, 0] for l in range(L)], [dst[l, 1] for l in range(L)],
+                      shape, wl.layout)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or passes >= 40:
+            break
+    gbps = passes * n * sh.block_bytes / el / 1e9
+    return {"value": round(gbps, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d blocks (%.2f GiB; %d host-region, %d staging blocks mirrored to host), "
+                      "destination slots renumbered, %d passes in %.1f s" % (
+                          n, q.n_present, n * sh.block_bytes / 2**30, n - len(mirrors), len(mirrors), passes, el),
+            "ms_per_request_extrapolated": round(q.n_present * sh.block_bytes / (gbps * 1e9) * 1e3, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, help="workload 1..5 (3: the 128K LLaMA-shaped request)")
+    ap.add_argument("--probe-gib", type=float, default=4.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probes", action="store_true")
+    ap.add_argument("--host-grid", type=int, default=0)
+    ap.add_argument("--staging-grid", type=int, default=0)
+    ap.add_argument("--host-flags", type=int, default=0)
+    ap.add_argument("--staging-flags", type=int, default=0)
+    ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "
+              "--gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = workloads.make(args.config)
+    sh = wl.shape
+    log("workload", wl.name, "retrieved bytes", wl.retrieved_bytes)
+    t = time.perf_counter()
+    run = WorkloadRun(wl, device=0, coherence=args.coherence)
+    t_create = time.perf_counter() - t
+    run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
+    run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
+    log("pool created in %.1f s" % t_create)
+    t = time.perf_counter()
+    run.fill_source()
+    run.fill_dst()
+    log("source filled in %.1f s" % (time.perf_counter() - t))
+    t = time.perf_counter()
+    run.place_all()
+    t_place = time.perf_counter() - t
+    run.pool.set_timing(True)
+    t = time.perf_counter()
+    run.store_all()
+    torch.cuda.synchronize()
+    store_wall = time.perf_counter() - t
+    store_t = run.pool.last_timing() if len(wl.requests) == 1 else None
+    log("placed in %.3f ms, stored in %.1f ms" % (t_place * 1e3, store_wall * 1e3))
+
+    host_blocks = sum(int(np.isin(run.maps[q.request_id]["region"],
+                                  [i for i, r in enumerate(wl.regions) if r.kind == "host"]).sum())
+                      for q in wl.requests)
+    stage_blocks = wl.present_blocks - host_blocks
+    host_bytes, stage_bytes = host_blocks * sh.block_bytes, stage_blocks * sh.block_bytes
+
+    cur = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        run.retrieve_all()
+        run.pool.last_timing()
+    torch.cuda.synchronize()
+
+    spans, host_ms, stage_ms = [], [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(cur)
+        run.retrieve_all()
+        e.record(cur)
+        tm = run.pool.last_timing()       # waits for this step's kernels
+        host_ms.append(tm["host_ms"])
+        stage_ms.append(tm["staging_ms"])
+        spans.append((s, e))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    span_ms = [s.elapsed_time(e) for s, e in spans]
+    ms_per_step = wall / args.steps * 1e3
+    gbps = wl.retrieved_bytes / (ms_per_step / 1e3) / 1e9
+    run.pool.set_timing(False)
+
+    # staging-side gather alone (HBM->HBM), from a map without the host blocks
+    stage_only = None
+    if stage_blocks and len(wl.requests) == 1:
+        q = wl.requests[0]
+        m = run.retrieve_maps[q.request_id].copy()
+        host_idx = [i for i, r in enumerate(wl.regions) if r.kind == "host"]
+        m["region"][np.isin(m["region"], host_idx)] = K.ABSENT
+        kp, vp = run.layer_ptrs(run.dst)
+        run.pool.set_timing(True)
+        ks = []
+        for _ in range(args.warmup + args.steps):
+            run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
+            ks.append(run.pool.last_timing()["staging_ms"])
+        run.pool.set_timing(False)
+        ks = ks[args.warmup:]
+        stage_only = {"ms_median": round(statistics.median(ks), 3), "ms_min": round(min(ks), 3),
+                      "copied_gbps": round(stage_bytes / (statistics.median(ks) / 1e3) / 1e9, 1)}
+
+    pr = None if args.no_probes else probes(torch, K, run, int(args.probe_gib * 2**30) // 4096 * 4096)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(run, wl)
+
+    host_med = statistics.median(host_ms) if host_blocks else None
+    stage_med = statistics.median(stage_ms) if stage_blocks else None
+    dominant_ms = statistics.mean(host_ms) if host_blocks else statistics.mean(stage_ms)
+    if host_blocks:
+        achieved = host_bytes / (dominant_ms / 1e3) / 1e9
+        roof = {"bound": "pcie", "kernel": "chunk_copy_kernel (host-region class, zero-copy gather)",
+                "achieved": round(achieved, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PCIE5_X16_GBPS, 4), "traffic": None,
+                "bytes_per_launch": host_bytes,
+                "measured_peak": pr["host_link_peak_gbps"] if pr else None,
+                "frac_measured": round(achieved / pr["host_link_peak_gbps"], 4) if pr else None}
+    else:
+        achieved = 2 * stage_bytes / (dominant_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "kernel": "chunk_copy_kernel (staging class)", "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None}
+    hbm_roof = None
+    if stage_only:
+        a = 2 * stage_bytes / (stage_only["ms_median"] / 1e3) / 1e9      # bytes read + written in HBM
+        hbm_roof = {"bound": "hbm", "kernel": "chunk_copy_kernel (staging class, alone)", "achieved": round(a, 1),
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(a / HBM_PEAK_GBPS, 4),
+                    "copied_gbps": stage_only["copied_gbps"],
+                    "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
+                    "frac_measured": round(stage_only["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}
+
+    ideal_ms = None
+    if pr:
+        ideal_ms = max(host_bytes / (pr["host_link_peak_gbps"] * 1e9) if host_bytes else 0.0,
+                       stage_bytes / (pr["hbm_copy_peak_gbps"] * 1e9) if stage_bytes else 0.0) * 1e3
+    out = {
+        "metric": "retrieved KV GB/s into HBM + retrieval ms per 128K-token request, LLaMA-8B shape",
+        "value": round(gbps, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "context_tokens": sum(q.n_blocks for q in wl.requests) * sh.block_size,
+                   "blocks": wl.present_blocks, "block_bytes": sh.block_bytes,
+                   "retrieved_bytes": wl.retrieved_bytes, "host_link_bytes": host_bytes,
+                   "staging_bytes": stage_bytes,
+                   "regions": [(r.kind, r.weight) for r in wl.regions], "layout": "head-major chunks",
+                   "dst_slots": wl.dst_num_slots, "seed": wl.seed},
+        "retrieval_ms": {"call_to_complete": round(ms_per_step, 3),
+                         "span_median": round(statistics.median(span_ms), 3), "span_min": round(min(span_ms), 3),
+                         "host_kernel_median": round(host_med, 3) if host_med else None,
+                         "staging_kernel_median": round(stage_med, 3) if stage_med else None,
+                         "ideal_at_measured_peaks": round(ideal_ms, 3) if ideal_ms else None},
+        "roofline": roof,
+        "roofline_staging": hbm_roof,
+        "probes": pr,
+        "place_ms": round(t_place * 1e3, 3),
+        "store_ms": round(store_wall * 1e3, 1),
+        "store_kernels_ms": store_t,
+        "cpu_baseline": cpu,
+        "launch": {"host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,
+                   "host_flags": args.host_flags, "staging_flags": args.staging_flags,
+                   "coherence": args.coherence},
+    }
+    print(json.dumps(out), flush=True)
+    run.close()
+
+
+if __name__ == "__main__":
+    main()

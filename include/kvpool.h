@@ -1,0 +1,270 @@
+/*
+ * kvpool.h -- C ABI of the MI355X (gfx950) KV-pool retrieval library.
+ *
+ * The library implements the data path of "Unified KV Pooling to Accelerate
+ * Long-Context LLM Serving": a request's offloaded KV blocks are spread over
+ * several pool regions in proportion to each region's bandwidth (Sec. 4.1.2,
+ * Eq. 1; Sec. 4.1.3, Eq. 2 and Algorithm 1), recorded in a global lookup
+ * table (Sec. 4.1.1, Table "Fields of the GLT"), and gathered back into the
+ * GPU's paged KV cache by looking the blocks up, grouping them by region and
+ * reading all regions in parallel (Sec. 4.3, "KV Retrieval").
+ *
+ * Pool regions ("pool devices" in the paper) are either
+ *   - KVP_REGION_HOST: pinned host memory bound to a NUMA node and mapped
+ *     into the GPU's address space; GPU kernels read it directly over the
+ *     host link (zero copy), or
+ *   - KVP_REGION_STAGING: a buffer in HBM that stands in for an SSD.
+ *
+ * Conventions for every function
+ *   - Return 0 (KVP_OK) on success or a negative KVP_ERR_* code.  Nothing
+ *     throws across the ABI.  kv_pool_last_error() gives a message for the
+ *     calling thread's last failure.
+ *   - All arguments are checked before any GPU work is enqueued; a failed
+ *     call has no side effects.
+ *   - "stream" is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Host arrays passed in (maps, block tables, pointer tables) may be freed
+ *     as soon as the call returns: the library copies what it keeps.
+ *   - The pool owns its regions, internal streams, events, GLT and work-list
+ *     buffers.  The caller owns maps, block tables, the engine caches and
+ *     its streams.
+ *
+ * Engine cache layout (destination of retrieve, source of store): for every
+ * layer l there is one K and one V buffer in device memory, each laid out
+ * [num_slots][num_kv_heads][block_size][head_dim] of elem_bytes-sized
+ * elements; a "slot" is one block of block_size tokens.  Pointers must be
+ * 16-byte aligned.
+ *
+ * Pool block layout: a placed block occupies block_bytes = 2 * L * C bytes
+ * at (region, offset), C = num_kv_heads * block_size * head_dim * elem_bytes.
+ * Chunk (layer l, K=0/V=1) sits at offset + (2l + kv) * C.  Inside a chunk,
+ * pool_layout 0 stores [heads][tokens][head_dim] (head-major, the engine's
+ * order) and pool_layout 1 stores [tokens][heads][head_dim] (token-major);
+ * retrieve converts to the engine layout and store converts from it.
+ */
+#ifndef KVPOOL_H
+#define KVPOOL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ---- */
+#define KVP_OK            0
+#define KVP_ERR_INVALID  -1   /* bad argument, shape, pointer, index or state */
+#define KVP_ERR_NOMEM    -2   /* host or device allocation failed */
+#define KVP_ERR_NOSPACE  -3   /* a region has no contiguous range large enough */
+#define KVP_ERR_NOTFOUND -4   /* unknown request */
+#define KVP_ERR_STALE    -5   /* map entry refers to a released or reused range */
+#define KVP_ERR_HIP      -6   /* a HIP runtime call failed */
+
+/* ---- region types and flags ---- */
+#define KVP_REGION_HOST     0u  /* pinned, NUMA-bound, GPU-mapped host memory */
+#define KVP_REGION_STAGING  1u  /* HBM buffer standing in for an SSD */
+
+#define KVP_HOST_DEFAULT      0u  /* library's choice of host-memory coherence */
+#define KVP_HOST_COHERENT     1u  /* fine-grained (coherent) pinned memory */
+#define KVP_HOST_NONCOHERENT  2u  /* coarse-grained (non-coherent) pinned memory */
+
+#define KVP_ABSENT 0xFFFFFFFFu    /* kvp_loc.region of a block that is not in the pool */
+
+/* One pool region ("pool device", Sec. 4.1.1: each gets a unique index). */
+typedef struct {
+    uint32_t type;            /* KVP_REGION_HOST or KVP_REGION_STAGING */
+    int32_t  numa_node;       /* host: NUMA node whose memory backs it; -1 = no binding */
+    uint64_t capacity_bytes;  /* usable bytes, rounded down to a multiple of 4096 */
+    uint32_t flags;           /* host: KVP_HOST_*; staging: 0 */
+    uint32_t reserved;        /* 0 */
+} kvp_region_desc;
+
+/* Shape of the KV cache being pooled. */
+typedef struct {
+    uint32_t num_layers;      /* L >= 1 */
+    uint32_t num_kv_heads;    /* H >= 1 */
+    uint32_t head_dim;        /* D >= 1 */
+    uint32_t block_size;      /* tokens per block, >= 1 */
+    uint32_t elem_bytes;      /* bytes per element (2 for bf16) */
+    uint32_t pool_layout;     /* 0 head-major chunks, 1 token-major chunks */
+} kvp_kv_spec;
+
+/* Location of one block (the GLT's device_idx and location, Table "Fields of
+ * the GLT"; the location is a byte offset inside the region for both region
+ * types).  16 bytes. */
+typedef struct {
+    uint32_t region;          /* region index, or KVP_ABSENT */
+    uint32_t gen;             /* placement generation; detects stale maps */
+    uint64_t offset;          /* byte offset of the block inside the region */
+} kvp_loc;
+
+typedef struct kvp_pool kvp_pool;   /* opaque */
+
+/*
+ * Create a pool (Sec. 4.1.1: enumerate the pool devices, index them, and
+ * initialise the GLT; Sec. 4.1.2, Eq. 1: placement ratio p_i = b_i / sum b_j).
+ *   regions[n_regions]   region descriptions; region i gets index i.
+ *   bandwidths[n_regions] positive integer bandwidth weights b_i (any unit,
+ *                        e.g. MB/s).  Integers keep floor(p_i * n) exact.
+ *   spec                 KV shape; C = H*bs*D*elem_bytes must be a multiple
+ *                        of 16 (and, for pool_layout 1, so must D*elem_bytes).
+ *   hip_device           GPU ordinal.  -1 creates a placement-only pool: no
+ *                        memory is allocated and no HIP call is made; place,
+ *                        lookup and release work, store and retrieve return
+ *                        KVP_ERR_INVALID.
+ *   out                  receives the pool handle.
+ * Host regions are allocated with hipHostMalloc under an MPOL_BIND policy for
+ * numa_node, staging regions with hipMalloc.  Errors: INVALID (bad
+ * description or NUMA node not available), NOMEM, HIP.
+ */
+int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths,
+                   uint32_t n_regions, const kvp_kv_spec *spec, int hip_device,
+                   kvp_pool **out);
+
+/*
+ * Place the n_blocks blocks of one request (Algorithm 1 without the writes):
+ * target counts c_i = floor(p_i * n) + r_i (Eq. 2), the r leftovers one each
+ * to the regions with the largest p_i (ties: lower index); blocks taken in
+ * index order, block j to the region with room whose deficit
+ * (j+1)*c_i - n*a_i is largest (ties: lower index), a_i counting blocks
+ * already given to region i; each region's share is one contiguous range of
+ * ceil(c_i * block_bytes / 4096) sectors (Sec. 4.2), first fit in address
+ * order; block k of region i's share sits at base_i + k*block_bytes.  The
+ * GLT records every block (UpdateGLT).
+ *   map_out[n_blocks]    caller-owned, receives (region, gen, offset).
+ * Atomic: on KVP_ERR_NOSPACE nothing is placed.  Errors: INVALID (n_blocks
+ * == 0 or request already placed), NOSPACE.
+ */
+int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
+
+/*
+ * GLT read (Sec. 4.3: "look up their GLT entries"): the map of a placed
+ * request.  n_blocks must equal the placed count.  Errors: NOTFOUND, INVALID.
+ */
+int kv_pool_lookup(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
+
+/*
+ * Store (offload; Algorithm 1 store part, MemStore / SSD write): for every
+ * present entry b of map and every layer l, K and V, copy slot
+ * src_block_table[b] of the engine cache into the pool at
+ * map[b].offset + (2l+kv)*C of region map[b].region, in pool_layout order.
+ * Entries with region == KVP_ABSENT are skipped.
+ *   map[n_blocks], src_block_table[n_blocks]   host arrays.
+ *   src_num_slots        slots in each engine buffer; table entries of
+ *                        present blocks must lie in [0, src_num_slots).
+ *   k_layers[L], v_layers[L]  host arrays of device pointers.
+ *   stream               work is ordered on it; the call returns after
+ *                        enqueueing.  A later retrieve of these blocks on any
+ *                        stream waits for this store.
+ * Map entries must be blocks of live placements (else STALE) and distinct.
+ * Errors: INVALID, STALE, HIP.
+ */
+int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
+                  const int32_t *src_block_table, uint32_t src_num_slots,
+                  void *const *k_layers, void *const *v_layers, void *stream);
+
+/*
+ * Retrieve (Sec. 4.3, "KV Retrieval"): group the present entries by region
+ * type, then read the host regions (zero-copy kernel) and the staging
+ * regions (HBM gather kernel) in parallel on two internal streams forked
+ * from and joined back into `stream`; every chunk lands in slot
+ * dst_block_table[b] of layer l's K or V buffer in the engine layout.
+ * Absent entries are skipped and every slot not named by a present entry is
+ * left untouched.
+ *   map[n_blocks], dst_block_table[n_blocks]   host arrays; destination slots
+ *                        of present entries must be distinct and lie in
+ *                        [0, dst_num_slots).
+ *   k_layers[L], v_layers[L]  host arrays of device pointers.
+ * Stream ordered; returns after enqueueing.  Errors: INVALID, STALE, HIP.
+ */
+int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
+                     const int32_t *dst_block_table, uint32_t dst_num_slots,
+                     void *const *k_layers, void *const *v_layers, void *stream);
+
+/*
+ * Release a request: its ranges go back to the regions' free lists (merged
+ * with free neighbours) and its GLT entries are removed.  Waits for store /
+ * retrieve work already enqueued on this request to finish.  Maps of it
+ * become stale.  Errors: NOTFOUND.
+ */
+int kv_pool_release(kvp_pool *pool, uint64_t request_id);
+
+/* Destroy the pool: waits for its internal streams, frees everything.  NULL is a no-op. */
+void kv_pool_destroy(kvp_pool *pool);
+
+/* Message for the calling thread's last failed call ("" if none). */
+const char *kv_pool_last_error(void);
+
+/* ---- introspection ---- */
+
+typedef struct {
+    uint32_t type;            /* KVP_REGION_* */
+    int32_t  numa_node;       /* requested node (-1 none) */
+    int32_t  numa_node_actual;/* node backing the first page, -1 if unknown */
+    uint32_t flags;           /* KVP_HOST_* actually used */
+    uint64_t capacity_bytes;  /* usable bytes */
+    uint64_t bandwidth;       /* b_i */
+    void    *host_ptr;        /* host regions: CPU address; else NULL */
+    void    *device_ptr;      /* address GPU kernels use; NULL for placement-only pools */
+} kvp_region_info;
+
+/* Describe region `region`.  Errors: INVALID. */
+int kv_pool_region_info(const kvp_pool *pool, uint32_t region, kvp_region_info *out);
+
+/* Synchronous copy of bytes [offset, offset+bytes) of a region into host memory
+ * (diagnostics and tests).  Errors: INVALID, HIP. */
+int kv_pool_region_read(kvp_pool *pool, uint32_t region, uint64_t offset, uint64_t bytes,
+                        void *host_dst);
+
+/* The library's target counts (Eq. 2 with the remainder rule) for n blocks
+ * over n_regions bandwidths; host only.  Errors: INVALID. */
+int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, uint64_t *counts_out);
+
+/* ---- launch configuration and timing ---- */
+
+#define KVP_CLASS_HOST     0u   /* work on host regions (zero-copy kernel) */
+#define KVP_CLASS_STAGING  1u   /* work on staging regions (HBM kernel) */
+#define KVP_OP_RETRIEVE    0u
+#define KVP_OP_STORE       1u
+
+#define KVP_LAUNCH_NT_LOAD   1u  /* non-temporal loads */
+#define KVP_LAUNCH_NT_STORE  2u  /* non-temporal stores */
+#define KVP_LAUNCH_LDS       4u  /* pool_layout 1: stage each chunk through LDS */
+
+/* Set the grid (workgroups of 256 threads; 0 = library default) and flags
+ * of one (class, op) kernel.  Errors: INVALID. */
+int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
+
+typedef struct {
+    float    host_ms;         /* duration of the host-class kernel, -1 if none ran */
+    float    staging_ms;      /* duration of the staging-class kernel, -1 if none ran */
+    uint32_t host_blocks;     /* blocks read from / written to host regions */
+    uint32_t staging_blocks;  /* blocks read from / written to staging regions */
+} kvp_timing;
+
+/* Enable (1) or disable (0) HIP-event timing of the kernels store/retrieve
+ * launch.  Timing events are recorded on the internal stream each kernel
+ * runs on.  Errors: INVALID. */
+int kv_pool_set_timing(kvp_pool *pool, int enable);
+
+/* Durations of the kernels of the last timed store or retrieve; waits for
+ * them to finish.  Errors: INVALID (timing off or nothing timed), HIP. */
+int kv_pool_last_timing(kvp_pool *pool, kvp_timing *out);
+
+/* ---- bandwidth probes (the measured peaks that bound the two kernels) ---- */
+
+/* Streaming copy kernel: bytes from src to dst (device-visible addresses,
+ * 16-byte aligned, bytes a multiple of 16), `grid` workgroups of 256
+ * threads (0 = default), KVP_LAUNCH_NT_* flags, on `stream` of the current
+ * device.  Errors: INVALID, HIP. */
+int kv_probe_copy_kernel(void *dst, const void *src, uint64_t bytes, uint32_t grid,
+                         uint32_t flags, void *stream);
+
+/* hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, stream): the copy
+ * engines' rate over the same buffers.  Errors: HIP. */
+int kv_probe_memcpy(void *dst, const void *src, uint64_t bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVPOOL_H */

@@ -50,6 +50,10 @@ def _load():
             lib.kvgen_fill_cache.restype = ctypes.c_int
             lib.kvgen_fill_cache.argtypes = [u64, u64, u32, vp, vp, u32, u32, u32, u32,
                                              vp, vp, u32]
+            lib.kvgen_normal_table.restype = None
+            lib.kvgen_normal_table.argtypes = [vp]
+            lib.kvgen_ppnd16.restype = ctypes.c_double
+            lib.kvgen_ppnd16.argtypes = [ctypes.c_double]
             lib.kvgen_fill_u16.restype = None
             lib.kvgen_fill_u16.argtypes = [vp, u64, ctypes.c_uint16, u32]
             _lib = lib
@@ -76,6 +80,18 @@ def subseed(seed: int, tag: str) -> int:
     for ch in tag.encode():
         h = sm64(h ^ ch)
     return h
+
+
+def normal_table() -> np.ndarray:
+    """The 65536-entry bf16 table Q[i] = bf16(Phi^-1((i + 0.5) / 65536)) the values come from."""
+    out = np.empty(65536, dtype=np.uint16)
+    _load().kvgen_normal_table(out.ctypes.data)
+    return out
+
+
+def ppnd16(p: float) -> float:
+    """Standard normal quantile (Wichura AS 241) as used to build the table."""
+    return float(_load().kvgen_ppnd16(p))
 
 
 def block_values(seed: int, request: int, block: int, L: int, H: int, bs: int, D: int) -> np.ndarray:

@@ -12,18 +12,17 @@
  * Definition (counter based, no generator state):
  *   key(seed, q, b)   = sm64(sm64(sm64(seed) ^ q) ^ b)
  *   element index e   = ((((l*2 + kv)*H + h)*bs + t)*D + d)
- *   pair m = e / 2,   r = sm64(key ^ m)
- *   u1 = ((r >> 40) + 1) / 2^24        in (0, 1]
- *   u2 = ((r >> 16) & 0xFFFFFF) / 2^24 in [0, 1)
- *   Box-Muller (Box & Muller, 1958), in float:
- *     rad = sqrtf(-2 logf(u1));  z0 = rad cosf(2 pi u2);  z1 = rad sinf(2 pi u2)
- *   element 2m takes z0, element 2m+1 takes z1, each rounded to bf16 with
- *   round-to-nearest-even.
+ *   r = sm64(key ^ (e / 4)),  u = bits [16*(e%4), 16*(e%4)+16) of r
+ *   value = Q[u],  Q[i] = bf16_rne( Phi^-1( (i + 0.5) / 65536 ) )
+ * i.e. a standard normal sampled by inversion on a 16-bit uniform grid (the
+ * tails beyond about 4.3 sigma are cut, which is invisible at bf16
+ * resolution for this purpose).  Phi^-1 is Wichura's algorithm AS 241
+ * (PPND16, Applied Statistics 37, 1988), accurate to about 1e-16 in double.
  * sm64 is the splitmix64 output function (Steele, Lea & Flood, "Fast
  * splittable pseudorandom number generators", OOPSLA 2014).
  *
- * The values are generated once on the host; both the GPU path and the oracle
- * read those same bytes, so no bit of the comparison depends on a GPU libm.
+ * The values are generated on the host; both the GPU path and the oracle read
+ * those same bytes.
  */
 #include <math.h>
 #include <pthread.h>
@@ -38,15 +37,72 @@ static inline uint64_t sm64(uint64_t x)
     return x ^ (x >> 31);
 }
 
-static inline uint16_t f32_to_bf16_rne(float f)
+static uint16_t f64_to_bf16_rne(double v)
 {
+    /* Nearest bf16 to a double (ties to even), without double rounding:
+     * the two bf16 neighbours of the nearest float bracket v, and the
+     * distances to them are compared exactly in double. */
+    float f = (float)v;
     uint32_t u;
     memcpy(&u, &f, 4);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) /* NaN: keep quiet */
-        return (uint16_t)((u >> 16) | 0x0040u);
-    uint32_t lsb = (u >> 16) & 1u;
-    u += 0x7FFFu + lsb;
-    return (uint16_t)(u >> 16);
+    uint32_t lo = u & 0xFFFF0000u, hi = lo + 0x10000u;
+    float flo, fhi;
+    memcpy(&flo, &lo, 4);
+    memcpy(&fhi, &hi, 4);
+    double dlo = fabs(v - (double)flo), dhi = fabs((double)fhi - v);
+    if (dlo < dhi) return (uint16_t)(lo >> 16);
+    if (dhi < dlo) return (uint16_t)(hi >> 16);
+    return (uint16_t)(((lo >> 16) & 1u) ? (hi >> 16) : (lo >> 16)); /* tie: even */
+}
+
+/* Wichura AS 241 PPND16: the p-quantile of the standard normal. */
+double kvgen_ppnd16(double p)
+{
+    const double q = p - 0.5;
+    if (fabs(q) <= 0.425) {
+        const double r = 0.180625 - q * q;
+        return q * (((((((2509.0809287301226727 * r + 33430.575583588128105) * r + 67265.770927008700853) * r +
+                        45921.953931549871457) * r + 13731.693765509461125) * r + 1971.5909503065514427) * r +
+                     133.14166789178437745) * r + 3.387132872796366608) /
+               (((((((5226.495278852545925 * r + 28729.085735721942674) * r + 39307.89580009271061) * r +
+                    21213.794301586595867) * r + 5394.1960214247511077) * r + 687.1870074920579083) * r +
+                 42.313330701600911252) * r + 1.0);
+    }
+    double r = q < 0 ? p : 1.0 - p;
+    r = sqrt(-log(r));
+    double val;
+    if (r <= 5.0) {
+        r -= 1.6;
+        val = (((((((7.7454501427834140764e-4 * r + 0.0227238449892691845833) * r + 0.24178072517745061177) * r +
+                   1.27045825245236838258) * r + 3.64784832476320460504) * r + 5.7694972214606914055) * r +
+                4.6303378461565452959) * r + 1.42343711074968357734) /
+              (((((((1.05075007164441684324e-9 * r + 5.475938084995344946e-4) * r + 0.0151986665636164571966) * r +
+                   0.14810397642748007459) * r + 0.68976733498510000455) * r + 1.6763848301838038494) * r +
+                2.05319162663775882187) * r + 1.0);
+    } else {
+        r -= 5.0;
+        val = (((((((2.01033439929228813265e-7 * r + 2.71155556874348757815e-5) * r + 0.0012426609473880784386) * r +
+                   0.026532189526576123093) * r + 0.29656057182850489123) * r + 1.7848265399172913358) * r +
+                5.4637849111641143699) * r + 6.6579046435011037772) /
+              (((((((2.04426310338993978564e-15 * r + 1.4215117583164458887e-7) * r + 1.8463183175100546818e-5) * r +
+                   7.868691311456132591e-4) * r + 0.0148753612908506148525) * r + 0.13692988092273580531) * r +
+                0.59983220655588793769) * r + 1.0);
+    }
+    return q < 0 ? -val : val;
+}
+
+static uint16_t g_table[65536];
+static pthread_once_t g_once = PTHREAD_ONCE_INIT;
+
+static void build_table(void)
+{
+    for (int i = 0; i < 65536; ++i) g_table[i] = f64_to_bf16_rne(kvgen_ppnd16((i + 0.5) / 65536.0));
+}
+
+void kvgen_normal_table(uint16_t *out)
+{
+    pthread_once(&g_once, build_table);
+    memcpy(out, g_table, sizeof(g_table));
 }
 
 uint64_t kvgen_block_key(uint64_t seed, uint64_t request, uint64_t block)
@@ -54,59 +110,47 @@ uint64_t kvgen_block_key(uint64_t seed, uint64_t request, uint64_t block)
     return sm64(sm64(sm64(seed) ^ request) ^ block);
 }
 
-/* Two N(0,1) bf16 values for pair m of a block key. */
-static inline void pair_values(uint64_t key, uint64_t m, uint16_t *v0, uint16_t *v1)
+/* Elements [e0, e0 + count) of block (seed, request, block) into out. */
+void kvgen_fill_elems(uint64_t seed, uint64_t request, uint64_t block, uint64_t e0, uint64_t count,
+                      uint16_t *out)
 {
-    uint64_t r = sm64(key ^ m);
-    float u1 = (float)((r >> 40) + 1) * (1.0f / 16777216.0f);
-    float u2 = (float)((r >> 16) & 0xFFFFFFull) * (1.0f / 16777216.0f);
-    float rad = sqrtf(-2.0f * logf(u1));
-    float ang = 6.28318530717958647692f * u2;
-    *v0 = f32_to_bf16_rne(rad * cosf(ang));
-    *v1 = f32_to_bf16_rne(rad * sinf(ang));
-}
-
-/*
- * Fill elements [e0, e0 + count) of block (seed, request, block) into out[0..count).
- * Elements are bf16 (uint16).  e0 may be odd.
- */
-void kvgen_fill_elems(uint64_t seed, uint64_t request, uint64_t block,
-                      uint64_t e0, uint64_t count, uint16_t *out)
-{
-    uint64_t key = kvgen_block_key(seed, request, block);
-    uint64_t e = e0, end = e0 + count;
-    uint16_t a, b;
-    if (e < end && (e & 1)) {
-        pair_values(key, e >> 1, &a, &b);
-        *out++ = b;
-        e++;
+    pthread_once(&g_once, build_table);
+    const uint64_t key = kvgen_block_key(seed, request, block);
+    uint64_t e = e0;
+    const uint64_t end = e0 + count;
+    while (e < end && (e & 3)) {
+        const uint64_t r = sm64(key ^ (e >> 2));
+        *out++ = g_table[(r >> (16 * (e & 3))) & 0xFFFF];
+        ++e;
     }
-    for (; e + 1 < end; e += 2) {
-        pair_values(key, e >> 1, &a, &b);
-        out[0] = a;
-        out[1] = b;
-        out += 2;
+    for (; e + 4 <= end; e += 4) {
+        const uint64_t r = sm64(key ^ (e >> 2));
+        out[0] = g_table[r & 0xFFFF];
+        out[1] = g_table[(r >> 16) & 0xFFFF];
+        out[2] = g_table[(r >> 32) & 0xFFFF];
+        out[3] = g_table[r >> 48];
+        out += 4;
     }
-    if (e < end) {
-        pair_values(key, e >> 1, &a, &b);
-        *out = a;
+    for (; e < end; ++e) {
+        const uint64_t r = sm64(key ^ (e >> 2));
+        *out++ = g_table[(r >> (16 * (e & 3))) & 0xFFFF];
     }
 }
 
 /*
- * Fill the engine-layout source cache for n_blocks logical blocks of one
- * request.  Layout per layer and per K/V: [num_slots][H][bs][D] of
- * elem_bytes == 2 elements; block b goes to slot slot_of_block[b].
- * k_layers[l] / v_layers[l] are host pointers.  Work is split over n_threads
- * POSIX threads by block.
+ * Fill the engine-layout source cache for n_blocks blocks of one request.
+ * Layout per layer and per K/V: [num_slots][H][bs][D] of 2-byte elements;
+ * block block_ids[b] (logical block index) goes to slot slot_of_block[b].
+ * k_layers[l] / v_layers[l] are host pointers.  Work is split over
+ * n_threads POSIX threads by block.
  */
 typedef struct {
     uint64_t seed, request;
     uint32_t L, H, bs, D;
+    const uint64_t *block_ids;
     const int32_t *slot_of_block;
     uint16_t *const *k_layers;
     uint16_t *const *v_layers;
-    const uint64_t *block_ids;   /* logical block index used in the key (NULL = b) */
     uint32_t b_begin, b_end;
 } fill_job;
 
@@ -115,8 +159,8 @@ static void *fill_worker(void *arg)
     const fill_job *j = (const fill_job *)arg;
     const uint64_t chunk = (uint64_t)j->H * j->bs * j->D;
     for (uint32_t b = j->b_begin; b < j->b_end; ++b) {
-        uint64_t blk = j->block_ids ? j->block_ids[b] : b;
-        uint64_t slot = (uint64_t)j->slot_of_block[b];
+        const uint64_t blk = j->block_ids[b];
+        const uint64_t slot = (uint64_t)j->slot_of_block[b];
         for (uint32_t l = 0; l < j->L; ++l) {
             kvgen_fill_elems(j->seed, j->request, blk, (uint64_t)(2 * l) * chunk, chunk,
                              j->k_layers[l] + slot * chunk);
@@ -127,39 +171,42 @@ static void *fill_worker(void *arg)
     return 0;
 }
 
-int kvgen_fill_cache(uint64_t seed, uint64_t request, uint32_t n_blocks,
-                     const uint64_t *block_ids, const int32_t *slot_of_block,
-                     uint32_t L, uint32_t H, uint32_t bs, uint32_t D,
-                     uint16_t *const *k_layers, uint16_t *const *v_layers,
-                     uint32_t n_threads)
+int kvgen_fill_cache(uint64_t seed, uint64_t request, uint32_t n_blocks, const uint64_t *block_ids,
+                     const int32_t *slot_of_block, uint32_t L, uint32_t H, uint32_t bs, uint32_t D,
+                     uint16_t *const *k_layers, uint16_t *const *v_layers, uint32_t n_threads)
 {
+    pthread_once(&g_once, build_table);
     if (n_threads < 1) n_threads = 1;
     if (n_threads > 256) n_threads = 256;
-    if (n_threads > n_blocks) n_threads = n_blocks ? n_blocks : 1;
+    if (n_blocks && n_threads > n_blocks) n_threads = n_blocks;
     pthread_t tid[256];
     fill_job jobs[256];
     uint32_t per = n_blocks / n_threads, extra = n_blocks % n_threads, at = 0;
     for (uint32_t i = 0; i < n_threads; ++i) {
         uint32_t take = per + (i < extra ? 1u : 0u);
-        fill_job j = {seed, request, L, H, bs, D, slot_of_block, k_layers, v_layers,
-                      block_ids, at, at + take};
+        fill_job j = {seed, request, L, H, bs, D, block_ids, slot_of_block, k_layers, v_layers, at, at + take};
         jobs[i] = j;
         at += take;
     }
-    uint32_t started = 0;
-    for (uint32_t i = 1; i < n_threads; ++i) {
-        if (pthread_create(&tid[i], 0, fill_worker, &jobs[i]) != 0) break;
-        started = i;
-    }
+    char started[256] = {0};
+    for (uint32_t i = 1; i < n_threads; ++i) started[i] = pthread_create(&tid[i], 0, fill_worker, &jobs[i]) == 0;
     fill_worker(&jobs[0]);
-    for (uint32_t i = 1; i <= started; ++i) pthread_join(tid[i], 0);
-    /* any thread that failed to start: run its share here */
-    for (uint32_t i = started + 1; i < n_threads; ++i) fill_worker(&jobs[i]);
+    for (uint32_t i = 1; i < n_threads; ++i) {
+        if (started[i])
+            pthread_join(tid[i], 0);
+        else
+            fill_worker(&jobs[i]);
+    }
     return 0;
 }
 
 /* Fill a host buffer with a repeated 16-bit pattern using n_threads threads. */
-typedef struct { uint16_t *p; uint64_t n; uint16_t v; } pat_job;
+typedef struct {
+    uint16_t *p;
+    uint64_t n;
+    uint16_t v;
+} pat_job;
+
 static void *pat_worker(void *arg)
 {
     pat_job *j = (pat_job *)arg;
@@ -179,14 +226,15 @@ void kvgen_fill_u16(uint16_t *p, uint64_t n, uint16_t v, uint32_t n_threads)
         jobs[i].n = (i == n_threads - 1) ? n - per * i : per;
         jobs[i].v = v;
     }
-    uint32_t started = 0;
-    for (uint32_t i = 1; i < n_threads; ++i) {
-        if (pthread_create(&tid[i], 0, pat_worker, &jobs[i]) != 0) break;
-        started = i;
-    }
+    char started[256] = {0};
+    for (uint32_t i = 1; i < n_threads; ++i) started[i] = pthread_create(&tid[i], 0, pat_worker, &jobs[i]) == 0;
     pat_worker(&jobs[0]);
-    for (uint32_t i = 1; i <= started; ++i) pthread_join(tid[i], 0);
-    for (uint32_t i = started + 1; i < n_threads; ++i) pat_worker(&jobs[i]);
+    for (uint32_t i = 1; i < n_threads; ++i) {
+        if (started[i])
+            pthread_join(tid[i], 0);
+        else
+            pat_worker(&jobs[i]);
+    }
 }
 
 uint64_t kvgen_sm64(uint64_t x) { return sm64(x); }

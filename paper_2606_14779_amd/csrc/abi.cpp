@@ -1,0 +1,174 @@
+// extern "C" entry points: argument checks, error codes and the thread-local
+// error message.  No C++ exception crosses this boundary.
+
+#include <new>
+#include <string>
+
+#include "internal.hpp"
+
+namespace kvp {
+Pool *pool_create(const kvp_region_desc *, const uint64_t *, uint32_t, const kvp_kv_spec *, int);
+void pool_destroy(Pool *);
+void pool_place(Pool &, uint64_t, uint32_t, kvp_loc *);
+void pool_lookup(Pool &, uint64_t, uint32_t, kvp_loc *);
+void pool_release(Pool &, uint64_t);
+void pool_transfer(Pool &, const kvp_loc *, uint32_t, const int32_t *, uint32_t, void *const *, void *const *,
+                   void *, bool);
+void pool_region_info(const Pool &, uint32_t, kvp_region_info *);
+void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
+void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
+void pool_set_timing(Pool &, int);
+void pool_last_timing(Pool &, kvp_timing *);
+}  // namespace kvp
+
+struct kvp_pool {
+    kvp::Pool *impl;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+template <class F>
+int guarded(F &&f)
+{
+    try {
+        f();
+        g_last_error.clear();
+        return KVP_OK;
+    } catch (const kvp::Error &e) {
+        g_last_error = e.msg;
+        return e.code;
+    } catch (const std::bad_alloc &) {
+        g_last_error = "host allocation failed";
+        return KVP_ERR_NOMEM;
+    } catch (const std::exception &e) {
+        g_last_error = e.what();
+        return KVP_ERR_INVALID;
+    } catch (...) {
+        g_last_error = "unknown error";
+        return KVP_ERR_INVALID;
+    }
+}
+
+kvp::Pool &impl(kvp_pool *p)
+{
+    if (!p || !p->impl) kvp::fail(KVP_ERR_INVALID, "null pool");
+    return *p->impl;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, uint32_t n_regions,
+                   const kvp_kv_spec *spec, int hip_device, kvp_pool **out)
+{
+    return guarded([&] {
+        if (!out) kvp::fail(KVP_ERR_INVALID, "out is null");
+        *out = nullptr;
+        kvp::Pool *p = kvp::pool_create(regions, bandwidths, n_regions, spec, hip_device);
+        *out = new kvp_pool{p};
+    });
+}
+
+int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out)
+{
+    return guarded([&] { kvp::pool_place(impl(pool), request_id, n_blocks, map_out); });
+}
+
+int kv_pool_lookup(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out)
+{
+    return guarded([&] { kvp::pool_lookup(impl(pool), request_id, n_blocks, map_out); });
+}
+
+int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, const int32_t *src_block_table,
+                  uint32_t src_num_slots, void *const *k_layers, void *const *v_layers, void *stream)
+{
+    return guarded([&] {
+        kvp::pool_transfer(impl(pool), map, n_blocks, src_block_table, src_num_slots, k_layers, v_layers, stream,
+                           false);
+    });
+}
+
+int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, const int32_t *dst_block_table,
+                     uint32_t dst_num_slots, void *const *k_layers, void *const *v_layers, void *stream)
+{
+    return guarded([&] {
+        kvp::pool_transfer(impl(pool), map, n_blocks, dst_block_table, dst_num_slots, k_layers, v_layers, stream,
+                           true);
+    });
+}
+
+int kv_pool_release(kvp_pool *pool, uint64_t request_id)
+{
+    return guarded([&] { kvp::pool_release(impl(pool), request_id); });
+}
+
+void kv_pool_destroy(kvp_pool *pool)
+{
+    if (!pool) return;
+    (void)guarded([&] { kvp::pool_destroy(pool->impl); });
+    delete pool;
+}
+
+const char *kv_pool_last_error(void) { return g_last_error.c_str(); }
+
+int kv_pool_region_info(const kvp_pool *pool, uint32_t region, kvp_region_info *out)
+{
+    return guarded([&] {
+        if (!pool || !pool->impl) kvp::fail(KVP_ERR_INVALID, "null pool");
+        kvp::pool_region_info(*pool->impl, region, out);
+    });
+}
+
+int kv_pool_region_read(kvp_pool *pool, uint32_t region, uint64_t offset, uint64_t bytes, void *host_dst)
+{
+    return guarded([&] { kvp::pool_region_read(impl(pool), region, offset, bytes, host_dst); });
+}
+
+int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, uint64_t *counts_out)
+{
+    return guarded([&] {
+        if (!bandwidths || !counts_out) kvp::fail(KVP_ERR_INVALID, "null argument");
+        kvp::target_counts(bandwidths, n_regions, n, counts_out);
+    });
+}
+
+int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)
+{
+    return guarded([&] { kvp::pool_set_launch(impl(pool), cls, op, grid, flags); });
+}
+
+int kv_pool_set_timing(kvp_pool *pool, int enable)
+{
+    return guarded([&] { kvp::pool_set_timing(impl(pool), enable); });
+}
+
+int kv_pool_last_timing(kvp_pool *pool, kvp_timing *out)
+{
+    return guarded([&] { kvp::pool_last_timing(impl(pool), out); });
+}
+
+int kv_probe_copy_kernel(void *dst, const void *src, uint64_t bytes, uint32_t grid, uint32_t flags, void *stream)
+{
+    return guarded([&] {
+        if (!dst || !src) kvp::fail(KVP_ERR_INVALID, "null pointer");
+        if ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src) | bytes) & 15)
+            kvp::fail(KVP_ERR_INVALID, "pointers and size must be multiples of 16");
+        if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE)) kvp::fail(KVP_ERR_INVALID, "unknown flags");
+        if (grid > (1u << 20)) kvp::fail(KVP_ERR_INVALID, "grid too large");
+        kvp::check_hip(kvp::launch_probe_copy(dst, src, bytes, grid, flags, static_cast<hipStream_t>(stream)),
+                       "probe kernel launch");
+    });
+}
+
+int kv_probe_memcpy(void *dst, const void *src, uint64_t bytes, void *stream)
+{
+    return guarded([&] {
+        kvp::check_hip(hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, static_cast<hipStream_t>(stream)),
+                       "hipMemcpyAsync");
+    });
+}
+
+}  // extern "C"

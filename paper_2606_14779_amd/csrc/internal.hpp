@@ -1,0 +1,179 @@
+// Internal types of the KV-pool library (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "kvpool.h"
+
+namespace kvp {
+
+// ---------------------------------------------------------------- errors
+
+struct Error {
+    int code;
+    std::string msg;
+};
+
+[[noreturn]] void fail(int code, const std::string &msg);
+void check_hip(hipError_t e, const char *what);
+
+// ---------------------------------------------------------------- placement (Sec. 4.1.2-4.1.3)
+
+// Eq. (2) target counts with the remainder rule.  Throws INVALID on bad input.
+void target_counts(const uint64_t *bandwidth, uint32_t n_dev, uint64_t n_blocks, uint64_t *counts);
+
+// Algorithm 1 partition: region of every block, striped by largest deficit.
+void stripe(const std::vector<uint64_t> &counts, uint32_t n_blocks, std::vector<uint32_t> &region_of);
+
+// Address-ordered first-fit allocator of byte ranges with coalescing on free.
+class RangeAllocator {
+public:
+    explicit RangeAllocator(uint64_t capacity = 0);
+    bool first_fit(uint64_t len, uint64_t *start) const;
+    void take(uint64_t start, uint64_t len);
+    void give(uint64_t start, uint64_t len);
+    uint64_t largest() const;
+
+private:
+    std::map<uint64_t, uint64_t> free_;  // start -> length
+};
+
+// ---------------------------------------------------------------- GLT (Sec. 4.1.1)
+
+struct GltEntry {
+    uint64_t request;
+    uint32_t block;
+    uint32_t region;    // device_idx
+    uint32_t type;      // KVP_REGION_HOST (MEM) / KVP_REGION_STAGING (SSD stand-in)
+    uint32_t gen;
+    uint64_t offset;    // location
+};
+
+// Open-addressing hash table keyed by (request, block).
+class Glt {
+public:
+    Glt();
+    void insert(const GltEntry &e);
+    const GltEntry *find(uint64_t request, uint32_t block) const;
+    bool erase(uint64_t request, uint32_t block);
+    size_t size() const { return count_; }
+
+private:
+    static uint64_t hash(uint64_t request, uint32_t block);
+    void grow();
+    std::vector<GltEntry> slots_;
+    std::vector<uint8_t> used_;
+    size_t count_ = 0;
+};
+
+// ---------------------------------------------------------------- pool state
+
+struct RequestRec;
+
+struct Allocation {       // one contiguous range of one request in one region
+    RequestRec *owner;
+    uint32_t region;
+    uint32_t gen;
+    uint64_t base;
+    uint64_t blocks;      // blocks of the request stored in this range
+    uint64_t len;         // bytes reserved (sector-rounded)
+};
+
+struct RequestRec {
+    uint64_t id;
+    uint32_t n_blocks;
+    uint32_t gen;
+    std::vector<Allocation> ranges;
+    hipEvent_t stored = nullptr;   // recorded after each store touching the request
+    hipEvent_t busy = nullptr;     // recorded after each store / retrieve touching it
+    bool stored_rec = false;
+    bool busy_rec = false;
+};
+
+struct Region {
+    kvp_region_desc desc{};
+    uint64_t bandwidth = 0;
+    uint64_t capacity = 0;
+    void *host = nullptr;
+    void *dev = nullptr;
+    int numa_actual = -1;
+    uint32_t flags_used = 0;
+    RangeAllocator alloc;
+    std::map<uint64_t, Allocation *> live;   // base -> allocation
+};
+
+struct LaunchCfg {
+    uint32_t grid;
+    uint32_t flags;
+};
+
+struct Slot {                    // one work-list buffer of the upload ring
+    void *host = nullptr;        // pinned
+    void *dev = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;   // recorded on the caller stream after the call's kernels
+    bool pending = false;
+};
+
+struct Pool {
+    int device = -1;
+    bool placement_only = true;
+    kvp_kv_spec spec{};
+    uint64_t chunk_bytes = 0;
+    uint64_t block_bytes = 0;
+    std::vector<Region> regions;
+    std::vector<uint64_t> bandwidth;
+    std::unordered_map<uint64_t, std::unique_ptr<RequestRec>> requests;
+    Glt glt;
+    uint32_t next_gen = 1;
+    std::mutex mu;
+
+    hipStream_t s_host = nullptr, s_stage = nullptr;
+    hipEvent_t fork = nullptr, host_done = nullptr, stage_done = nullptr;
+    std::vector<Slot> ring;
+    uint32_t ring_next = 0;
+    LaunchCfg launch[2][2];      // [class][op]
+
+    bool timing = false;
+    bool timed_valid = false;
+    hipEvent_t t0[2] = {nullptr, nullptr}, t1[2] = {nullptr, nullptr};
+    uint32_t timed_blocks[2] = {0, 0};
+    bool timed_ran[2] = {false, false};
+};
+
+// ---------------------------------------------------------------- kernels (kernels.hip)
+
+struct CopyItem {          // 16 bytes, one block of work
+    uint64_t pool;         // device-visible address of the block in its region
+    uint32_t slot;         // engine-cache slot
+    uint32_t reserved;
+};
+
+struct CopyArgs {
+    const CopyItem *items;     // device
+    const uint64_t *cache;     // device, [2L]: base of layer l's K (2l) / V (2l+1)
+    uint32_t n_items;
+    uint32_t chunks;           // 2L
+    uint64_t chunk_bytes;      // C, multiple of 16
+    uint32_t heads;            // token-major conversion: H
+    uint32_t tokens;           //   bs
+    uint32_t row_vec;          //   D*elem_bytes/16
+    uint32_t layout;           // 0 head-major, 1 token-major
+};
+
+// gather: pool -> cache (retrieve); !gather: cache -> pool (store)
+hipError_t launch_chunk_copy(const CopyArgs &a, bool gather, uint32_t grid, uint32_t flags,
+                             hipStream_t s);
+hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid,
+                             uint32_t flags, hipStream_t s);
+uint32_t default_grid(uint32_t cls, uint32_t op);
+
+}  // namespace kvp

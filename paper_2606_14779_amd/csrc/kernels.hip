@@ -1,0 +1,279 @@
+// Data-movement kernels of the KV pool, for gfx950 (MI355X).
+//
+// Nothing here is a contraction, so there is no MFMA: every kernel is a bit
+// copy of 16-byte vectors.  One unit of work is one (block, layer, K/V)
+// chunk of C bytes.  A 256-thread workgroup (four 64-lane wavefronts) copies
+// a whole chunk per step; each lane holds up to UNROLL 16-byte loads in
+// flight before it stores, so a workgroup keeps 256*UNROLL*16 bytes in flight
+// (32 KiB at UNROLL = 8, one LLaMA-shaped chunk).  Loads and stores of a
+// wavefront cover 1 KiB of contiguous memory, which the memory system merges
+// into full 128-byte lines.
+//
+// The grid is persistent: workgroup g takes units g, g+G, g+2G, ...  Unit u
+// is chunk u % (2L) of work item u / (2L), so neighbouring workgroups read
+// neighbouring chunks of the same pool block (the pool side streams through
+// memory in address order).  There is no data reuse, so the round-robin
+// placement of workgroups on the 8 XCDs needs no remapping.
+//
+// Three copy forms:
+//   - head-major pool chunks: the chunk is [H][bs][D] on both sides; a plain
+//     contiguous copy (this moves the layer axis from inside the block to
+//     the per-layer engine buffers).
+//   - token-major pool chunks, direct: every 16-byte vector of a [bs][H][D]
+//     chunk maps to one vector of the [H][bs][D] chunk; both sides move in
+//     runs of D*elem_bytes bytes.
+//   - token-major pool chunks, LDS-staged: the chunk is read contiguously
+//     into LDS, then written contiguously in the other order, so both global
+//     sides are fully contiguous per workgroup.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "internal.hpp"
+
+namespace kvp {
+
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+// Every buffer the kernels touch is global memory (HBM or mapped host
+// memory); saying so lets the compiler emit global_* instead of flat_*
+// accesses, which do not occupy the LDS counter.
+typedef __attribute__((address_space(1))) v4u gv4u;
+
+constexpr uint32_t kThreads = 256;
+constexpr uint64_t kMaxLdsChunk = 64 * 1024;
+
+template <bool NT>
+__device__ __forceinline__ v4u load16(const v4u *p)
+{
+    const gv4u *g = (const gv4u *)p;
+    if constexpr (NT)
+        return __builtin_nontemporal_load(g);
+    else
+        return *g;
+}
+
+template <bool NT>
+__device__ __forceinline__ void store16(v4u *p, v4u v)
+{
+    gv4u *g = (gv4u *)p;
+    if constexpr (NT)
+        __builtin_nontemporal_store(v, g);
+    else
+        *g = v;
+}
+
+// Workgroup-cooperative contiguous copy of nvec 16-byte vectors.
+template <int UNROLL, bool NTL, bool NTS>
+__device__ __forceinline__ void wg_copy(const v4u *__restrict__ src, v4u *__restrict__ dst, uint32_t nvec)
+{
+    const uint32_t tid = threadIdx.x;
+    uint32_t base = 0;
+    for (; base + kThreads * UNROLL <= nvec; base += kThreads * UNROLL) {
+        v4u r[UNROLL];
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) r[i] = load16<NTL>(src + base + i * kThreads + tid);
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) store16<NTS>(dst + base + i * kThreads + tid, r[i]);
+    }
+    if (base < nvec) {  // ragged tail: one predicated batch
+        v4u r[UNROLL];
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = base + i * kThreads + tid;
+            if (v < nvec) r[i] = load16<NTL>(src + v);
+        }
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = base + i * kThreads + tid;
+            if (v < nvec) store16<NTS>(dst + v, r[i]);
+        }
+    }
+}
+
+// Vector index inside a token-major chunk [bs][H][rv] of the vector at
+// head-major index v of [H][bs][rv].
+__device__ __forceinline__ uint32_t hm_to_tm(uint32_t v, uint32_t heads, uint32_t tokens, uint32_t rv)
+{
+    const uint32_t row = v / rv, w = v - row * rv;
+    const uint32_t h = row / tokens, t = row - h * tokens;
+    return (t * heads + h) * rv + w;
+}
+
+// Direct token-major <-> head-major chunk conversion.  The lane index runs
+// over the destination, so stores are contiguous; loads come in runs of rv
+// vectors.  GATHER: src token-major (pool) -> dst head-major (cache).
+template <bool GATHER, int UNROLL, bool NTL, bool NTS>
+__device__ __forceinline__ void wg_convert(const v4u *__restrict__ src, v4u *__restrict__ dst, uint32_t nvec,
+                                           uint32_t heads, uint32_t tokens, uint32_t rv)
+{
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t base = 0; base < nvec; base += kThreads * UNROLL) {
+        v4u r[UNROLL];
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = base + i * kThreads + tid;
+            if (v < nvec) {
+                uint32_t s;
+                if constexpr (GATHER) {
+                    s = hm_to_tm(v, heads, tokens, rv);  // dst head-major v <- src token-major s
+                } else {
+                    // dst token-major v = (t*H + h)*rv + w <- src head-major (h*bs + t)*rv + w
+                    const uint32_t row = v / rv, w = v - row * rv;
+                    const uint32_t t = row / heads, h = row - t * heads;
+                    s = (h * tokens + t) * rv + w;
+                }
+                r[i] = load16<NTL>(src + s);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = base + i * kThreads + tid;
+            if (v < nvec) store16<NTS>(dst + v, r[i]);
+        }
+    }
+}
+
+// LDS-staged conversion: contiguous global read into LDS, contiguous global
+// write out of LDS in the other order.
+template <bool GATHER, bool NTL, bool NTS>
+__device__ __forceinline__ void wg_convert_lds(const v4u *__restrict__ src, v4u *__restrict__ dst, uint32_t nvec,
+                                               uint32_t heads, uint32_t tokens, uint32_t rv, v4u *lds)
+{
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t v = tid; v < nvec; v += kThreads) lds[v] = load16<NTL>(src + v);
+    __syncthreads();
+    for (uint32_t v = tid; v < nvec; v += kThreads) {
+        uint32_t s;
+        if constexpr (GATHER) {
+            s = hm_to_tm(v, heads, tokens, rv);
+        } else {
+            const uint32_t row = v / rv, w = v - row * rv;
+            const uint32_t t = row / heads, h = row - t * heads;
+            s = (h * tokens + t) * rv + w;
+        }
+        store16<NTS>(dst + v, lds[s]);
+    }
+    __syncthreads();  // LDS is reused by the next chunk
+}
+
+enum Form { kPlain = 0, kConvert = 1, kConvertLds = 2 };
+
+template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+__global__ __launch_bounds__(kThreads) void chunk_copy_kernel(CopyArgs a)
+{
+    extern __shared__ v4u lds[];
+    const uint32_t units = a.n_items * a.chunks;
+    const uint32_t nvec = static_cast<uint32_t>(a.chunk_bytes >> 4);
+    for (uint32_t u = blockIdx.x; u < units; u += gridDim.x) {
+        const uint32_t item = u / a.chunks;
+        const uint32_t c = u - item * a.chunks;
+        const CopyItem it = a.items[item];
+        char *pool = reinterpret_cast<char *>(it.pool) + static_cast<uint64_t>(c) * a.chunk_bytes;
+        char *cache = reinterpret_cast<char *>(a.cache[c]) + static_cast<uint64_t>(it.slot) * a.chunk_bytes;
+        const v4u *src = reinterpret_cast<const v4u *>(GATHER ? pool : cache);
+        v4u *dst = reinterpret_cast<v4u *>(GATHER ? cache : pool);
+        if constexpr (FORM == kPlain)
+            wg_copy<UNROLL, NTL, NTS>(src, dst, nvec);
+        else if constexpr (FORM == kConvert)
+            wg_convert<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec);
+        else
+            wg_convert_lds<GATHER, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec, lds);
+    }
+}
+
+// Contiguous streaming copy over tiles of 256*UNROLL vectors (bandwidth probe).
+template <int UNROLL, bool NTL, bool NTS>
+__global__ __launch_bounds__(kThreads) void probe_copy_kernel(const v4u *__restrict__ src, v4u *__restrict__ dst,
+                                                              uint64_t nvec)
+{
+    const uint64_t tile = static_cast<uint64_t>(kThreads) * UNROLL;
+    const uint64_t tiles = (nvec + tile - 1) / tile;
+    for (uint64_t t = blockIdx.x; t < tiles; t += gridDim.x) {
+        const uint64_t base = t * tile;
+        const uint64_t left = nvec - base;
+        wg_copy<UNROLL, NTL, NTS>(src + base, dst + base, static_cast<uint32_t>(left < tile ? left : tile));
+    }
+}
+
+// ---------------------------------------------------------------- host-side dispatch
+
+template <bool GATHER, int FORM, int UNROLL>
+static hipError_t launch_form(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
+{
+    const bool ntl = flags & KVP_LAUNCH_NT_LOAD, nts = flags & KVP_LAUNCH_NT_STORE;
+    dim3 g(grid), b(kThreads);
+    if (ntl && nts)
+        hipLaunchKernelGGL((chunk_copy_kernel<GATHER, FORM, UNROLL, true, true>), g, b, lds, s, a);
+    else if (ntl)
+        hipLaunchKernelGGL((chunk_copy_kernel<GATHER, FORM, UNROLL, true, false>), g, b, lds, s, a);
+    else if (nts)
+        hipLaunchKernelGGL((chunk_copy_kernel<GATHER, FORM, UNROLL, false, true>), g, b, lds, s, a);
+    else
+        hipLaunchKernelGGL((chunk_copy_kernel<GATHER, FORM, UNROLL, false, false>), g, b, lds, s, a);
+    return hipGetLastError();
+}
+
+template <bool GATHER, int FORM>
+static hipError_t launch_unroll(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
+{
+    // enough 16-byte loads in flight per lane to cover the whole chunk, up to 8
+    const uint64_t per_lane = (a.chunk_bytes / 16 + kThreads - 1) / kThreads;
+    if (per_lane >= 8) return launch_form<GATHER, FORM, 8>(a, grid, flags, lds, s);
+    if (per_lane >= 4) return launch_form<GATHER, FORM, 4>(a, grid, flags, lds, s);
+    if (per_lane >= 2) return launch_form<GATHER, FORM, 2>(a, grid, flags, lds, s);
+    return launch_form<GATHER, FORM, 1>(a, grid, flags, lds, s);
+}
+
+hipError_t launch_chunk_copy(const CopyArgs &a, bool gather, uint32_t grid, uint32_t flags, hipStream_t s)
+{
+    if (a.n_items == 0) return hipSuccess;
+    const uint64_t units = static_cast<uint64_t>(a.n_items) * a.chunks;
+    if (grid > units) grid = static_cast<uint32_t>(units);
+    if (grid == 0) grid = 1;
+    if (a.layout == 0) {
+        return gather ? launch_unroll<true, kPlain>(a, grid, flags, 0, s)
+                      : launch_unroll<false, kPlain>(a, grid, flags, 0, s);
+    }
+    if ((flags & KVP_LAUNCH_LDS) && a.chunk_bytes <= kMaxLdsChunk) {
+        const size_t lds = a.chunk_bytes;
+        return gather ? launch_form<true, kConvertLds, 1>(a, grid, flags, lds, s)
+                      : launch_form<false, kConvertLds, 1>(a, grid, flags, lds, s);
+    }
+    return gather ? launch_unroll<true, kConvert>(a, grid, flags, 0, s)
+                  : launch_unroll<false, kConvert>(a, grid, flags, 0, s);
+}
+
+hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid, uint32_t flags,
+                             hipStream_t s)
+{
+    const uint64_t nvec = bytes / 16;
+    if (nvec == 0) return hipSuccess;
+    const uint64_t tiles = (nvec + kThreads * 8 - 1) / (kThreads * 8);
+    if (grid == 0) grid = 2048;
+    if (grid > tiles) grid = static_cast<uint32_t>(tiles);
+    const bool ntl = flags & KVP_LAUNCH_NT_LOAD, nts = flags & KVP_LAUNCH_NT_STORE;
+    const v4u *sp = static_cast<const v4u *>(src);
+    v4u *dp = static_cast<v4u *>(dst);
+    dim3 g(grid), b(kThreads);
+    if (ntl && nts)
+        hipLaunchKernelGGL((probe_copy_kernel<8, true, true>), g, b, 0, s, sp, dp, nvec);
+    else if (ntl)
+        hipLaunchKernelGGL((probe_copy_kernel<8, true, false>), g, b, 0, s, sp, dp, nvec);
+    else if (nts)
+        hipLaunchKernelGGL((probe_copy_kernel<8, false, true>), g, b, 0, s, sp, dp, nvec);
+    else
+        hipLaunchKernelGGL((probe_copy_kernel<8, false, false>), g, b, 0, s, sp, dp, nvec);
+    return hipGetLastError();
+}
+
+uint32_t default_grid(uint32_t cls, uint32_t op)
+{
+    (void)op;
+    // host class: link bound, a modest number of workgroups keeps the link
+    // busy and leaves CUs to the staging kernel; staging class: fill all
+    // 256 CUs several times over.
+    return cls == KVP_CLASS_HOST ? 128u : 2048u;
+}
+
+}  // namespace kvp

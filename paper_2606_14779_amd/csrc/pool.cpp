@@ -1,0 +1,588 @@
+// KV pool engine: regions, placement bookkeeping, and the store / retrieve
+// enqueue path.
+//
+// Retrieval follows Sec. 4.3 of the paper: look every block up, group the
+// blocks by pool device, and read all devices in parallel.  Here the groups
+// are the two region classes -- pinned host regions, read by a zero-copy
+// kernel over the host link, and HBM staging regions, read by an HBM gather
+// kernel -- and "in parallel" means two internal HIP streams forked from the
+// caller's stream and joined back into it, so both kernels run at once and
+// the caller sees one stream-ordered operation.  The per-call work list (one
+// 16-byte item per block plus the 2L engine-buffer pointers) is written to a
+// pinned buffer and uploaded with one asynchronous copy; buffers come from a
+// small ring guarded by events, so a call only blocks when the ring wraps
+// onto work that is still running.
+
+#include <numaif.h>
+#include <sys/syscall.h>
+#include <unistd.h>
+
+#include <algorithm>
+#include <cerrno>
+#include <cstring>
+
+#include "internal.hpp"
+
+namespace kvp {
+
+void fail(int code, const std::string &msg) { throw Error{code, msg}; }
+
+void check_hip(hipError_t e, const char *what)
+{
+    if (e != hipSuccess) fail(KVP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+namespace {
+
+constexpr uint64_t kSector = 4096;
+constexpr uint32_t kRingSlots = 8;
+constexpr size_t kSlotMin = 64 * 1024;
+
+uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// Make `dev` the calling thread's device for the scope, then restore.
+class DeviceScope {
+public:
+    explicit DeviceScope(int dev)
+    {
+        if (dev < 0) return;
+        check_hip(hipGetDevice(&old_), "hipGetDevice");
+        if (old_ != dev) check_hip(hipSetDevice(dev), "hipSetDevice");
+        else old_ = -1;
+    }
+    ~DeviceScope()
+    {
+        if (old_ >= 0) (void)hipSetDevice(old_);
+    }
+
+private:
+    int old_ = -1;
+};
+
+// Bind the calling thread's memory policy to one NUMA node for the scope.
+class NumaScope {
+public:
+    explicit NumaScope(int node)
+    {
+        if (node < 0) return;
+        if (node >= kMaxNodes) fail(KVP_ERR_INVALID, "NUMA node " + std::to_string(node) + " out of range");
+        saved_ = syscall(SYS_get_mempolicy, &old_mode_, old_mask_, kMaxNodes + 1, nullptr, 0) == 0;
+        unsigned long mask[kWords] = {};
+        mask[node / 64] = 1ul << (node % 64);
+        if (syscall(SYS_set_mempolicy, MPOL_BIND, mask, kMaxNodes + 1) != 0)
+            fail(KVP_ERR_INVALID, "cannot bind memory to NUMA node " + std::to_string(node) + ": " +
+                                      std::strerror(errno));
+        active_ = true;
+    }
+    ~NumaScope()
+    {
+        if (!active_) return;
+        if (saved_ && old_mode_ != MPOL_DEFAULT)
+            syscall(SYS_set_mempolicy, old_mode_, old_mask_, kMaxNodes + 1);
+        else
+            syscall(SYS_set_mempolicy, MPOL_DEFAULT, nullptr, 0);
+    }
+
+private:
+    static constexpr int kMaxNodes = 1024;
+    static constexpr int kWords = kMaxNodes / 64;
+    bool active_ = false, saved_ = false;
+    int old_mode_ = MPOL_DEFAULT;
+    unsigned long old_mask_[kWords] = {};
+};
+
+int page_node(void *p)
+{
+    int node = -1;
+    if (syscall(SYS_get_mempolicy, &node, nullptr, 0, p, MPOL_F_NODE | MPOL_F_ADDR) != 0) return -1;
+    return node;
+}
+
+void alloc_region(Region &r)
+{
+    if (r.desc.type == KVP_REGION_HOST) {
+        unsigned flags = hipHostMallocMapped;
+        const uint32_t coh = r.desc.flags;
+        // Default: coarse-grained.  Nothing writes a region from the CPU while
+        // a kernel reads it, and coarse-grained pages may be cached on the GPU.
+        r.flags_used = coh == KVP_HOST_DEFAULT ? KVP_HOST_NONCOHERENT : coh;
+        flags |= r.flags_used == KVP_HOST_COHERENT ? hipHostMallocCoherent : hipHostMallocNonCoherent;
+        if (r.desc.numa_node >= 0) flags |= hipHostMallocNumaUser;
+        void *p = nullptr;
+        hipError_t e;
+        {
+            NumaScope bind(r.desc.numa_node);
+            e = hipHostMalloc(&p, r.capacity, flags);
+        }
+        if (e != hipSuccess || !p)
+            fail(KVP_ERR_NOMEM, "hipHostMalloc of " + std::to_string(r.capacity) + " bytes: " + hipGetErrorString(e));
+        r.host = p;
+        void *d = nullptr;
+        check_hip(hipHostGetDevicePointer(&d, p, 0), "hipHostGetDevicePointer");
+        r.dev = d;
+        r.numa_actual = page_node(p);
+    } else {
+        void *d = nullptr;
+        hipError_t e = hipMalloc(&d, r.capacity);
+        if (e != hipSuccess || !d)
+            fail(KVP_ERR_NOMEM, "hipMalloc of " + std::to_string(r.capacity) + " bytes: " + hipGetErrorString(e));
+        r.dev = d;
+    }
+}
+
+void free_slot(Slot &s)
+{
+    if (s.host) (void)hipHostFree(s.host);
+    if (s.dev) (void)hipFree(s.dev);
+    s.host = s.dev = nullptr;
+    s.cap = 0;
+}
+
+void release_gpu(Pool &p)
+{
+    if (p.placement_only) return;
+    if (p.s_host) (void)hipStreamSynchronize(p.s_host);
+    if (p.s_stage) (void)hipStreamSynchronize(p.s_stage);
+    for (auto &s : p.ring) {
+        if (s.pending && s.done) (void)hipEventSynchronize(s.done);
+        free_slot(s);
+        if (s.done) (void)hipEventDestroy(s.done);
+        s.done = nullptr;
+    }
+    for (auto &kv : p.requests) {
+        if (kv.second->busy_rec) (void)hipEventSynchronize(kv.second->busy);
+        if (kv.second->stored) (void)hipEventDestroy(kv.second->stored);
+        if (kv.second->busy) (void)hipEventDestroy(kv.second->busy);
+    }
+    hipEvent_t *evs[] = {&p.fork, &p.host_done, &p.stage_done, &p.t0[0], &p.t0[1], &p.t1[0], &p.t1[1]};
+    for (auto e : evs)
+        if (*e) (void)hipEventDestroy(*e), *e = nullptr;
+    if (p.s_host) (void)hipStreamDestroy(p.s_host);
+    if (p.s_stage) (void)hipStreamDestroy(p.s_stage);
+    p.s_host = p.s_stage = nullptr;
+    for (auto &r : p.regions) {
+        if (r.host) (void)hipHostFree(r.host);
+        else if (r.dev) (void)hipFree(r.dev);
+        r.host = r.dev = nullptr;
+    }
+}
+
+void check_spec(const kvp_kv_spec &s, uint64_t &chunk, uint64_t &block)
+{
+    if (s.num_layers == 0 || s.num_kv_heads == 0 || s.head_dim == 0 || s.block_size == 0 || s.elem_bytes == 0)
+        fail(KVP_ERR_INVALID, "kv spec has a zero dimension");
+    if (s.pool_layout > 1) fail(KVP_ERR_INVALID, "pool_layout must be 0 or 1");
+    const unsigned __int128 c = static_cast<unsigned __int128>(s.num_kv_heads) * s.block_size * s.head_dim * s.elem_bytes;
+    if (c % 16 != 0) fail(KVP_ERR_INVALID, "chunk bytes H*bs*D*elem_bytes must be a multiple of 16");
+    if (c >= (static_cast<unsigned __int128>(1) << 36)) fail(KVP_ERR_INVALID, "chunk too large");
+    if (s.pool_layout == 1 && (static_cast<uint64_t>(s.head_dim) * s.elem_bytes) % 16 != 0)
+        fail(KVP_ERR_INVALID, "token-major pool layout needs head_dim*elem_bytes to be a multiple of 16");
+    if (2ull * s.num_layers > (1u << 20)) fail(KVP_ERR_INVALID, "too many layers");
+    chunk = static_cast<uint64_t>(c);
+    block = 2ull * s.num_layers * chunk;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- create / destroy
+
+Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, uint32_t n_regions,
+                  const kvp_kv_spec *spec, int hip_device)
+{
+    if (!regions || !bandwidths || !spec) fail(KVP_ERR_INVALID, "null argument");
+    if (n_regions == 0 || n_regions > 4096) fail(KVP_ERR_INVALID, "n_regions must be in [1, 4096]");
+    if (hip_device < -1) fail(KVP_ERR_INVALID, "hip_device must be >= -1");
+    auto p = std::make_unique<Pool>();
+    p->spec = *spec;
+    check_spec(p->spec, p->chunk_bytes, p->block_bytes);
+    p->regions.resize(n_regions);
+    p->bandwidth.assign(bandwidths, bandwidths + n_regions);
+    for (uint32_t i = 0; i < n_regions; ++i) {
+        const kvp_region_desc &d = regions[i];
+        const std::string who = "region " + std::to_string(i) + ": ";
+        if (d.type != KVP_REGION_HOST && d.type != KVP_REGION_STAGING) fail(KVP_ERR_INVALID, who + "bad type");
+        if (bandwidths[i] == 0) fail(KVP_ERR_INVALID, who + "bandwidth must be positive");
+        if (d.capacity_bytes < kSector) fail(KVP_ERR_INVALID, who + "capacity below one 4096-byte sector");
+        if (d.numa_node < -1) fail(KVP_ERR_INVALID, who + "numa_node must be >= -1");
+        if (d.type == KVP_REGION_HOST && d.flags > KVP_HOST_NONCOHERENT) fail(KVP_ERR_INVALID, who + "bad flags");
+        if (d.type == KVP_REGION_STAGING && (d.flags != 0 || d.numa_node != -1))
+            fail(KVP_ERR_INVALID, who + "staging regions take no flags and no NUMA node");
+        if (d.reserved != 0) fail(KVP_ERR_INVALID, who + "reserved must be 0");
+        Region &r = p->regions[i];
+        r.desc = d;
+        r.bandwidth = bandwidths[i];
+        r.capacity = d.capacity_bytes / kSector * kSector;
+        r.alloc = RangeAllocator(r.capacity);
+    }
+    for (uint32_t c = 0; c < 2; ++c)
+        for (uint32_t o = 0; o < 2; ++o) p->launch[c][o] = LaunchCfg{default_grid(c, o), 0u};
+
+    p->device = hip_device;
+    p->placement_only = hip_device < 0;
+    if (p->placement_only) return p.release();
+
+    int n_dev = 0;
+    check_hip(hipGetDeviceCount(&n_dev), "hipGetDeviceCount");
+    if (hip_device >= n_dev) fail(KVP_ERR_INVALID, "hip_device " + std::to_string(hip_device) + " not present");
+    DeviceScope dev(hip_device);
+    try {
+        for (auto &r : p->regions) alloc_region(r);
+        check_hip(hipStreamCreateWithFlags(&p->s_host, hipStreamNonBlocking), "hipStreamCreate");
+        check_hip(hipStreamCreateWithFlags(&p->s_stage, hipStreamNonBlocking), "hipStreamCreate");
+        check_hip(hipEventCreateWithFlags(&p->fork, hipEventDisableTiming), "hipEventCreate");
+        check_hip(hipEventCreateWithFlags(&p->host_done, hipEventDisableTiming), "hipEventCreate");
+        check_hip(hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming), "hipEventCreate");
+        for (int c = 0; c < 2; ++c) {
+            check_hip(hipEventCreate(&p->t0[c]), "hipEventCreate");
+            check_hip(hipEventCreate(&p->t1[c]), "hipEventCreate");
+        }
+        p->ring.resize(kRingSlots);
+        for (auto &s : p->ring) check_hip(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreate");
+    } catch (...) {
+        release_gpu(*p);
+        throw;
+    }
+    return p.release();
+}
+
+void pool_destroy(Pool *p)
+{
+    if (!p) return;
+    {
+        std::lock_guard<std::mutex> lock(p->mu);
+        if (!p->placement_only) {
+            DeviceScope dev(p->device);
+            release_gpu(*p);
+        }
+    }
+    delete p;
+}
+
+// ---------------------------------------------------------------- place / lookup / release
+
+void pool_place(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
+{
+    if (n_blocks == 0) fail(KVP_ERR_INVALID, "n_blocks must be positive");
+    if (!out) fail(KVP_ERR_INVALID, "map_out is null");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (p.requests.count(request)) fail(KVP_ERR_INVALID, "request " + std::to_string(request) + " is already placed");
+    const uint32_t N = static_cast<uint32_t>(p.regions.size());
+    std::vector<uint64_t> counts(N);
+    target_counts(p.bandwidth.data(), N, n_blocks, counts.data());
+
+    // one contiguous, sector-rounded range per region with a nonzero share;
+    // find them all before taking any, so a failure changes nothing
+    std::vector<uint64_t> base(N, 0), len(N, 0);
+    for (uint32_t i = 0; i < N; ++i) {
+        len[i] = round_up(counts[i] * p.block_bytes, kSector);
+        if (len[i] && !p.regions[i].alloc.first_fit(len[i], &base[i]))
+            fail(KVP_ERR_NOSPACE, "region " + std::to_string(i) + " has no free range of " + std::to_string(len[i]) +
+                                      " bytes");
+    }
+
+    auto rec = std::make_unique<RequestRec>();
+    if (!p.placement_only) {
+        DeviceScope dev(p.device);
+        check_hip(hipEventCreateWithFlags(&rec->stored, hipEventDisableTiming), "hipEventCreate");
+        hipError_t e = hipEventCreateWithFlags(&rec->busy, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            (void)hipEventDestroy(rec->stored);
+            check_hip(e, "hipEventCreate");
+        }
+    }
+    rec->id = request;
+    rec->n_blocks = n_blocks;
+    rec->gen = p.next_gen++;
+    rec->ranges.reserve(N);
+    for (uint32_t i = 0; i < N; ++i) {
+        if (!len[i]) continue;
+        p.regions[i].alloc.take(base[i], len[i]);
+        rec->ranges.push_back(Allocation{rec.get(), i, rec->gen, base[i], counts[i], len[i]});
+    }
+    for (auto &a : rec->ranges) p.regions[a.region].live[a.base] = &a;
+
+    std::vector<uint32_t> region_of;
+    stripe(counts, n_blocks, region_of);
+    std::vector<uint64_t> next(N, 0);
+    for (uint32_t j = 0; j < n_blocks; ++j) {
+        const uint32_t r = region_of[j];
+        const uint64_t off = base[r] + next[r]++ * p.block_bytes;
+        out[j] = kvp_loc{r, rec->gen, off};
+        p.glt.insert(GltEntry{request, j, r, p.regions[r].desc.type, rec->gen, off});
+    }
+    p.requests.emplace(request, std::move(rec));
+}
+
+void pool_lookup(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
+{
+    if (!out && n_blocks) fail(KVP_ERR_INVALID, "map_out is null");
+    std::lock_guard<std::mutex> lock(p.mu);
+    auto it = p.requests.find(request);
+    if (it == p.requests.end()) fail(KVP_ERR_NOTFOUND, "request " + std::to_string(request) + " is not placed");
+    if (it->second->n_blocks != n_blocks)
+        fail(KVP_ERR_INVALID, "request has " + std::to_string(it->second->n_blocks) + " blocks, not " +
+                                  std::to_string(n_blocks));
+    for (uint32_t j = 0; j < n_blocks; ++j) {
+        const GltEntry *e = p.glt.find(request, j);
+        if (!e) fail(KVP_ERR_NOTFOUND, "GLT entry missing");
+        out[j] = kvp_loc{e->region, e->gen, e->offset};
+    }
+}
+
+void pool_release(Pool &p, uint64_t request)
+{
+    std::lock_guard<std::mutex> lock(p.mu);
+    auto it = p.requests.find(request);
+    if (it == p.requests.end()) fail(KVP_ERR_NOTFOUND, "request " + std::to_string(request) + " is not placed");
+    RequestRec &rec = *it->second;
+    if (!p.placement_only) {
+        DeviceScope dev(p.device);
+        if (rec.busy_rec) check_hip(hipEventSynchronize(rec.busy), "hipEventSynchronize");
+        (void)hipEventDestroy(rec.stored);
+        (void)hipEventDestroy(rec.busy);
+    }
+    for (auto &a : rec.ranges) {
+        p.regions[a.region].live.erase(a.base);
+        p.regions[a.region].alloc.give(a.base, a.len);
+    }
+    for (uint32_t j = 0; j < rec.n_blocks; ++j) p.glt.erase(request, j);
+    p.requests.erase(it);
+}
+
+// ---------------------------------------------------------------- store / retrieve
+
+namespace {
+
+// The live allocation holding the block at map entry e, or an error.
+const Allocation *resolve(const Pool &p, const kvp_loc &e, uint32_t b, const Allocation *hint)
+{
+    const uint32_t N = static_cast<uint32_t>(p.regions.size());
+    if (e.region >= N)
+        fail(KVP_ERR_INVALID, "map entry " + std::to_string(b) + ": region " + std::to_string(e.region) +
+                                  " out of range");
+    const Region &r = p.regions[e.region];
+    if (e.offset % 16 != 0 || e.offset > r.capacity || r.capacity - e.offset < p.block_bytes)
+        fail(KVP_ERR_INVALID, "map entry " + std::to_string(b) + ": offset outside region");
+    const Allocation *a = hint;
+    if (!(a && a->region == e.region && e.offset >= a->base && e.offset < a->base + a->blocks * p.block_bytes)) {
+        auto it = r.live.upper_bound(e.offset);
+        if (it == r.live.begin()) fail(KVP_ERR_STALE, "map entry " + std::to_string(b) + ": no live placement there");
+        a = std::prev(it)->second;
+        if (e.offset >= a->base + a->blocks * p.block_bytes)
+            fail(KVP_ERR_STALE, "map entry " + std::to_string(b) + ": no live placement there");
+    }
+    if ((e.offset - a->base) % p.block_bytes != 0 || a->gen != e.gen)
+        fail(KVP_ERR_STALE, "map entry " + std::to_string(b) + ": stale generation or block boundary");
+    return a;
+}
+
+Slot &acquire_slot(Pool &p, size_t bytes)
+{
+    Slot &s = p.ring[p.ring_next];
+    p.ring_next = (p.ring_next + 1) % static_cast<uint32_t>(p.ring.size());
+    if (s.pending) {
+        check_hip(hipEventSynchronize(s.done), "hipEventSynchronize");
+        s.pending = false;
+    }
+    if (s.cap < bytes) {
+        free_slot(s);
+        const size_t cap = round_up(std::max(bytes, kSlotMin), kSlotMin);
+        void *h = nullptr, *d = nullptr;
+        if (hipHostMalloc(&h, cap, hipHostMallocDefault) != hipSuccess || !h)
+            fail(KVP_ERR_NOMEM, "work-list pinned buffer");
+        if (hipMalloc(&d, cap) != hipSuccess || !d) {
+            (void)hipHostFree(h);
+            fail(KVP_ERR_NOMEM, "work-list device buffer");
+        }
+        s.host = h;
+        s.dev = d;
+        s.cap = cap;
+    }
+    return s;
+}
+
+}  // namespace
+
+void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t *table, uint32_t num_slots,
+                   void *const *k_layers, void *const *v_layers, void *stream_ptr, bool gather)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to copy");
+    if (n_blocks && (!map || !table)) fail(KVP_ERR_INVALID, "null map or block table");
+    const uint32_t L = p.spec.num_layers;
+    if (!k_layers || !v_layers) fail(KVP_ERR_INVALID, "null layer pointer array");
+    for (uint32_t l = 0; l < L; ++l) {
+        const uintptr_t k = reinterpret_cast<uintptr_t>(k_layers[l]), v = reinterpret_cast<uintptr_t>(v_layers[l]);
+        if (!k || !v || (k & 15) || (v & 15))
+            fail(KVP_ERR_INVALID, "layer " + std::to_string(l) + ": null or unaligned cache pointer");
+    }
+    if (static_cast<uint64_t>(n_blocks) * 2 * L >= (1ull << 32)) fail(KVP_ERR_INVALID, "request too large");
+
+    std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+
+    // GLT-resolved locations, grouped by region class (Sec. 4.3)
+    std::vector<CopyItem> items[2];
+    std::vector<RequestRec *> touched;
+    std::vector<uint64_t> targets;
+    std::vector<uint8_t> slot_used;
+    if (gather) slot_used.assign(num_slots, 0);
+    const Allocation *hint = nullptr;
+    for (uint32_t b = 0; b < n_blocks; ++b) {
+        const kvp_loc &e = map[b];
+        if (e.region == KVP_ABSENT) continue;
+        hint = resolve(p, e, b, hint);
+        const int32_t slot = table[b];
+        if (slot < 0 || static_cast<uint32_t>(slot) >= num_slots)
+            fail(KVP_ERR_INVALID, "block table entry " + std::to_string(b) + " = " + std::to_string(slot) +
+                                      " outside [0, " + std::to_string(num_slots) + ")");
+        if (gather) {
+            if (slot_used[slot]) fail(KVP_ERR_INVALID, "destination slot " + std::to_string(slot) + " named twice");
+            slot_used[slot] = 1;
+        } else {
+            targets.push_back((static_cast<uint64_t>(e.region) << 48) | (e.offset >> 4));
+        }
+        if (std::find(touched.begin(), touched.end(), hint->owner) == touched.end()) touched.push_back(hint->owner);
+        const Region &r = p.regions[e.region];
+        const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
+        items[cls].push_back(CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
+    }
+    if (!gather) {
+        std::sort(targets.begin(), targets.end());
+        if (std::adjacent_find(targets.begin(), targets.end()) != targets.end())
+            fail(KVP_ERR_INVALID, "two map entries name the same pool block");
+    }
+    const size_t n_items = items[0].size() + items[1].size();
+    const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
+    if (p.timing) {
+        p.timed_valid = true;
+        for (int c = 0; c < 2; ++c) {
+            p.timed_ran[c] = false;
+            p.timed_blocks[c] = static_cast<uint32_t>(items[c].size());
+        }
+    }
+    if (n_items == 0) return;
+
+    // work list: [2L cache pointers][host items][staging items]
+    const size_t ptr_bytes = round_up(2ull * L * sizeof(uint64_t), 16);
+    const size_t bytes = ptr_bytes + n_items * sizeof(CopyItem);
+    Slot &slot = acquire_slot(p, bytes);
+    auto *ptrs = static_cast<uint64_t *>(slot.host);
+    for (uint32_t l = 0; l < L; ++l) {
+        ptrs[2 * l] = reinterpret_cast<uint64_t>(k_layers[l]);
+        ptrs[2 * l + 1] = reinterpret_cast<uint64_t>(v_layers[l]);
+    }
+    auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(slot.host) + ptr_bytes);
+    std::copy(items[0].begin(), items[0].end(), list);
+    std::copy(items[1].begin(), items[1].end(), list + items[0].size());
+
+    hipStream_t s = static_cast<hipStream_t>(stream_ptr);
+    // ordering with earlier work on the same requests from any stream:
+    // retrieve after store (read after write), store after store/retrieve
+    for (RequestRec *rec : touched) {
+        if (gather && rec->stored_rec) check_hip(hipStreamWaitEvent(s, rec->stored, 0), "hipStreamWaitEvent");
+        if (!gather && rec->busy_rec) check_hip(hipStreamWaitEvent(s, rec->busy, 0), "hipStreamWaitEvent");
+    }
+    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
+    check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
+    slot.pending = true;  // from here on the slot is in use even if a launch fails
+
+    const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
+    hipStream_t cls_stream[2] = {p.s_host, p.s_stage};
+    hipEvent_t cls_done[2] = {p.host_done, p.stage_done};
+    size_t first = 0;
+    for (uint32_t c = 0; c < 2; ++c) {
+        if (items[c].empty()) continue;
+        CopyArgs a{};
+        a.items = dev_list + first;
+        a.cache = static_cast<const uint64_t *>(slot.dev);
+        a.n_items = static_cast<uint32_t>(items[c].size());
+        a.chunks = 2 * L;
+        a.chunk_bytes = p.chunk_bytes;
+        a.heads = p.spec.num_kv_heads;
+        a.tokens = p.spec.block_size;
+        a.row_vec = static_cast<uint32_t>(static_cast<uint64_t>(p.spec.head_dim) * p.spec.elem_bytes / 16);
+        a.layout = p.spec.pool_layout;
+        first += items[c].size();
+        const LaunchCfg &lc = p.launch[c][op];
+        check_hip(hipStreamWaitEvent(cls_stream[c], p.fork, 0), "hipStreamWaitEvent");
+        if (p.timing) check_hip(hipEventRecord(p.t0[c], cls_stream[c]), "hipEventRecord");
+        check_hip(launch_chunk_copy(a, gather, lc.grid, lc.flags, cls_stream[c]), "kernel launch");
+        if (p.timing) {
+            check_hip(hipEventRecord(p.t1[c], cls_stream[c]), "hipEventRecord");
+            p.timed_ran[c] = true;
+        }
+        check_hip(hipEventRecord(cls_done[c], cls_stream[c]), "hipEventRecord");
+        check_hip(hipStreamWaitEvent(s, cls_done[c], 0), "hipStreamWaitEvent");
+    }
+    check_hip(hipEventRecord(slot.done, s), "hipEventRecord");
+    for (RequestRec *rec : touched) {
+        check_hip(hipEventRecord(rec->busy, s), "hipEventRecord");
+        rec->busy_rec = true;
+        if (!gather) {
+            check_hip(hipEventRecord(rec->stored, s), "hipEventRecord");
+            rec->stored_rec = true;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- introspection, launch config, timing
+
+void pool_region_info(const Pool &p, uint32_t region, kvp_region_info *out)
+{
+    if (!out) fail(KVP_ERR_INVALID, "null output");
+    if (region >= p.regions.size()) fail(KVP_ERR_INVALID, "region index out of range");
+    const Region &r = p.regions[region];
+    *out = kvp_region_info{r.desc.type, r.desc.numa_node, r.numa_actual, r.flags_used, r.capacity,
+                           r.bandwidth, r.host, r.dev};
+}
+
+void pool_region_read(Pool &p, uint32_t region, uint64_t offset, uint64_t bytes, void *dst)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory");
+    if (region >= p.regions.size()) fail(KVP_ERR_INVALID, "region index out of range");
+    const Region &r = p.regions[region];
+    if (!dst && bytes) fail(KVP_ERR_INVALID, "null destination");
+    if (offset > r.capacity || r.capacity - offset < bytes) fail(KVP_ERR_INVALID, "range outside region");
+    if (!bytes) return;
+    if (r.host) {
+        std::memcpy(dst, static_cast<const char *>(r.host) + offset, bytes);
+    } else {
+        DeviceScope dev(p.device);
+        check_hip(hipMemcpy(dst, static_cast<const char *>(r.dev) + offset, bytes, hipMemcpyDeviceToHost),
+                  "hipMemcpy");
+    }
+}
+
+void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)
+{
+    if (cls > 1 || op > 1) fail(KVP_ERR_INVALID, "class and op must be 0 or 1");
+    if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS)) fail(KVP_ERR_INVALID, "unknown flags");
+    if (grid > (1u << 20)) fail(KVP_ERR_INVALID, "grid too large");
+    std::lock_guard<std::mutex> lock(p.mu);
+    p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op), flags};
+}
+
+void pool_set_timing(Pool &p, int enable)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
+    std::lock_guard<std::mutex> lock(p.mu);
+    p.timing = enable != 0;
+    p.timed_valid = false;
+}
+
+void pool_last_timing(Pool &p, kvp_timing *out)
+{
+    if (!out) fail(KVP_ERR_INVALID, "null output");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (!p.timing || !p.timed_valid) fail(KVP_ERR_INVALID, "no timed call");
+    DeviceScope dev(p.device);
+    float ms[2] = {-1.f, -1.f};
+    for (int c = 0; c < 2; ++c) {
+        if (!p.timed_ran[c]) continue;
+        check_hip(hipEventSynchronize(p.t1[c]), "hipEventSynchronize");
+        check_hip(hipEventElapsedTime(&ms[c], p.t0[c], p.t1[c]), "hipEventElapsedTime");
+    }
+    *out = kvp_timing{ms[0], ms[1], p.timed_blocks[0], p.timed_blocks[1]};
+}
+
+}  // namespace kvp

@@ -1,0 +1,272 @@
+"""ctypes binding of libkvpool.so (argument marshalling only).
+
+Every function maps one-to-one onto an ``extern "C"`` entry point declared in
+``include/kvpool.h``; all computation, validation and GPU work happens in the
+library.  Device memory and streams are passed as integers (``tensor.data_ptr()``,
+``torch.cuda.Stream.cuda_stream``).  If the library has not been built this
+module raises on import: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkvpool.so")
+
+KVP_OK = 0
+ERRORS = {-1: "INVALID", -2: "NOMEM", -3: "NOSPACE", -4: "NOTFOUND", -5: "STALE", -6: "HIP"}
+REGION_HOST, REGION_STAGING = 0, 1
+HOST_DEFAULT, HOST_COHERENT, HOST_NONCOHERENT = 0, 1, 2
+ABSENT = 0xFFFFFFFF
+CLASS_HOST, CLASS_STAGING = 0, 1
+OP_RETRIEVE, OP_STORE = 0, 1
+LAUNCH_NT_LOAD, LAUNCH_NT_STORE, LAUNCH_LDS = 1, 2, 4
+
+LOC_DTYPE = np.dtype([("region", "<u4"), ("gen", "<u4"), ("offset", "<u8")])
+
+
+class _RegionDesc(ctypes.Structure):
+    _fields_ = [("type", ctypes.c_uint32), ("numa_node", ctypes.c_int32),
+                ("capacity_bytes", ctypes.c_uint64), ("flags", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32)]
+
+
+class _KVSpec(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_uint32), ("num_kv_heads", ctypes.c_uint32),
+                ("head_dim", ctypes.c_uint32), ("block_size", ctypes.c_uint32),
+                ("elem_bytes", ctypes.c_uint32), ("pool_layout", ctypes.c_uint32)]
+
+
+class _RegionInfo(ctypes.Structure):
+    _fields_ = [("type", ctypes.c_uint32), ("numa_node", ctypes.c_int32),
+                ("numa_node_actual", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("capacity_bytes", ctypes.c_uint64), ("bandwidth", ctypes.c_uint64),
+                ("host_ptr", ctypes.c_void_p), ("device_ptr", ctypes.c_void_p)]
+
+
+class _Timing(ctypes.Structure):
+    _fields_ = [("host_ms", ctypes.c_float), ("staging_ms", ctypes.c_float),
+                ("host_blocks", ctypes.c_uint32), ("staging_blocks", ctypes.c_uint32)]
+
+
+assert ctypes.sizeof(_RegionDesc) == 24 and ctypes.sizeof(_KVSpec) == 24
+assert LOC_DTYPE.itemsize == 16
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libkvpool.so is not built (%s); run `python -m paper_2606_14779_amd.build`"
+                      % LIB_PATH)
+_lib = ctypes.CDLL(LIB_PATH)
+
+_u32, _u64, _i32, _vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p
+_SIGS = {
+    "kv_pool_create": (_i32, [_vp, _vp, _u32, _vp, _i32, _vp]),
+    "kv_pool_place": (_i32, [_vp, _u64, _u32, _vp]),
+    "kv_pool_lookup": (_i32, [_vp, _u64, _u32, _vp]),
+    "kv_pool_store": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
+    "kv_pool_retrieve": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
+    "kv_pool_release": (_i32, [_vp, _u64]),
+    "kv_pool_destroy": (None, [_vp]),
+    "kv_pool_last_error": (ctypes.c_char_p, []),
+    "kv_pool_region_info": (_i32, [_vp, _u32, _vp]),
+    "kv_pool_region_read": (_i32, [_vp, _u32, _u64, _u64, _vp]),
+    "kv_pool_counts": (_i32, [_vp, _u32, _u64, _vp]),
+    "kv_pool_set_launch": (_i32, [_vp, _u32, _u32, _u32, _u32]),
+    "kv_pool_set_timing": (_i32, [_vp, _i32]),
+    "kv_pool_last_timing": (_i32, [_vp, _vp]),
+    "kv_probe_copy_kernel": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp]),
+    "kv_probe_memcpy": (_i32, [_vp, _vp, _u64, _vp]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+EXPORTED = tuple(_SIGS)
+
+
+class KVPoolError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("%s (%d): %s" % (ERRORS.get(code, "?"), code, msg))
+        self.code = code
+        self.name = ERRORS.get(code, "?")
+
+
+def _check(rc: int) -> None:
+    if rc != KVP_OK:
+        raise KVPoolError(rc, (_lib.kv_pool_last_error() or b"").decode())
+
+
+def _ptrs(ptrs) -> ctypes.Array:
+    return (ctypes.c_void_p * len(ptrs))(*[int(p) for p in ptrs])
+
+
+def _loc_array(m) -> np.ndarray:
+    a = np.ascontiguousarray(m, dtype=LOC_DTYPE)
+    return a
+
+
+@dataclass
+class Region:
+    kind: str                 # "host" or "staging"
+    capacity_bytes: int
+    numa_node: int = -1
+    coherence: int = HOST_DEFAULT
+
+
+@dataclass
+class KVSpec:
+    num_layers: int
+    num_kv_heads: int
+    head_dim: int
+    block_size: int = 16
+    elem_bytes: int = 2
+    pool_layout: int = 0
+
+    @property
+    def chunk_bytes(self) -> int:
+        return self.num_kv_heads * self.block_size * self.head_dim * self.elem_bytes
+
+    @property
+    def block_bytes(self) -> int:
+        return 2 * self.num_layers * self.chunk_bytes
+
+
+def counts(bandwidths, n: int) -> np.ndarray:
+    """The library's per-region target counts for n blocks (kv_pool_counts)."""
+    bw = np.ascontiguousarray(bandwidths, dtype=np.uint64)
+    out = np.zeros(len(bw), dtype=np.uint64)
+    _check(_lib.kv_pool_counts(bw.ctypes.data if len(bw) else None, len(bw), n, out.ctypes.data))
+    return out
+
+
+def probe_copy_kernel(dst: int, src: int, nbytes: int, grid: int = 0, flags: int = 0, stream: int = 0):
+    _check(_lib.kv_probe_copy_kernel(dst, src, nbytes, grid, flags, stream or None))
+
+
+def probe_memcpy(dst: int, src: int, nbytes: int, stream: int = 0):
+    _check(_lib.kv_probe_memcpy(dst, src, nbytes, stream or None))
+
+
+class KVPool:
+    """A pool of regions with bandwidth weights (kv_pool_create ... kv_pool_destroy)."""
+
+    def __init__(self, regions, bandwidths, spec: KVSpec, device: int = 0):
+        n = len(regions)
+        descs = (_RegionDesc * n)()
+        for i, r in enumerate(regions):
+            kind = {"host": REGION_HOST, "staging": REGION_STAGING}[r.kind]
+            descs[i] = _RegionDesc(kind, r.numa_node, r.capacity_bytes, r.coherence, 0)
+        bw = np.ascontiguousarray(bandwidths, dtype=np.uint64)
+        if len(bw) != n:
+            raise ValueError("one bandwidth per region")
+        self.spec = spec
+        self.n_regions = n
+        cs = _KVSpec(spec.num_layers, spec.num_kv_heads, spec.head_dim, spec.block_size,
+                     spec.elem_bytes, spec.pool_layout)
+        h = ctypes.c_void_p()
+        _check(_lib.kv_pool_create(ctypes.addressof(descs), bw.ctypes.data, n, ctypes.addressof(cs),
+                                   device, ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            _lib.kv_pool_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        self.close()
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # ---- placement / GLT
+    def place(self, request: int, n_blocks: int) -> np.ndarray:
+        out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
+        _check(_lib.kv_pool_place(self._h, request, n_blocks, out.ctypes.data))
+        return out[:n_blocks]
+
+    def lookup(self, request: int, n_blocks: int) -> np.ndarray:
+        out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
+        _check(_lib.kv_pool_lookup(self._h, request, n_blocks, out.ctypes.data))
+        return out[:n_blocks]
+
+    def release(self, request: int) -> None:
+        _check(_lib.kv_pool_release(self._h, request))
+
+    # ---- data path
+    def _transfer(self, fn, loc_map, table, num_slots, k_ptrs, v_ptrs, stream):
+        m = _loc_array(loc_map)
+        t = np.ascontiguousarray(table, dtype=np.int32)
+        if len(m) != len(t):
+            raise ValueError("map and block table differ in length")
+        ks, vs = _ptrs(k_ptrs), _ptrs(v_ptrs)
+        if len(ks) != self.spec.num_layers or len(vs) != self.spec.num_layers:
+            raise ValueError("one K and one V pointer per layer")
+        _check(fn(self._h, m.ctypes.data if len(m) else None, len(m), t.ctypes.data if len(t) else None,
+                  num_slots, ctypes.addressof(ks), ctypes.addressof(vs), stream or None))
+
+    def store(self, loc_map, src_table, src_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
+        self._transfer(_lib.kv_pool_store, loc_map, src_table, src_num_slots, k_ptrs, v_ptrs, stream)
+
+    def retrieve(self, loc_map, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
+        self._transfer(_lib.kv_pool_retrieve, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream)
+
+    # ---- introspection
+    def region_info(self, region: int) -> dict:
+        info = _RegionInfo()
+        _check(_lib.kv_pool_region_info(self._h, region, ctypes.byref(info)))
+        return {k: getattr(info, k) for k, _ in _RegionInfo._fields_}
+
+    def region_read(self, region: int, offset: int, nbytes: int, out: np.ndarray | None = None) -> np.ndarray:
+        if out is None:
+            out = np.empty(nbytes, dtype=np.uint8)
+        assert out.flags.c_contiguous and out.nbytes >= nbytes
+        _check(_lib.kv_pool_region_read(self._h, region, offset, nbytes, out.ctypes.data))
+        return out
+
+    # ---- launch configuration and timing
+    def set_launch(self, cls: int, op: int, grid: int = 0, flags: int = 0) -> None:
+        _check(_lib.kv_pool_set_launch(self._h, cls, op, grid, flags))
+
+    def set_timing(self, enable: bool) -> None:
+        _check(_lib.kv_pool_set_timing(self._h, 1 if enable else 0))
+
+    def last_timing(self) -> dict:
+        t = _Timing()
+        _check(_lib.kv_pool_last_timing(self._h, ctypes.byref(t)))
+        return {k: getattr(t, k) for k, _ in _Timing._fields_}
+
+
+def allowed_numa_nodes() -> list[int]:
+    """NUMA nodes this process may allocate on (online nodes within Mems_allowed)."""
+    def parse(s):
+        out = set()
+        for part in s.strip().split(","):
+            if not part:
+                continue
+            if "-" in part:
+                a, b = part.split("-")
+                out.update(range(int(a), int(b) + 1))
+            else:
+                out.add(int(part))
+        return out
+    try:
+        online = parse(open("/sys/devices/system/node/online").read())
+    except OSError:
+        online = {0}
+    allowed = online
+    try:
+        for line in open("/proc/self/status"):
+            if line.startswith("Mems_allowed_list:"):
+                allowed = parse(line.split(":", 1)[1])
+    except OSError:
+        pass
+    nodes = sorted(online & allowed)
+    return nodes or [0]

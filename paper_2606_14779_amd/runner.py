@@ -1,0 +1,119 @@
+"""Set one synthetic workload up on a GPU through the library.
+
+A ``WorkloadRun`` owns the pool (``kv_pool_create``), the engine's source and
+destination paged caches (torch tensors: device memory only), the placement
+maps (``kv_pool_place``) and the offload (``kv_pool_store``).  Retrieval is a
+single ``kv_pool_retrieve`` call per request.  The tests and the bench drive
+the hot path through this class; it performs no copy of its own besides
+putting the seeded source values into GPU memory.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import kvgen
+from kvgen.workloads import Workload
+
+from . import kvpool as K
+
+SENTINEL = 0x7FA5  # a bf16 NaN pattern that the generator never produces
+
+
+class WorkloadRun:
+    def __init__(self, wl: Workload, device: int = 0, coherence: int = K.HOST_DEFAULT,
+                 numa_nodes=None, retrieve_grid: int = 0, retrieve_flags: int = 0):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.device = device
+        sh = wl.shape
+        nodes = list(numa_nodes) if numa_nodes else K.allowed_numa_nodes()
+        self.regions = []
+        for r in wl.regions:
+            if r.kind == "host":
+                node = nodes[r.numa % len(nodes)] if r.numa >= 0 else -1
+                self.regions.append(K.Region("host", r.capacity_bytes, node, coherence))
+            else:
+                self.regions.append(K.Region("staging", r.capacity_bytes))
+        self.weights = [r.weight for r in wl.regions]
+        self.spec = K.KVSpec(sh.layers, sh.kv_heads, sh.head_dim, sh.block_size, sh.elem_bytes, wl.layout)
+        self.pool = K.KVPool(self.regions, self.weights, self.spec, device)
+        dev = torch.device("cuda", device)
+        shape = (sh.layers, 2)
+        tail = (sh.kv_heads, sh.block_size, sh.head_dim)
+        self.src = torch.empty(shape + (wl.src_num_slots,) + tail, dtype=torch.int16, device=dev)
+        self.dst = torch.empty(shape + (wl.dst_num_slots,) + tail, dtype=torch.int16, device=dev)
+        self.maps = {}            # request_id -> placed map (present prefix)
+        self.retrieve_maps = {}   # request_id -> map of the whole context (absent tail)
+        self.streams = [torch.cuda.Stream(device=dev) for _ in range(wl.n_streams)]
+
+    # ---- pointers
+    @staticmethod
+    def layer_ptrs(cache):
+        L = cache.shape[0]
+        return [cache[l, 0].data_ptr() for l in range(L)], [cache[l, 1].data_ptr() for l in range(L)]
+
+    # ---- setup steps
+    def fill_source(self, threads=None, keep_host=False):
+        """Seeded values of every present block into the source cache (host generate, then copy)."""
+        sh = self.wl.shape
+        host = np.empty(tuple(self.src.shape), dtype=np.uint16)
+        kp = [host[l, 0].ctypes.data for l in range(sh.layers)]
+        vp = [host[l, 1].ctypes.data for l in range(sh.layers)]
+        for q in self.wl.requests:
+            kvgen.fill_cache(self.wl.seed, q.request_id, np.arange(q.n_present, dtype=np.uint64), q.src_slots,
+                             sh.layers, sh.kv_heads, sh.block_size, sh.head_dim, kp, vp, threads)
+        self.src.copy_(self.torch.from_numpy(host.view(np.int16)))
+        self.torch.cuda.synchronize(self.device)
+        return host if keep_host else None
+
+    def fill_dst(self, value=SENTINEL):
+        self.dst.fill_(np.int16(np.uint16(value).view(np.int16)).item())
+
+    def place_all(self):
+        for q in self.wl.requests:
+            m = self.pool.place(q.request_id, q.n_present)
+            self.maps[q.request_id] = m
+            full = np.zeros(q.n_blocks, dtype=K.LOC_DTYPE)
+            full[:q.n_present] = m
+            full["region"][q.n_present:] = K.ABSENT
+            self.retrieve_maps[q.request_id] = full
+
+    def store_all(self, stream=None):
+        kp, vp = self.layer_ptrs(self.src)
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        for q in self.wl.requests:
+            self.pool.store(self.maps[q.request_id], q.src_slots, self.wl.src_num_slots, kp, vp, s.cuda_stream)
+
+    def retrieve(self, q, stream=None):
+        kp, vp = self.layer_ptrs(self.dst)
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        self.pool.retrieve(self.retrieve_maps[q.request_id], q.dst_slots, self.wl.dst_num_slots, kp, vp,
+                           s.cuda_stream)
+
+    def retrieve_all(self):
+        """One retrieve per request; request i on stream i % n_streams (forked from the current stream)."""
+        torch = self.torch
+        cur = torch.cuda.current_stream(self.device)
+        if len(self.streams) == 1:
+            for q in self.wl.requests:
+                self.retrieve(q, cur)
+            return
+        for s in self.streams:
+            s.wait_stream(cur)
+        for i, q in enumerate(self.wl.requests):
+            self.retrieve(q, self.streams[q.stream % len(self.streams)])
+        for s in self.streams:
+            cur.wait_stream(s)
+
+    def setup(self, threads=None, keep_host=False):
+        host = self.fill_source(threads, keep_host)
+        self.fill_dst()
+        self.place_all()
+        self.store_all()
+        self.torch.cuda.synchronize(self.device)
+        return host
+
+    def close(self):
+        self.pool.close()
+        self.src = self.dst = None

@@ -1,0 +1,106 @@
+"""Helpers of the GPU tests: run a workload through the library and compare
+with the oracle.  Only the tests import this module."""
+import sys
+
+import numpy as np
+
+import kvgen
+import oracle
+from paper_2606_14779_amd.runner import SENTINEL, WorkloadRun
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def oracle_expectation(wl, run, host_src):
+    """Oracle placement, pool contents and destination cache for a whole workload."""
+    sh = wl.shape
+    L = sh.layers
+    shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
+    ora = oracle.Pool([r.weight for r in wl.regions], [r.capacity_bytes for r in wl.regions], sh.block_bytes)
+    regions = [np.zeros(r.capacity_bytes, np.uint8) for r in wl.regions]
+    expect = np.full(tuple(run.dst.shape), SENTINEL, np.uint16)
+    maps = {}
+    for q in wl.requests:
+        m = ora.place(q.request_id, q.n_present)
+        maps[q.request_id] = m
+        oracle.store(m, q.src_slots, regions, [host_src[l, 0] for l in range(L)],
+                     [host_src[l, 1] for l in range(L)], shape, wl.layout)
+    for q in wl.requests:
+        full = np.zeros(q.n_blocks, dtype=oracle.LOC_DTYPE)
+        full[:q.n_present] = maps[q.request_id]
+        full["region"][q.n_present:] = oracle.ABSENT
+        oracle.gather(full, q.dst_slots, regions, [expect[l, 0] for l in range(L)],
+                      [expect[l, 1] for l in range(L)], shape, wl.layout)
+    return maps, regions, expect
+
+
+def check_full(wl, run, host_src):
+    """Element-by-element comparison of maps, pool bytes and destination."""
+    maps, regions, expect = oracle_expectation(wl, run, host_src)
+    bb = wl.shape.block_bytes
+    for q in wl.requests:
+        assert np.array_equal(run.maps[q.request_id], maps[q.request_id]), "placement differs"
+        m = maps[q.request_id]
+        for r in range(len(wl.regions)):
+            offs = m["offset"][m["region"] == r]
+            if len(offs) == 0:
+                continue
+            lo, hi = int(offs.min()), int(offs.max()) + bb
+            got = run.pool.region_read(r, lo, hi - lo)
+            assert np.array_equal(got, regions[r][lo:hi]), "pool region %d bytes differ" % r
+    got = run.dst.cpu().numpy().view(np.uint16)
+    if not np.array_equal(got, expect):
+        bad = np.argwhere(got != expect)
+        raise AssertionError("destination differs at %d elements, first %s" % (len(bad), bad[:4].tolist()))
+
+
+def check_sampled(wl, run, n_sample=48, seed=0):
+    """Full-size check: sampled blocks through the oracle, every block by round trip,
+    every untouched slot by sentinel."""
+    import torch
+    sh = wl.shape
+    L, bb = sh.layers, sh.block_bytes
+    shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
+    rng = np.random.default_rng(seed)
+    ora = oracle.Pool([r.weight for r in wl.regions], [r.capacity_bytes for r in wl.regions], bb)
+    for q in wl.requests:
+        om = ora.place(q.request_id, q.n_present)
+        assert np.array_equal(om, run.maps[q.request_id]), "placement differs"
+        picks = {0, q.n_present - 1} | set(rng.integers(0, q.n_present, n_sample).tolist())
+        for b in sorted(picks):
+            vals = kvgen.block_values(wl.seed, q.request_id, b, L, sh.kv_heads, sh.block_size, sh.head_dim)
+            src1 = np.ascontiguousarray(vals[:, :, None])           # [L][2][1 slot][H][bs][D]
+            loc = np.zeros(1, dtype=oracle.LOC_DTYPE)               # same block in a 1-block pool
+            reg = np.zeros(bb, np.uint8)
+            oracle.store(loc, [0], [reg], [src1[l, 0] for l in range(L)], [src1[l, 1] for l in range(L)],
+                         shape, wl.layout)
+            got_pool = run.pool.region_read(int(om["region"][b]), int(om["offset"][b]), bb)
+            assert np.array_equal(got_pool, reg), "pool block %d of request %d differs" % (b, q.request_id)
+            dst1 = np.full_like(src1, SENTINEL)
+            oracle.gather(loc, [0], [reg], [dst1[l, 0] for l in range(L)], [dst1[l, 1] for l in range(L)],
+                          shape, wl.layout)
+            slot = int(q.dst_slots[b])
+            got = run.dst[:, :, slot].cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, dst1[:, :, 0]), "dst slot %d (block %d) differs" % (slot, b)
+    # every present block: retrieve(store(x)) == x, compared layer by layer on the GPU with torch
+    dev = run.dst.device
+    touched = np.zeros(wl.dst_num_slots, bool)
+    for q in wl.requests:
+        ds = torch.from_numpy(q.dst_slots[:q.n_present].astype(np.int64)).to(dev)
+        ss = torch.from_numpy(q.src_slots.astype(np.int64)).to(dev)
+        touched[q.dst_slots[:q.n_present]] = True
+        for l in range(L):
+            assert torch.equal(run.dst[l].index_select(1, ds), run.src[l].index_select(1, ss)), \
+                "round trip differs in layer %d of request %d" % (l, q.request_id)
+    rest = torch.from_numpy(np.flatnonzero(~touched).astype(np.int64)).to(dev)
+    sent = int(np.uint16(SENTINEL).view(np.int16))
+    for l in range(L):
+        assert bool((run.dst[l].index_select(1, rest) == sent).all()), "untouched slot changed (layer %d)" % l
+
+
+def make_run(wl, **kw):
+    run = WorkloadRun(wl, device=0, **kw)
+    return run

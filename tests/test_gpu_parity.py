@@ -1,0 +1,297 @@
+"""GPU parity of the KV-pool store / retrieve path against the CPU oracle.
+
+All GPU work goes through the C ABI (``paper_2606_14779_amd.kvpool``).  The
+bar is bit-exact: the path copies bf16 words and does no arithmetic.
+"""
+import numpy as np
+import pytest
+
+from kvgen import workloads
+from paper_2606_14779_amd import kvpool as K
+from paper_2606_14779_amd.runner import SENTINEL
+
+from gpu_util import check_full, check_sampled, make_run, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _run_and_check(wl, label, **kw):
+    say("case", label, wl.describe()["workload"], "layout", wl.layout,
+        "blocks", [q.n_present for q in wl.requests])
+    run = make_run(wl, **kw)
+    try:
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("layout", [0, 1])
+def test_parity_scaled_workloads(cfg, layout):
+    wl = workloads.make(cfg, max_blocks=61, layout=layout)
+    _run_and_check(wl, "scaled")
+
+
+@pytest.mark.parametrize("grid,flags", [(1, 0), (7, K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE),
+                                        (4096, K.LAUNCH_NT_LOAD), (300, K.LAUNCH_NT_STORE)])
+def test_parity_launch_shapes(grid, flags):
+    wl = workloads.make(2, max_blocks=45)
+    say("case launch", grid, flags)
+    run = make_run(wl)
+    try:
+        for cls in (K.CLASS_HOST, K.CLASS_STAGING):
+            for op in (K.OP_RETRIEVE, K.OP_STORE):
+                run.pool.set_launch(cls, op, grid, flags)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("flags", [0, K.LAUNCH_LDS, K.LAUNCH_LDS | K.LAUNCH_NT_LOAD])
+def test_parity_token_major_lds(flags):
+    wl = workloads.make(4, max_blocks=33, layout=1)
+    say("case token-major", flags)
+    run = make_run(wl)
+    try:
+        for cls in (K.CLASS_HOST, K.CLASS_STAGING):
+            for op in (K.OP_RETRIEVE, K.OP_STORE):
+                run.pool.set_launch(cls, op, 0, flags)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def _custom(shape, regions, n, layout=0, dst_slots=None, src_slots=None, extra_slots=3, absent=()):
+    """A one-request workload with an arbitrary shape (ragged chunk sizes)."""
+    rng = np.random.default_rng(n * 31 + len(regions))
+    src = rng.permutation(n + extra_slots)[:n].astype(np.int32) if src_slots is None else src_slots
+    dslots = n + extra_slots
+    dst = rng.permutation(dslots)[:n].astype(np.int32) if dst_slots is None else dst_slots
+    req = workloads.RequestSpec(1, n, n, src, dst)
+    wl = workloads.Workload(0, "custom", 77, shape, layout, regions, [req], n + extra_slots, dslots)
+    workloads._size_regions(wl.regions, [n], shape.block_bytes)
+    return wl
+
+
+RAGGED = workloads.KVShape("ragged", 3, 3, 24)          # chunk 2304 B = 144 vectors: tail path
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+@pytest.mark.parametrize("flags", [0, K.LAUNCH_LDS])
+def test_parity_ragged_chunk(layout, flags):
+    regions = [workloads.RegionSpec("host", 2, 0), workloads.RegionSpec("staging", 3),
+               workloads.RegionSpec("host", 1, 1)]
+    wl = _custom(RAGGED, regions, 29, layout)
+    say("case ragged", layout, flags)
+    run = make_run(wl)
+    try:
+        for cls in (0, 1):
+            for op in (0, 1):
+                run.pool.set_launch(cls, op, 5, flags)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("kind", ["host", "staging"])
+def test_single_block_single_region(kind):
+    wl = _custom(workloads.LLAMA_8B, [workloads.RegionSpec(kind, 1, 0 if kind == "host" else -1)], 1)
+    _run_and_check(wl, "n=1 N=1 " + kind)
+
+
+def test_last_slot_and_full_region():
+    """Destination slot num_slots-1 and a region filled to its last byte."""
+    shape = workloads.KVShape("tiny", 2, 2, 64)
+    bb = shape.block_bytes                                  # 16 KiB, sector multiple
+    n = 6
+    dst = np.array([5, 0, 3, 1, 4, 2], np.int32) + 2        # includes slot 7 = num_slots - 1
+    wl = _custom(shape, [workloads.RegionSpec("staging", 1), workloads.RegionSpec("host", 1, 0)], n,
+                 dst_slots=dst, extra_slots=2)
+    for r in wl.regions:
+        r.capacity_bytes = (n // 2) * bb                    # exactly full
+    _run_and_check(wl, "last slot / full region")
+
+
+def test_absent_entries_and_all_absent():
+    wl = workloads.make(2, max_blocks=40)
+    say("case absent")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        m = run.retrieve_maps[q.request_id].copy()
+        skip = np.arange(0, q.n_blocks, 3)
+        m["region"][skip] = K.ABSENT
+        kp, vp = run.layer_ptrs(run.dst)
+        table = q.dst_slots.copy()
+        table[skip] = -1                                     # never read for absent entries
+        run.pool.retrieve(m, table, wl.dst_num_slots, kp, vp, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        got = run.dst.cpu().numpy().view(np.uint16)
+        src = host
+        for b in range(q.n_blocks):
+            s = q.dst_slots[b]
+            if b in set(skip.tolist()):
+                assert np.all(got[:, :, s] == SENTINEL)
+            else:
+                assert np.array_equal(got[:, :, s], src[:, :, q.src_slots[b]])
+        m["region"][:] = K.ABSENT                            # nothing to do, nothing launched
+        run.pool.retrieve(m, table, wl.dst_num_slots, kp, vp, 0)
+        torch.cuda.synchronize()
+    finally:
+        run.close()
+
+
+def test_errors_leave_destination_untouched():
+    wl = workloads.make(2, max_blocks=20)
+    say("case errors")
+    run = make_run(wl)
+    try:
+        run.setup()
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        m = run.retrieve_maps[q.request_id]
+
+        def code(fn, *a):
+            with pytest.raises(K.KVPoolError) as ei:
+                fn(*a)
+            return ei.value.name
+
+        bad = q.dst_slots.copy()
+        bad[3] = wl.dst_num_slots
+        assert code(run.pool.retrieve, m, bad, wl.dst_num_slots, kp, vp, 0) == "INVALID"
+        dup = q.dst_slots.copy()
+        dup[4] = dup[5]
+        assert code(run.pool.retrieve, m, dup, wl.dst_num_slots, kp, vp, 0) == "INVALID"
+        mm = m.copy()
+        mm["region"][2] = 17
+        assert code(run.pool.retrieve, mm, q.dst_slots, wl.dst_num_slots, kp, vp, 0) == "INVALID"
+        mm = m.copy()
+        mm["offset"][2] += 16                                 # not a block boundary
+        assert code(run.pool.retrieve, mm, q.dst_slots, wl.dst_num_slots, kp, vp, 0) == "STALE"
+        mm = m.copy()
+        mm["gen"][1] += 1
+        assert code(run.pool.retrieve, mm, q.dst_slots, wl.dst_num_slots, kp, vp, 0) == "STALE"
+        kp2 = list(kp)
+        kp2[1] += 8
+        assert code(run.pool.retrieve, m, q.dst_slots, wl.dst_num_slots, kp2, vp, 0) == "INVALID"
+        same = m.copy()
+        same[1] = same[0]
+        assert code(run.pool.store, same, q.src_slots, wl.src_num_slots, *run.layer_ptrs(run.src), 0) == "INVALID"
+        torch.cuda.synchronize()
+        got = run.dst.cpu().numpy().view(np.uint16)
+        assert np.all(got == SENTINEL)                        # no failed call touched it
+        run.pool.release(q.request_id)
+        assert code(run.pool.retrieve, m, q.dst_slots, wl.dst_num_slots, kp, vp, 0) == "STALE"
+    finally:
+        run.close()
+
+
+def test_release_and_reuse():
+    """A released range is reused by the next placement; old maps turn stale."""
+    wl = workloads.make(1, max_blocks=16)
+    say("case reuse")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        old = run.maps[q.request_id].copy()
+        run.pool.release(q.request_id)
+        new = run.pool.place(q.request_id, q.n_present)
+        assert np.array_equal(new["offset"], old["offset"]) and int(new["gen"][0]) == int(old["gen"][0]) + 1
+        run.maps[q.request_id] = new
+        run.retrieve_maps[q.request_id] = new
+        run.store_all()
+        run.fill_dst()
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def test_store_then_retrieve_across_streams():
+    """A retrieve on another stream, enqueued right after the store, waits for it."""
+    wl = workloads.make(3, max_blocks=200)
+    say("case cross-stream")
+    run = make_run(wl)
+    try:
+        host = run.fill_source(keep_host=True)
+        run.fill_dst()
+        run.place_all()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Stream(), torch.cuda.Stream()
+        run.store_all(stream=a)
+        run.retrieve(wl.requests[0], stream=b)               # no host synchronisation in between
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def test_timing_reports_both_classes():
+    wl = workloads.make(2, max_blocks=64)
+    run = make_run(wl)
+    try:
+        run.setup()
+        run.pool.set_timing(True)
+        run.retrieve_all()
+        t = run.pool.last_timing()
+        m = run.maps[1]
+        n_host = int(np.sum(np.isin(m["region"], [0, 1])))
+        assert t["host_blocks"] == n_host and t["staging_blocks"] == len(m) - n_host
+        assert t["host_ms"] > 0 and t["staging_ms"] > 0
+    finally:
+        run.close()
+
+
+def test_probes_copy_exactly():
+    n = 64 << 20
+    src = torch.randint(-32768, 32767, (n // 2,), dtype=torch.int16, device="cuda")
+    dst = torch.zeros_like(src)
+    K.probe_copy_kernel(dst.data_ptr(), src.data_ptr(), n - 48, 0, 0, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:(n - 48) // 2], src[:(n - 48) // 2]) and bool((dst[(n - 48) // 2:] == 0).all())
+    host = torch.empty(n // 2, dtype=torch.int16, pin_memory=True)
+    K.probe_memcpy(host.data_ptr(), src.data_ptr(), n, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert torch.equal(host, src.cpu())
+
+
+# ---- full-size workloads, in the launch configuration the bench times
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_full_size_workloads(cfg):
+    wl = workloads.make(cfg)
+    say("case full-size", wl.name, "bytes", wl.retrieved_bytes)
+    run = make_run(wl)
+    try:
+        run.setup()
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_sampled(wl, run)
+    finally:
+        run.close()
+        torch.cuda.empty_cache()

@@ -47,6 +47,27 @@ def test_values_are_standard_normal_bf16():
     assert abs(np.mean(np.abs(v) < 2.0) - 0.9545) < 0.002
 
 
+def _bf16_rne(x):
+    """Round float64 values to bf16 bits (ties to even) with exact comparisons."""
+    f = x.astype(np.float32)
+    u = f.view(np.uint32)
+    lo = (u & 0xFFFF0000).astype(np.uint32)
+    hi = lo + 0x10000
+    dlo = np.abs(x - lo.view(np.float32).astype(np.float64))
+    dhi = np.abs(hi.view(np.float32).astype(np.float64) - x)
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & ((lo >> 16) & 1 == 1))
+    return np.where(pick_hi, hi >> 16, lo >> 16).astype(np.uint16)
+
+
+def test_normal_table_matches_scipy_quantiles():
+    from scipy.special import ndtri
+    q = kvgen.normal_table()
+    expect = _bf16_rne(ndtri((np.arange(65536) + 0.5) / 65536.0))
+    assert np.array_equal(q, expect)
+    assert abs(kvgen.ppnd16(0.975) - 1.959963984540054) < 1e-14
+    assert kvgen.ppnd16(0.5) == 0.0
+
+
 def test_workloads_structure_full_size():
     bytes_expect = {1: 2 * 2**30, 2: 8 * 2**30, 3: 16 * 2**30, 4: 6 * 2**30}
     for cfg in (1, 2, 3, 4):

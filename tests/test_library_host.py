@@ -1,0 +1,167 @@
+"""Host-side checks of libkvpool.so that need no GPU.
+
+- every function the header declares is exported;
+- placement in the library (placement-only pools make no HIP call) equals the
+  oracle's placement bit for bit over random place/release sequences;
+- argument validation returns the documented error codes.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings
+from hypothesis import strategies as st
+
+import oracle
+from paper_2606_14779_amd import kvpool as K
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "kvpool.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kv_\w+)\s*\(", src)))
+
+
+def test_header_symbols_exported():
+    names = _declared_functions()
+    assert len(names) >= 16
+    lib = ctypes.CDLL(K.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(K.EXPORTED)
+
+
+def _pool(weights, caps, bb_layers=1):
+    spec = K.KVSpec(bb_layers, 1, 8, 16, 2, 0)      # chunk 256 B, block 512*L B
+    regions = [K.Region("host" if i % 2 == 0 else "staging", c, -1) for i, c in enumerate(caps)]
+    return K.KVPool(regions, weights, spec, device=-1), spec
+
+
+def test_counts_match_oracle_random():
+    rng = np.random.default_rng(1)
+    for _ in range(500):
+        N = int(rng.integers(1, 9))
+        w = rng.integers(1, 1 << 40, size=N, dtype=np.uint64)
+        n = int(rng.integers(0, 1 << 40))
+        assert np.array_equal(K.counts(w, n), oracle.counts(w, n))
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.lists(st.integers(1, 9), min_size=1, max_size=6), st.integers(1, 4),
+       st.lists(st.tuples(st.booleans(), st.integers(1, 90)), min_size=1, max_size=30))
+def test_placement_equals_oracle(weights, layers, ops):
+    bb = 2 * layers * 256
+    caps = [(w * 60 + 7) * bb + 3000 for w in weights]
+    lib_pool, spec = _pool(weights, caps, layers)
+    assert spec.block_bytes == bb
+    ora = oracle.Pool(weights, caps, bb)
+    live, req = [], 100
+    for is_release, n in ops:
+        if is_release and live:
+            r = live.pop(n % len(live))
+            assert ora.release(r) == 0
+            lib_pool.release(r)
+            continue
+        rc, om = ora.try_place(req, n)
+        if rc == 0:
+            lm = lib_pool.place(req, n)
+            assert np.array_equal(lm.view(np.uint8), om.view(np.uint8))
+            assert np.array_equal(lib_pool.lookup(req, n), om)
+            live.append(req)
+        else:
+            with pytest.raises(K.KVPoolError) as ei:
+                lib_pool.place(req, n)
+            assert ei.value.code == rc == -3
+        req += 1
+    lib_pool.close()
+
+
+def test_workload_scale_placement_equals_oracle():
+    from kvgen import workloads
+    for cfg in (1, 2, 3, 4, 5):
+        wl = workloads.make(cfg)
+        bb = wl.shape.block_bytes
+        w = [r.weight for r in wl.regions]
+        caps = [r.capacity_bytes for r in wl.regions]
+        spec = K.KVSpec(wl.shape.layers, wl.shape.kv_heads, wl.shape.head_dim)
+        lp = K.KVPool([K.Region(r.kind, r.capacity_bytes) for r in wl.regions], w, spec, device=-1)
+        op = oracle.Pool(w, caps, bb)
+        for q in wl.requests:
+            assert np.array_equal(lp.place(q.request_id, q.n_present), op.place(q.request_id, q.n_present))
+        lp.close()
+
+
+def _err(fn, *a):
+    with pytest.raises(K.KVPoolError) as ei:
+        fn(*a)
+    return ei.value.name
+
+
+def test_create_validation():
+    spec = K.KVSpec(2, 2, 8)
+    ok = [K.Region("host", 1 << 20)]
+    assert _err(K.KVPool, ok, [0], spec, -1) == "INVALID"                    # zero bandwidth
+    assert _err(K.KVPool, [K.Region("host", 100)], [1], spec, -1) == "INVALID"  # below a sector
+    assert _err(K.KVPool, ok, [1], K.KVSpec(2, 1, 3, 1, 2, 0), -1) == "INVALID"  # chunk 6 B
+    assert _err(K.KVPool, ok, [1], K.KVSpec(2, 4, 4, 16, 2, 1), -1) == "INVALID"  # token-major row 8 B
+    assert _err(K.KVPool, ok, [1], K.KVSpec(0, 2, 8), -1) == "INVALID"
+    assert _err(K.KVPool, ok, [1], K.KVSpec(2, 2, 8, 16, 2, 2), -1) == "INVALID"  # layout 2
+    assert _err(K.KVPool, [K.Region("staging", 1 << 20, 0)], [1], spec, -1) == "INVALID"
+    assert _err(K.KVPool, [K.Region("host", 1 << 20, -2)], [1], spec, -1) == "INVALID"
+    assert _err(K.KVPool, [], [], spec, -1) == "INVALID"
+    assert _err(K.KVPool, ok, [1], spec, -5) == "INVALID"
+
+
+def test_place_lookup_release_errors():
+    p, spec = _pool([1, 1], [1 << 20, 1 << 20])
+    assert _err(p.place, 1, 0) == "INVALID"
+    m = p.place(1, 5)
+    assert _err(p.place, 1, 5) == "INVALID"
+    assert _err(p.lookup, 1, 4) == "INVALID"
+    assert _err(p.lookup, 2, 5) == "NOTFOUND"
+    assert _err(p.release, 2) == "NOTFOUND"
+    assert _err(p.place, 3, 10 ** 6) == "NOSPACE"
+    assert np.array_equal(p.lookup(1, 5), m)
+    p.release(1)
+    assert _err(p.lookup, 1, 5) == "NOTFOUND"
+    # gen keeps counting across failures and releases
+    assert int(p.place(4, 1)["gen"][0]) == 2
+    p.close()
+
+
+def test_transfers_rejected_without_device():
+    p, spec = _pool([1], [1 << 20])
+    m = p.place(1, 2)
+    ptrs = [16 * 1024] * spec.num_layers
+    assert _err(p.retrieve, m, [0, 1], 2, ptrs, ptrs) == "INVALID"
+    assert _err(p.store, m, [0, 1], 2, ptrs, ptrs) == "INVALID"
+    assert _err(p.set_timing, True) == "INVALID"
+    assert _err(p.set_launch, 2, 0, 0, 0) == "INVALID"
+    assert _err(p.set_launch, 0, 0, 0, 64) == "INVALID"
+    p.set_launch(0, 0, 64, K.LAUNCH_NT_LOAD)
+    info = p.region_info(0)
+    assert info["device_ptr"] is None and info["capacity_bytes"] == 1 << 20
+    assert _err(p.region_info, 1) == "INVALID"
+    assert _err(p.region_read, 0, 0, 16) == "INVALID"
+    p.close()
+
+
+def test_glt_survives_many_requests():
+    """Table growth and backward-shift deletion keep every lookup exact."""
+    p, spec = _pool([3, 1, 2], [1 << 34] * 3)
+    rng = np.random.default_rng(0)
+    maps = {}
+    for r in range(400):
+        n = int(rng.integers(1, 60))
+        maps[r] = p.place(r, n)
+        if r % 3 == 0:
+            victim = int(rng.choice(list(maps)))
+            p.release(victim)
+            del maps[victim]
+    for r, m in maps.items():
+        assert np.array_equal(p.lookup(r, len(m)), m)
+    p.close()
