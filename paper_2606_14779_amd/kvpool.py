@@ -56,6 +56,15 @@ class _Timing(ctypes.Structure):
 assert ctypes.sizeof(_RegionDesc) == 24 and ctypes.sizeof(_KVSpec) == 24
 assert LOC_DTYPE.itemsize == 16
 
+# A process must hold one HIP runtime.  PyTorch-ROCm ships its own
+# libamdhip64 and asks for it by an unversioned name, which would not match a
+# runtime loaded earlier under its soname; loading torch first makes this
+# library bind to torch's runtime instead of mapping a second one.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
+
 if not os.path.exists(LIB_PATH):
     raise ImportError("libkvpool.so is not built (%s); run `python -m paper_2606_14779_amd.build`"
                       % LIB_PATH)

@@ -14,12 +14,17 @@ def say(*a):
     sys.stdout.flush()
 
 
-def oracle_expectation(wl, run, host_src):
+def oracle_pool(wl):
+    return oracle.Pool([r.weight for r in wl.regions], [r.capacity_bytes for r in wl.regions],
+                       wl.shape.block_bytes)
+
+
+def oracle_expectation(wl, run, host_src, ora=None):
     """Oracle placement, pool contents and destination cache for a whole workload."""
     sh = wl.shape
     L = sh.layers
     shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
-    ora = oracle.Pool([r.weight for r in wl.regions], [r.capacity_bytes for r in wl.regions], sh.block_bytes)
+    ora = ora or oracle_pool(wl)
     regions = [np.zeros(r.capacity_bytes, np.uint8) for r in wl.regions]
     expect = np.full(tuple(run.dst.shape), SENTINEL, np.uint16)
     maps = {}
@@ -37,9 +42,12 @@ def oracle_expectation(wl, run, host_src):
     return maps, regions, expect
 
 
-def check_full(wl, run, host_src):
-    """Element-by-element comparison of maps, pool bytes and destination."""
-    maps, regions, expect = oracle_expectation(wl, run, host_src)
+def check_full(wl, run, host_src, ora=None):
+    """Element-by-element comparison of maps, pool bytes and destination.
+
+    ``ora``: an oracle pool carrying the same place/release history as the
+    library's pool before the workload's placements (default: a fresh one)."""
+    maps, regions, expect = oracle_expectation(wl, run, host_src, ora)
     bb = wl.shape.block_bytes
     for q in wl.requests:
         assert np.array_equal(run.maps[q.request_id], maps[q.request_id]), "placement differs"

@@ -10,7 +10,7 @@ from kvgen import workloads
 from paper_2606_14779_amd import kvpool as K
 from paper_2606_14779_amd.runner import SENTINEL
 
-from gpu_util import check_full, check_sampled, make_run, say
+from gpu_util import check_full, check_sampled, make_run, oracle_pool, say
 
 pytestmark = pytest.mark.gpu
 
@@ -227,7 +227,10 @@ def test_release_and_reuse():
         run.fill_dst()
         run.retrieve_all()
         torch.cuda.synchronize()
-        check_full(wl, run, host)
+        ora = oracle_pool(wl)                                # same history: place, release
+        ora.place(q.request_id, q.n_present)
+        assert ora.release(q.request_id) == 0
+        check_full(wl, run, host, ora)
     finally:
         run.close()
 
