@@ -91,6 +91,31 @@ def probes(torch, K, run, nbytes):
     return res
 
 
+def pmc_traffic(wl_name, kernel_prefix):
+    """HBM/fabric bytes per dispatch from the committed rocprofv3 PMC summary of this workload.
+
+    Returns None when there is no summary or when kernels.hip changed since the
+    counters were taken (the summary records the source's sha256)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "retrieve_%s_pmc.txt" % wl_name)
+    if not os.path.exists(path):
+        return None
+    src = os.path.join(ROOT, "paper_2606_14779_amd", "csrc", "kernels.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    rec = {}
+    for line in open(path):
+        if line.startswith("kernels_hip_sha256:"):
+            rec["sha"] = line.split(":", 1)[1].strip()
+        elif line.startswith("kernel: ") and kernel_prefix in line:
+            fields = dict(f.strip().split("=", 1) for f in line.split("|")[1:])
+            rec["fetch_bytes"] = float(fields["fetch_bytes"])
+            rec["write_bytes"] = float(fields["write_bytes"])
+            rec["workgroups"] = int(fields["workgroups"])
+    if rec.get("sha") != sha or "fetch_bytes" not in rec:
+        return None
+    return rec
+
+
 def cpu_baseline(run, wl, budget_s=12.0, max_blocks=1024):
     """The oracle's gather (memcpy per chunk, one thread) on a bounded sample of the same request."""
     import numpy as np
@@ -205,6 +230,7 @@ def main():
         run.pool.last_timing()
     torch.cuda.synchronize()
 
+    log("warm-up done; timing %d steps" % args.steps)
     spans, host_ms, stage_ms = [], [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -242,29 +268,41 @@ def main():
         stage_only = {"ms_median": round(statistics.median(ks), 3), "ms_min": round(min(ks), 3),
                       "copied_gbps": round(stage_bytes / (statistics.median(ks) / 1e3) / 1e9, 1)}
 
+    log("timed region done: %.3f ms per retrieve" % ms_per_step)
     pr = None if args.no_probes else probes(torch, K, run, int(args.probe_gib * 2**30) // 4096 * 4096)
+    log("probes done")
     cpu = None if args.no_cpu_baseline else cpu_baseline(run, wl)
+    if cpu:
+        log("cpu baseline done")
 
     host_med = statistics.median(host_ms) if host_blocks else None
     stage_med = statistics.median(stage_ms) if stage_blocks else None
     dominant_ms = statistics.mean(host_ms) if host_blocks else statistics.mean(stage_ms)
     if host_blocks:
         achieved = host_bytes / (dominant_ms / 1e3) / 1e9
-        roof = {"bound": "pcie", "kernel": "chunk_copy_kernel (host-region class, zero-copy gather)",
+        tr = pmc_traffic(wl.name, "host_region_copy<true, 0,")
+        roof = {"bound": "pcie", "kernel": "host_region_copy (zero-copy gather from pinned host regions)",
                 "achieved": round(achieved, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
-                "frac": round(achieved / PCIE5_X16_GBPS, 4), "traffic": None,
+                "frac": round(achieved / PCIE5_X16_GBPS, 4),
+                "traffic": round(tr["fetch_bytes"] + tr["write_bytes"]) if tr else None,
+                "traffic_detail": {"fetch_bytes": round(tr["fetch_bytes"]), "write_bytes": round(tr["write_bytes"]),
+                                   "algorithmic_read_bytes": host_bytes, "algorithmic_write_bytes": host_bytes,
+                                   "source": "profiles/retrieve_%s_pmc.txt" % wl.name} if tr else None,
                 "bytes_per_launch": host_bytes,
                 "measured_peak": pr["host_link_peak_gbps"] if pr else None,
                 "frac_measured": round(achieved / pr["host_link_peak_gbps"], 4) if pr else None}
     else:
         achieved = 2 * stage_bytes / (dominant_ms / 1e3) / 1e9
-        roof = {"bound": "hbm", "kernel": "chunk_copy_kernel (staging class)", "achieved": round(achieved, 1),
+        roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather)", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None}
     hbm_roof = None
     if stage_only:
         a = 2 * stage_bytes / (stage_only["ms_median"] / 1e3) / 1e9      # bytes read + written in HBM
-        hbm_roof = {"bound": "hbm", "kernel": "chunk_copy_kernel (staging class, alone)", "achieved": round(a, 1),
+        trs = pmc_traffic(wl.name, "staging_region_copy<true, 0,")
+        hbm_roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather, alone)", "achieved": round(a, 1),
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(a / HBM_PEAK_GBPS, 4),
+                    "traffic": round(trs["fetch_bytes"] + trs["write_bytes"]) if trs else None,
+                    "algorithmic_bytes": 2 * stage_bytes,
                     "copied_gbps": stage_only["copied_gbps"],
                     "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
                     "frac_measured": round(stage_only["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}

@@ -169,8 +169,9 @@ struct CopyArgs {
     uint32_t layout;           // 0 head-major, 1 token-major
 };
 
+// cls: KVP_CLASS_HOST / KVP_CLASS_STAGING (selects the kernel entry point);
 // gather: pool -> cache (retrieve); !gather: cache -> pool (store)
-hipError_t launch_chunk_copy(const CopyArgs &a, bool gather, uint32_t grid, uint32_t flags,
+hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
                              hipStream_t s);
 hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid,
                              uint32_t flags, hipStream_t s);

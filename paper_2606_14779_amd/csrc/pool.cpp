@@ -506,7 +506,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         const LaunchCfg &lc = p.launch[c][op];
         check_hip(hipStreamWaitEvent(cls_stream[c], p.fork, 0), "hipStreamWaitEvent");
         if (p.timing) check_hip(hipEventRecord(p.t0[c], cls_stream[c]), "hipEventRecord");
-        check_hip(launch_chunk_copy(a, gather, lc.grid, lc.flags, cls_stream[c]), "kernel launch");
+        check_hip(launch_chunk_copy(a, c, gather, lc.grid, lc.flags, cls_stream[c]), "kernel launch");
         if (p.timing) {
             check_hip(hipEventRecord(p.t1[c], cls_stream[c]), "hipEventRecord");
             p.timed_ran[c] = true;
