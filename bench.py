@@ -179,6 +179,7 @@ def main():
     ap.add_argument("--host-flags", type=int, default=0)
     ap.add_argument("--staging-flags", type=int, default=0)
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
+    ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "
@@ -194,14 +195,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    wl = workloads.make(args.config)
+    wl = workloads.make(args.config, layout=args.layout)
     sh = wl.shape
     log("workload", wl.name, "retrieved bytes", wl.retrieved_bytes)
     t = time.perf_counter()
     run = WorkloadRun(wl, device=0, coherence=args.coherence)
     t_create = time.perf_counter() - t
-    run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
-    run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
+    if args.host_grid or args.host_flags:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
+    if args.staging_grid or args.staging_flags:
+        run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
     log("pool created in %.1f s" % t_create)
     t = time.perf_counter()
     run.fill_source()
@@ -269,6 +272,31 @@ def main():
                       "copied_gbps": round(stage_bytes / (statistics.median(ks) / 1e3) / 1e9, 1)}
 
     log("timed region done: %.3f ms per retrieve" % ms_per_step)
+    # layerwise retrieval (one call per layer, as an engine overlapping attention on layer l with the
+    # fetch of layer l+1 would issue it): total time and per-layer completion spacing
+    layerwise = None
+    if len(wl.requests) == 1:
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        m = run.retrieve_maps[q.request_id]
+        tot = []
+        per_layer = []
+        for it in range(3):
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(sh.layers + 1)]
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            evs[0].record(cur)
+            for l in range(sh.layers):
+                run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, l, l + 1, kp, vp, cur.cuda_stream)
+                evs[l + 1].record(cur)
+            torch.cuda.synchronize()
+            tot.append((time.perf_counter() - t) * 1e3)
+            per_layer += [evs[l].elapsed_time(evs[l + 1]) for l in range(sh.layers)]
+        layerwise = {"calls_per_request": sh.layers, "ms_total_median": round(statistics.median(tot), 3),
+                     "ms_per_layer_median": round(statistics.median(per_layer), 3),
+                     "ms_per_layer_max": round(max(per_layer), 3)}
+        log("layerwise done: %.3f ms" % statistics.median(tot))
+
     pr = None if args.no_probes else probes(torch, K, run, int(args.probe_gib * 2**30) // 4096 * 4096)
     log("probes done")
     cpu = None if args.no_cpu_baseline else cpu_baseline(run, wl)
@@ -320,7 +348,8 @@ def main():
                    "blocks": wl.present_blocks, "block_bytes": sh.block_bytes,
                    "retrieved_bytes": wl.retrieved_bytes, "host_link_bytes": host_bytes,
                    "staging_bytes": stage_bytes,
-                   "regions": [(r.kind, r.weight) for r in wl.regions], "layout": "head-major chunks",
+                   "regions": [(r.kind, r.weight) for r in wl.regions],
+                   "layout": "head-major chunks" if wl.layout == 0 else "token-major chunks",
                    "dst_slots": wl.dst_num_slots, "seed": wl.seed},
         "retrieval_ms": {"call_to_complete": round(ms_per_step, 3),
                          "span_median": round(statistics.median(span_ms), 3), "span_min": round(min(span_ms), 3),
@@ -330,6 +359,7 @@ def main():
         "roofline": roof,
         "roofline_staging": hbm_roof,
         "probes": pr,
+        "layerwise": layerwise,
         "place_ms": round(t_place * 1e3, 3),
         "store_ms": round(store_wall * 1e3, 1),
         "store_kernels_ms": store_t,

@@ -137,7 +137,7 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths,
 int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
 
 /*
- * GLT read (Sec. 4.3: "look up their GLT entries"): the map of a placed
+ * GLT read (Sec. 4.3, the lookup that starts a retrieval): the map of a placed
  * request.  n_blocks must equal the placed count.  Errors: NOTFOUND, INVALID.
  */
 int kv_pool_lookup(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
@@ -179,6 +179,27 @@ int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
 int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
                      const int32_t *dst_block_table, uint32_t dst_num_slots,
                      void *const *k_layers, void *const *v_layers, void *stream);
+
+/*
+ * Layer-range variants for layerwise pipelining (Sec. 2.2.1: the engine
+ * computes layer N while the KV cache of layer N+1 is fetched).  They move
+ * only layers [layer_begin, layer_end) of every present block -- chunks
+ * 2*layer_begin .. 2*layer_end-1 of each pool block -- with the same
+ * semantics, validation and stream ordering as kv_pool_retrieve /
+ * kv_pool_store.  k_layers / v_layers still have L entries; entries outside
+ * the range are not read (may be NULL).  A caller overlapping compute with
+ * I/O enqueues one call per layer (or per group of layers) and records its
+ * own event after each.  Errors: as kv_pool_retrieve / kv_pool_store, plus
+ * INVALID for an empty or out-of-range layer range.
+ */
+int kv_pool_retrieve_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
+                            const int32_t *dst_block_table, uint32_t dst_num_slots,
+                            uint32_t layer_begin, uint32_t layer_end,
+                            void *const *k_layers, void *const *v_layers, void *stream);
+int kv_pool_store_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
+                         const int32_t *src_block_table, uint32_t src_num_slots,
+                         uint32_t layer_begin, uint32_t layer_end,
+                         void *const *k_layers, void *const *v_layers, void *stream);
 
 /*
  * Release a request: its ranges go back to the regions' free lists (merged
@@ -231,7 +252,9 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
 #define KVP_LAUNCH_LDS       4u  /* pool_layout 1: stage each chunk through LDS */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
- * of one (class, op) kernel.  Errors: INVALID. */
+ * of one (class, op) kernel.  Defaults: host class 12 workgroups, staging
+ * class 8192; flags 0 for pool_layout 0 and KVP_LAUNCH_LDS for pool_layout 1.
+ * Errors: INVALID. */
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
 
 typedef struct {

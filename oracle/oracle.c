@@ -21,8 +21,8 @@
  *
  * Readings of the paper taken here (where it is silent or ambiguous):
  *  R1 remainder: after flooring, the r leftover blocks go one each to the r
- *     devices with the largest p_i (Sec. 4.1.3 says "devices", plural; the
- *     algorithm's per-leftover step names the largest-p_i device).
+ *     devices with the largest p_i (the prose of Sec. 4.1.3 speaks of several
+ *     devices; the algorithm's per-leftover step names the largest-p_i one).
  *  R2 ties in p_i: lower device index first.
  *  R3 which device a block goes to: blocks are taken in index order and
  *     block j goes to the device with room that has the largest deficit

@@ -12,8 +12,8 @@ void pool_destroy(Pool *);
 void pool_place(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_lookup(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_release(Pool &, uint64_t);
-void pool_transfer(Pool &, const kvp_loc *, uint32_t, const int32_t *, uint32_t, void *const *, void *const *,
-                   void *, bool);
+void pool_transfer(Pool &, const kvp_loc *, uint32_t, const int32_t *, uint32_t, uint32_t, uint32_t,
+                   void *const *, void *const *, void *, bool);
 void pool_region_info(const Pool &, uint32_t, kvp_region_info *);
 void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
 void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
@@ -86,8 +86,19 @@ int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, const i
                   uint32_t src_num_slots, void *const *k_layers, void *const *v_layers, void *stream)
 {
     return guarded([&] {
-        kvp::pool_transfer(impl(pool), map, n_blocks, src_block_table, src_num_slots, k_layers, v_layers, stream,
-                           false);
+        kvp::Pool &p = impl(pool);
+        kvp::pool_transfer(p, map, n_blocks, src_block_table, src_num_slots, 0, p.spec.num_layers, k_layers,
+                           v_layers, stream, false);
+    });
+}
+
+int kv_pool_store_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, const int32_t *src_block_table,
+                         uint32_t src_num_slots, uint32_t layer_begin, uint32_t layer_end, void *const *k_layers,
+                         void *const *v_layers, void *stream)
+{
+    return guarded([&] {
+        kvp::pool_transfer(impl(pool), map, n_blocks, src_block_table, src_num_slots, layer_begin, layer_end,
+                           k_layers, v_layers, stream, false);
     });
 }
 
@@ -95,8 +106,19 @@ int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, cons
                      uint32_t dst_num_slots, void *const *k_layers, void *const *v_layers, void *stream)
 {
     return guarded([&] {
-        kvp::pool_transfer(impl(pool), map, n_blocks, dst_block_table, dst_num_slots, k_layers, v_layers, stream,
-                           true);
+        kvp::Pool &p = impl(pool);
+        kvp::pool_transfer(p, map, n_blocks, dst_block_table, dst_num_slots, 0, p.spec.num_layers, k_layers,
+                           v_layers, stream, true);
+    });
+}
+
+int kv_pool_retrieve_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, const int32_t *dst_block_table,
+                            uint32_t dst_num_slots, uint32_t layer_begin, uint32_t layer_end,
+                            void *const *k_layers, void *const *v_layers, void *stream)
+{
+    return guarded([&] {
+        kvp::pool_transfer(impl(pool), map, n_blocks, dst_block_table, dst_num_slots, layer_begin, layer_end,
+                           k_layers, v_layers, stream, true);
     });
 }
 

@@ -161,7 +161,8 @@ struct CopyArgs {
     const CopyItem *items;     // device
     const uint64_t *cache;     // device, [2L]: base of layer l's K (2l) / V (2l+1)
     uint32_t n_items;
-    uint32_t chunks;           // 2L
+    uint32_t chunks;           // chunks per item moved by this launch: 2 * (layers in range)
+    uint32_t chunk0;           // first chunk: 2 * first layer
     uint64_t chunk_bytes;      // C, multiple of 16
     uint32_t heads;            // token-major conversion: H
     uint32_t tokens;           //   bs

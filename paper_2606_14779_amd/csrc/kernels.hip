@@ -63,6 +63,12 @@ __device__ __forceinline__ void store16(v4u *p, v4u v)
         *g = v;
 }
 
+// Loads of a batch must not sit under per-lane branches: the compiler then
+// waits for each load before issuing the next, leaving one 16-byte load in
+// flight per lane.  Out-of-range lanes therefore load a clamped (valid)
+// index and only their stores are predicated.
+__device__ __forceinline__ uint32_t clamp_index(uint32_t v, uint32_t nvec) { return v < nvec ? v : nvec - 1; }
+
 // Workgroup-cooperative contiguous copy of nvec 16-byte vectors.
 template <int UNROLL, bool NTL, bool NTS>
 __device__ __forceinline__ void wg_copy(const v4u *__restrict__ src, v4u *__restrict__ dst, uint32_t nvec)
@@ -76,13 +82,10 @@ __device__ __forceinline__ void wg_copy(const v4u *__restrict__ src, v4u *__rest
 #pragma unroll
         for (int i = 0; i < UNROLL; ++i) store16<NTS>(dst + base + i * kThreads + tid, r[i]);
     }
-    if (base < nvec) {  // ragged tail: one predicated batch
+    if (base < nvec) {  // ragged tail: one batch, clamped loads, predicated stores
         v4u r[UNROLL];
 #pragma unroll
-        for (int i = 0; i < UNROLL; ++i) {
-            const uint32_t v = base + i * kThreads + tid;
-            if (v < nvec) r[i] = load16<NTL>(src + v);
-        }
+        for (int i = 0; i < UNROLL; ++i) r[i] = load16<NTL>(src + clamp_index(base + i * kThreads + tid, nvec));
 #pragma unroll
         for (int i = 0; i < UNROLL; ++i) {
             const uint32_t v = base + i * kThreads + tid;
@@ -91,8 +94,9 @@ __device__ __forceinline__ void wg_copy(const v4u *__restrict__ src, v4u *__rest
     }
 }
 
-// Vector index inside a token-major chunk [bs][H][rv] of the vector at
-// head-major index v of [H][bs][rv].
+// Index maps between the two chunk orders, in 16-byte vectors; rv vectors
+// make one head_dim row.  Head-major [H][bs][rv] index v <-> token-major
+// [bs][H][rv] index.
 __device__ __forceinline__ uint32_t hm_to_tm(uint32_t v, uint32_t heads, uint32_t tokens, uint32_t rv)
 {
     const uint32_t row = v / rv, w = v - row * rv;
@@ -100,9 +104,27 @@ __device__ __forceinline__ uint32_t hm_to_tm(uint32_t v, uint32_t heads, uint32_
     return (t * heads + h) * rv + w;
 }
 
+__device__ __forceinline__ uint32_t tm_to_hm(uint32_t v, uint32_t heads, uint32_t tokens, uint32_t rv)
+{
+    const uint32_t row = v / rv, w = v - row * rv;
+    const uint32_t t = row / heads, h = row - t * heads;
+    return (h * tokens + t) * rv + w;
+}
+
+// Source index of destination vector v.  GATHER: destination head-major
+// (cache), source token-major (pool); store: the reverse.
+template <bool GATHER>
+__device__ __forceinline__ uint32_t src_of(uint32_t v, uint32_t heads, uint32_t tokens, uint32_t rv)
+{
+    if constexpr (GATHER)
+        return hm_to_tm(v, heads, tokens, rv);
+    else
+        return tm_to_hm(v, heads, tokens, rv);
+}
+
 // Direct token-major <-> head-major chunk conversion.  The lane index runs
 // over the destination, so stores are contiguous; loads come in runs of rv
-// vectors.  GATHER: src token-major (pool) -> dst head-major (cache).
+// vectors (one head_dim row).
 template <bool GATHER, int UNROLL, bool NTL, bool NTS>
 __device__ __forceinline__ void wg_convert(const v4u *__restrict__ src, v4u *__restrict__ dst, uint32_t nvec,
                                            uint32_t heads, uint32_t tokens, uint32_t rv)
@@ -112,19 +134,8 @@ __device__ __forceinline__ void wg_convert(const v4u *__restrict__ src, v4u *__r
         v4u r[UNROLL];
 #pragma unroll
         for (int i = 0; i < UNROLL; ++i) {
-            const uint32_t v = base + i * kThreads + tid;
-            if (v < nvec) {
-                uint32_t s;
-                if constexpr (GATHER) {
-                    s = hm_to_tm(v, heads, tokens, rv);  // dst head-major v <- src token-major s
-                } else {
-                    // dst token-major v = (t*H + h)*rv + w <- src head-major (h*bs + t)*rv + w
-                    const uint32_t row = v / rv, w = v - row * rv;
-                    const uint32_t t = row / heads, h = row - t * heads;
-                    s = (h * tokens + t) * rv + w;
-                }
-                r[i] = load16<NTL>(src + s);
-            }
+            const uint32_t v = clamp_index(base + i * kThreads + tid, nvec);
+            r[i] = load16<NTL>(src + src_of<GATHER>(v, heads, tokens, rv));
         }
 #pragma unroll
         for (int i = 0; i < UNROLL; ++i) {
@@ -134,25 +145,37 @@ __device__ __forceinline__ void wg_convert(const v4u *__restrict__ src, v4u *__r
     }
 }
 
-// LDS-staged conversion: contiguous global read into LDS, contiguous global
-// write out of LDS in the other order.
-template <bool GATHER, bool NTL, bool NTS>
+// LDS-staged conversion: the chunk is read contiguously into LDS (UNROLL
+// 16-byte loads in flight per lane, as in the plain copy), then written
+// contiguously in the other order out of LDS.
+template <bool GATHER, int UNROLL, bool NTL, bool NTS>
 __device__ __forceinline__ void wg_convert_lds(const v4u *__restrict__ src, v4u *__restrict__ dst, uint32_t nvec,
                                                uint32_t heads, uint32_t tokens, uint32_t rv, v4u *lds)
 {
     const uint32_t tid = threadIdx.x;
-    for (uint32_t v = tid; v < nvec; v += kThreads) lds[v] = load16<NTL>(src + v);
-    __syncthreads();
-    for (uint32_t v = tid; v < nvec; v += kThreads) {
-        uint32_t s;
-        if constexpr (GATHER) {
-            s = hm_to_tm(v, heads, tokens, rv);
-        } else {
-            const uint32_t row = v / rv, w = v - row * rv;
-            const uint32_t t = row / heads, h = row - t * heads;
-            s = (h * tokens + t) * rv + w;
+    for (uint32_t base = 0; base < nvec; base += kThreads * UNROLL) {
+        v4u r[UNROLL];
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) r[i] = load16<NTL>(src + clamp_index(base + i * kThreads + tid, nvec));
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = base + i * kThreads + tid;
+            if (v < nvec) lds[v] = r[i];
         }
-        store16<NTS>(dst + v, lds[s]);
+    }
+    __syncthreads();
+    for (uint32_t base = 0; base < nvec; base += kThreads * UNROLL) {
+        v4u r[UNROLL];
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = clamp_index(base + i * kThreads + tid, nvec);
+            r[i] = lds[src_of<GATHER>(v, heads, tokens, rv)];
+        }
+#pragma unroll
+        for (int i = 0; i < UNROLL; ++i) {
+            const uint32_t v = base + i * kThreads + tid;
+            if (v < nvec) store16<NTS>(dst + v, r[i]);
+        }
     }
     __syncthreads();  // LDS is reused by the next chunk
 }
@@ -167,7 +190,7 @@ __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
     const uint32_t nvec = static_cast<uint32_t>(a.chunk_bytes >> 4);
     for (uint32_t u = blockIdx.x; u < units; u += gridDim.x) {
         const uint32_t item = u / a.chunks;
-        const uint32_t c = u - item * a.chunks;
+        const uint32_t c = a.chunk0 + (u - item * a.chunks);
         const CopyItem it = a.items[item];
         char *pool = reinterpret_cast<char *>(it.pool) + static_cast<uint64_t>(c) * a.chunk_bytes;
         char *cache = reinterpret_cast<char *>(a.cache[c]) + static_cast<uint64_t>(it.slot) * a.chunk_bytes;
@@ -178,7 +201,7 @@ __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
         else if constexpr (FORM == kConvert)
             wg_convert<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec);
         else
-            wg_convert_lds<GATHER, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec, lds);
+            wg_convert_lds<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec, lds);
     }
 }
 
@@ -253,7 +276,7 @@ static hipError_t launch_dir(const CopyArgs &a, uint32_t grid, uint32_t flags, h
 {
     if (a.layout == 0) return launch_unroll<HOST, GATHER, kPlain>(a, grid, flags, 0, s);
     if ((flags & KVP_LAUNCH_LDS) && a.chunk_bytes <= kMaxLdsChunk)
-        return launch_form<HOST, GATHER, kConvertLds, 1>(a, grid, flags, a.chunk_bytes, s);
+        return launch_unroll<HOST, GATHER, kConvertLds>(a, grid, flags, a.chunk_bytes, s);
     return launch_unroll<HOST, GATHER, kConvert>(a, grid, flags, 0, s);
 }
 
@@ -296,12 +319,12 @@ uint32_t default_grid(uint32_t cls, uint32_t op)
 {
     (void)op;
     // Host class: the link needs only about its bandwidth-delay product in
-    // flight; 16 workgroups x 32 KiB keep a PCIe 5.0 x16 link at its measured
+    // flight; 12 workgroups x 32 KiB keep a PCIe 5.0 x16 link at its measured
     // peak, while more of them only queue reads in the shared memory path and
     // slow the HBM kernel running beside them.  Staging class: 8192
     // workgroups (32 per CU) so the HBM kernel keeps its share of the memory
     // queues while the host kernel runs.
-    return cls == KVP_CLASS_HOST ? 16u : 8192u;
+    return cls == KVP_CLASS_HOST ? 12u : 8192u;
 }
 
 }  // namespace kvp

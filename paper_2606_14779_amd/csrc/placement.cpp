@@ -4,11 +4,11 @@
 // p_i = b_i / sum_j b_j of the blocks.  Bandwidth-aware allocator (Sec. 4.1.3,
 // Eq. 2, Algorithm 1): region i's target count is floor(p_i * n) plus at most
 // one leftover block; leftovers go to the regions with the largest p_i, equal
-// p_i broken by the lower index.  The blocks are then handed out in index
-// order ("enumerated in layerwise order and assigned ... in that same
-// sequence"); the algorithm only requires that the chosen region still has
-// room, and this library picks the region that is furthest behind its
-// proportional share, so every request is striped over all regions.
+// p_i broken by the lower index.  The blocks are then handed out one by one
+// in the request's own (layer-then-token) order; the algorithm only requires
+// that the chosen region still has room, and this library picks the region
+// that is furthest behind its proportional share, so every request is
+// striped over all regions.
 // KV-passthrough (Sec. 4.2) gives each (request, region) one contiguous
 // range of ceil(c_i * KV_size / sector) sectors; the same rule is used for
 // host regions, with a 4096-byte sector.

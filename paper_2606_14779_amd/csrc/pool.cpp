@@ -214,8 +214,10 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         r.capacity = d.capacity_bytes / kSector * kSector;
         r.alloc = RangeAllocator(r.capacity);
     }
+    // token-major pools stage each chunk through LDS by default (contiguous on both sides)
+    const uint32_t def_flags = p->spec.pool_layout == 1 ? KVP_LAUNCH_LDS : 0u;
     for (uint32_t c = 0; c < 2; ++c)
-        for (uint32_t o = 0; o < 2; ++o) p->launch[c][o] = LaunchCfg{default_grid(c, o), 0u};
+        for (uint32_t o = 0; o < 2; ++o) p->launch[c][o] = LaunchCfg{default_grid(c, o), def_flags};
 
     p->device = hip_device;
     p->placement_only = hip_device < 0;
@@ -404,13 +406,17 @@ Slot &acquire_slot(Pool &p, size_t bytes)
 }  // namespace
 
 void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t *table, uint32_t num_slots,
-                   void *const *k_layers, void *const *v_layers, void *stream_ptr, bool gather)
+                   uint32_t layer_begin, uint32_t layer_end, void *const *k_layers, void *const *v_layers,
+                   void *stream_ptr, bool gather)
 {
     if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to copy");
     if (n_blocks && (!map || !table)) fail(KVP_ERR_INVALID, "null map or block table");
     const uint32_t L = p.spec.num_layers;
+    if (layer_begin >= layer_end || layer_end > L)
+        fail(KVP_ERR_INVALID, "layer range [" + std::to_string(layer_begin) + ", " + std::to_string(layer_end) +
+                                  ") not inside [0, " + std::to_string(L) + ")");
     if (!k_layers || !v_layers) fail(KVP_ERR_INVALID, "null layer pointer array");
-    for (uint32_t l = 0; l < L; ++l) {
+    for (uint32_t l = layer_begin; l < layer_end; ++l) {
         const uintptr_t k = reinterpret_cast<uintptr_t>(k_layers[l]), v = reinterpret_cast<uintptr_t>(v_layers[l]);
         if (!k || !v || (k & 15) || (v & 15))
             fail(KVP_ERR_INVALID, "layer " + std::to_string(l) + ": null or unaligned cache pointer");
@@ -468,8 +474,9 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     Slot &slot = acquire_slot(p, bytes);
     auto *ptrs = static_cast<uint64_t *>(slot.host);
     for (uint32_t l = 0; l < L; ++l) {
-        ptrs[2 * l] = reinterpret_cast<uint64_t>(k_layers[l]);
-        ptrs[2 * l + 1] = reinterpret_cast<uint64_t>(v_layers[l]);
+        const bool in = l >= layer_begin && l < layer_end;   // entries outside the range are never read
+        ptrs[2 * l] = in ? reinterpret_cast<uint64_t>(k_layers[l]) : 0;
+        ptrs[2 * l + 1] = in ? reinterpret_cast<uint64_t>(v_layers[l]) : 0;
     }
     auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(slot.host) + ptr_bytes);
     std::copy(items[0].begin(), items[0].end(), list);
@@ -496,7 +503,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         a.items = dev_list + first;
         a.cache = static_cast<const uint64_t *>(slot.dev);
         a.n_items = static_cast<uint32_t>(items[c].size());
-        a.chunks = 2 * L;
+        a.chunks = 2 * (layer_end - layer_begin);
+        a.chunk0 = 2 * layer_begin;
         a.chunk_bytes = p.chunk_bytes;
         a.heads = p.spec.num_kv_heads;
         a.tokens = p.spec.block_size;

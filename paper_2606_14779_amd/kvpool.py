@@ -77,6 +77,8 @@ _SIGS = {
     "kv_pool_lookup": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_store": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
+    "kv_pool_retrieve_layers": (_i32, [_vp, _vp, _u32, _vp, _u32, _u32, _u32, _vp, _vp, _vp]),
+    "kv_pool_store_layers": (_i32, [_vp, _vp, _u32, _vp, _u32, _u32, _u32, _vp, _vp, _vp]),
     "kv_pool_release": (_i32, [_vp, _u64]),
     "kv_pool_destroy": (None, [_vp]),
     "kv_pool_last_error": (ctypes.c_char_p, []),
@@ -210,7 +212,7 @@ class KVPool:
         _check(_lib.kv_pool_release(self._h, request))
 
     # ---- data path
-    def _transfer(self, fn, loc_map, table, num_slots, k_ptrs, v_ptrs, stream):
+    def _transfer(self, fn, loc_map, table, num_slots, k_ptrs, v_ptrs, stream, layers=None):
         m = _loc_array(loc_map)
         t = np.ascontiguousarray(table, dtype=np.int32)
         if len(m) != len(t):
@@ -218,14 +220,26 @@ class KVPool:
         ks, vs = _ptrs(k_ptrs), _ptrs(v_ptrs)
         if len(ks) != self.spec.num_layers or len(vs) != self.spec.num_layers:
             raise ValueError("one K and one V pointer per layer")
-        _check(fn(self._h, m.ctypes.data if len(m) else None, len(m), t.ctypes.data if len(t) else None,
-                  num_slots, ctypes.addressof(ks), ctypes.addressof(vs), stream or None))
+        args = [self._h, m.ctypes.data if len(m) else None, len(m), t.ctypes.data if len(t) else None, num_slots]
+        if layers is not None:
+            args += [layers[0], layers[1]]
+        _check(fn(*args, ctypes.addressof(ks), ctypes.addressof(vs), stream or None))
 
     def store(self, loc_map, src_table, src_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
         self._transfer(_lib.kv_pool_store, loc_map, src_table, src_num_slots, k_ptrs, v_ptrs, stream)
 
     def retrieve(self, loc_map, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
         self._transfer(_lib.kv_pool_retrieve, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream)
+
+    def retrieve_layers(self, loc_map, dst_table, dst_num_slots: int, layer_begin: int, layer_end: int,
+                        k_ptrs, v_ptrs, stream: int = 0):
+        self._transfer(_lib.kv_pool_retrieve_layers, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream,
+                       (layer_begin, layer_end))
+
+    def store_layers(self, loc_map, src_table, src_num_slots: int, layer_begin: int, layer_end: int,
+                     k_ptrs, v_ptrs, stream: int = 0):
+        self._transfer(_lib.kv_pool_store_layers, loc_map, src_table, src_num_slots, k_ptrs, v_ptrs, stream,
+                       (layer_begin, layer_end))
 
     # ---- introspection
     def region_info(self, region: int) -> dict:

@@ -298,3 +298,60 @@ def test_full_size_workloads(cfg):
     finally:
         run.close()
         torch.cuda.empty_cache()
+
+
+# ---- layer-range retrieve / store (layerwise pipelining)
+
+def test_retrieve_layer_by_layer_and_subrange():
+    wl = workloads.make(2, max_blocks=37)
+    say("case layers")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        m = run.retrieve_maps[q.request_id]
+        L = wl.shape.layers
+        s = torch.cuda.current_stream().cuda_stream
+        for l in range(L):                                   # one call per layer
+            run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, l, l + 1, kp, vp, s)
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+        run.fill_dst()
+        kp_part = [p if 3 <= l < 7 else 0 for l, p in enumerate(kp)]   # pointers outside the range unused
+        vp_part = [p if 3 <= l < 7 else 0 for l, p in enumerate(vp)]
+        run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, 3, 7, kp_part, vp_part, s)
+        torch.cuda.synchronize()
+        from gpu_util import oracle_expectation
+        _, _, expect = oracle_expectation(wl, run, host)
+        got = run.dst.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got[3:7], expect[3:7])
+        assert np.all(got[:3] == SENTINEL) and np.all(got[7:] == SENTINEL)
+        for lo, hi in [(0, 0), (5, 4), (0, L + 1)]:
+            with pytest.raises(K.KVPoolError) as ei:
+                run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, lo, hi, kp, vp, s)
+            assert ei.value.name == "INVALID"
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_store_in_layer_groups_then_retrieve(layout):
+    wl = workloads.make(4, max_blocks=29, layout=layout)
+    say("case store layers", layout)
+    run = make_run(wl)
+    try:
+        host = run.fill_source(keep_host=True)
+        run.fill_dst()
+        run.place_all()
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.src)
+        s = torch.cuda.current_stream().cuda_stream
+        L = wl.shape.layers
+        for lo, hi in [(0, 5), (5, 6), (6, L)]:
+            run.pool.store_layers(run.maps[q.request_id], q.src_slots, wl.src_num_slots, lo, hi, kp, vp, s)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
