@@ -180,6 +180,8 @@ def main():
     ap.add_argument("--staging-flags", type=int, default=0)
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
+    ap.add_argument("--layerwise", action="store_true",
+                    help="also time the request retrieved one layer per call (kv_pool_retrieve_layers)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "
@@ -275,7 +277,7 @@ def main():
     # layerwise retrieval (one call per layer, as an engine overlapping attention on layer l with the
     # fetch of layer l+1 would issue it): total time and per-layer completion spacing
     layerwise = None
-    if len(wl.requests) == 1:
+    if args.layerwise and len(wl.requests) == 1:
         q = wl.requests[0]
         kp, vp = run.layer_ptrs(run.dst)
         m = run.retrieve_maps[q.request_id]
