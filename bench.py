@@ -86,7 +86,18 @@ def probes(torch, K, run, nbytes):
                      "kernel_grid": bgrid, "memcpy_h2d_gbps": round(n / ms / 1e6, 2)})
     res["host_link"] = link
     res["host_link_peak_gbps"] = max([max(x["kernel_gbps"], x["memcpy_h2d_gbps"]) for x in link] or [0.0])
-    del a, b
+    # GPU -> host direction (the store path): writes into a separate pinned buffer
+    h = torch.empty(nbytes // 2, dtype=torch.int16, pin_memory=True)
+    best, bgrid = 0.0, 0
+    for grid in (8, 12, 16, 32):
+        ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(h.data_ptr(), b.data_ptr(), nbytes, grid,
+                                                               K.LAUNCH_NT_STORE, cur.cuda_stream), iters=2))
+        if nbytes / ms / 1e6 > best:
+            best, bgrid = nbytes / ms / 1e6, grid
+    ms = min(_events_ms(torch, lambda: K.probe_memcpy(h.data_ptr(), b.data_ptr(), nbytes, cur.cuda_stream), iters=2))
+    res["d2h"] = {"kernel_gbps": round(best, 2), "kernel_grid": bgrid, "memcpy_d2h_gbps": round(nbytes / ms / 1e6, 2)}
+    res["d2h_peak_gbps"] = max(res["d2h"]["kernel_gbps"], res["d2h"]["memcpy_d2h_gbps"])
+    del a, b, h
     torch.cuda.empty_cache()
     return res
 
@@ -165,6 +176,65 @@ def cpu_baseline(run, wl, budget_s=12.0, max_blocks=1024):
             "ms_per_request_extrapolated": round(q.n_present * sh.block_bytes / (gbps * 1e9) * 1e3, 1)}
 
 
+def ablation(args):
+    """Retrieval of the same request through differently organised pools (the
+    paper's ablation of its orchestrator, Sec. 5.3, restated for this path):
+    everything on one host region; striped over the two host regions only;
+    the configured 4:4:1:1:1:1 striping; and weights measured by the pool
+    organizer (per-region read probes, host regions sharing one link)."""
+    import copy
+
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    base = workloads.make(args.config)
+    n = base.requests[0].n_present
+
+    def variant(name, regions):
+        wl = copy.deepcopy(base)
+        wl.regions = regions
+        workloads._size_regions(wl.regions, [q.n_present for q in wl.requests], wl.shape.block_bytes)
+        run = WorkloadRun(wl, device=0)
+        run.setup()
+        counts = [int(x) for x in np.bincount(run.maps[wl.requests[0].request_id]["region"].astype(np.int64),
+                                             minlength=len(regions))]
+        ms = []
+        for i in range(args.warmup + args.steps):
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            run.retrieve_all()
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                ms.append((time.perf_counter() - t) * 1e3)
+        out = {"variant": name, "regions": [(r.kind, r.weight) for r in regions], "blocks": counts,
+               "ms_median": round(statistics.median(ms), 3),
+               "gbps": round(wl.retrieved_bytes / statistics.median(ms) / 1e6, 2)}
+        measured = None
+        if name.startswith("configured"):
+            measured = [int(x) for x in run.pool.measure_bandwidth(256 << 20, K.MEASURE_SHARED_LINK)]
+            out["measured_mbps_shared_link"] = measured
+        run.close()
+        torch.cuda.empty_cache()
+        log(json.dumps(out))
+        return out, measured
+
+    import numpy as np
+    R = workloads.RegionSpec
+    res = []
+    res.append(variant("single host region", [R("host", 1, 0)])[0])
+    res.append(variant("two host regions 1:1", [R("host", 1, 0), R("host", 1, 1)])[0])
+    conf, measured = variant("configured 4:4:1:1:1:1", copy.deepcopy(base.regions))
+    res.append(conf)
+    mregions = [R(r.kind, int(w), r.numa) for r, w in zip(base.regions, measured)]
+    res.append(variant("measured weights (shared host link)", mregions)[0])
+    print(json.dumps({"metric": "retrieval ms of one request by pool organisation (ablation)",
+                      "workload": base.name, "blocks": n, "retrieved_bytes": base.retrieved_bytes,
+                      "steps": args.steps, "warmup": args.warmup, "variants": res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,9 +250,14 @@ def main():
     ap.add_argument("--staging-flags", type=int, default=0)
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the bench line, compare pool organisations on the same request")
     ap.add_argument("--layerwise", action="store_true",
                     help="also time the request retrieved one layer per call (kv_pool_retrieve_layers)")
     args = ap.parse_args()
+    if args.gpus == 1 and args.ablation:
+        ablation(args)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "
               "--gpus %d is not supported" % args.gpus, file=sys.stderr)
@@ -274,6 +349,28 @@ def main():
                       "copied_gbps": round(stage_bytes / (statistics.median(ks) / 1e3) / 1e9, 1)}
 
     log("timed region done: %.3f ms per retrieve" % ms_per_step)
+    # store (offload) direction: the same request written back into its placed ranges
+    store = None
+    if len(wl.requests) == 1:
+        run.pool.set_timing(True)
+        hs, ss, walls = [], [], []
+        for i in range(args.warmup + args.steps):
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            run.store_all()
+            tm = run.pool.last_timing()
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                walls.append((time.perf_counter() - t) * 1e3)
+                hs.append(tm["host_ms"])
+                ss.append(tm["staging_ms"])
+        run.pool.set_timing(False)
+        store = {"ms_median": round(statistics.median(walls), 3),
+                 "gbps": round(wl.retrieved_bytes / statistics.median(walls) / 1e6, 2),
+                 "host_kernel_ms_median": round(statistics.median(hs), 3) if host_blocks else None,
+                 "staging_kernel_ms_median": round(statistics.median(ss), 3) if stage_blocks else None}
+        log("store timed: %.3f ms" % store["ms_median"])
+
     # layerwise retrieval (one call per layer, as an engine overlapping attention on layer l with the
     # fetch of layer l+1 would issue it): total time and per-layer completion spacing
     layerwise = None
@@ -337,6 +434,15 @@ def main():
                     "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
                     "frac_measured": round(stage_only["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}
 
+    store_roof = None
+    if store and host_blocks:
+        a = host_bytes / (store["host_kernel_ms_median"] / 1e3) / 1e9
+        store_roof = {"bound": "pcie", "kernel": "host_region_copy<false,...> (zero-copy store to pinned host regions)",
+                      "achieved": round(a, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
+                      "frac": round(a / PCIE5_X16_GBPS, 4),
+                      "measured_peak": pr["d2h_peak_gbps"] if pr else None,
+                      "frac_measured": round(a / pr["d2h_peak_gbps"], 4) if pr else None}
+
     ideal_ms = None
     if pr:
         ideal_ms = max(host_bytes / (pr["host_link_peak_gbps"] * 1e9) if host_bytes else 0.0,
@@ -361,6 +467,8 @@ def main():
         "roofline": roof,
         "roofline_staging": hbm_roof,
         "probes": pr,
+        "store": store,
+        "roofline_store": store_roof,
         "layerwise": layerwise,
         "place_ms": round(t_place * 1e3, 3),
         "store_ms": round(store_wall * 1e3, 1),

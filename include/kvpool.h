@@ -105,6 +105,9 @@ typedef struct kvp_pool kvp_pool;   /* opaque */
  *   regions[n_regions]   region descriptions; region i gets index i.
  *   bandwidths[n_regions] positive integer bandwidth weights b_i (any unit,
  *                        e.g. MB/s).  Integers keep floor(p_i * n) exact.
+ *                        NULL: measure them (kv_pool_measure_bandwidth with
+ *                        256 MiB per region, no flags) and use the result
+ *                        (not allowed for placement-only pools).
  *   spec                 KV shape; C = H*bs*D*elem_bytes must be a multiple
  *                        of 16 (and, for pool_layout 1, so must D*elem_bytes).
  *   hip_device           GPU ordinal.  -1 creates a placement-only pool: no
@@ -240,6 +243,31 @@ int kv_pool_region_read(kvp_pool *pool, uint32_t region, uint64_t offset, uint64
  * over n_regions bandwidths; host only.  Errors: INVALID. */
 int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, uint64_t *counts_out);
 
+/* ---- measured bandwidths (pool organizer, Sec. 4.1.2) ---- */
+
+#define KVP_MEASURE_SHARED_LINK 1u  /* divide host regions' rate by their count */
+
+/*
+ * Measure each region's read rate into HBM, the b_i of Eq. 1: the region's
+ * class kernel shape streams min(probe_bytes, capacity) bytes of the region
+ * into a scratch buffer (allocated for the call); best of 3 timed runs after
+ * a warm-up, in MB/s (>= 1).  Host regions are measured one at a time; all of
+ * them reach the GPU over the same host link, so KVP_MEASURE_SHARED_LINK
+ * divides their figure by the number of host regions.  Region contents are
+ * read, not changed.  Waits for the probes.
+ *   probe_bytes   in [64 KiB, 64 GiB].
+ *   mbps_out[n_regions]   caller-owned.
+ * Errors: INVALID (placement-only pool, bad flags or size), NOMEM, HIP.
+ */
+int kv_pool_measure_bandwidth(kvp_pool *pool, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_out);
+
+/*
+ * Replace the bandwidth weights b_i (Eq. 1) used by later kv_pool_place
+ * calls; existing placements keep their locations.
+ *   bandwidths[n_regions]  positive integers.  Errors: INVALID.
+ */
+int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
+
 /* ---- launch configuration and timing ---- */
 
 #define KVP_CLASS_HOST     0u   /* work on host regions (zero-copy kernel) */
@@ -252,9 +280,9 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
 #define KVP_LAUNCH_LDS       4u  /* pool_layout 1: stage each chunk through LDS */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
- * of one (class, op) kernel.  Defaults: host class 12 workgroups, staging
- * class 8192; flags 0 for pool_layout 0 and KVP_LAUNCH_LDS for pool_layout 1.
- * Errors: INVALID. */
+ * of one (class, op) kernel; flags replace the current ones.  Defaults: host
+ * class 12 workgroups, staging class 8192; KVP_LAUNCH_LDS for pool_layout 1;
+ * KVP_LAUNCH_NT_STORE for the host-class store.  Errors: INVALID. */
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
 
 typedef struct {

@@ -19,6 +19,8 @@ void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
 void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
 void pool_set_timing(Pool &, int);
 void pool_last_timing(Pool &, kvp_timing *);
+void pool_measure(Pool &, uint64_t, uint32_t, uint64_t *);
+void pool_set_bandwidths(Pool &, const uint64_t *);
 }  // namespace kvp
 
 struct kvp_pool {
@@ -155,6 +157,16 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
         if (!bandwidths || !counts_out) kvp::fail(KVP_ERR_INVALID, "null argument");
         kvp::target_counts(bandwidths, n_regions, n, counts_out);
     });
+}
+
+int kv_pool_measure_bandwidth(kvp_pool *pool, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_out)
+{
+    return guarded([&] { kvp::pool_measure(impl(pool), probe_bytes, flags, mbps_out); });
+}
+
+int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths)
+{
+    return guarded([&] { kvp::pool_set_bandwidths(impl(pool), bandwidths); });
 }
 
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)

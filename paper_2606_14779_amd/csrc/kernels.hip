@@ -315,16 +315,4 @@ hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_
     return hipGetLastError();
 }
 
-uint32_t default_grid(uint32_t cls, uint32_t op)
-{
-    (void)op;
-    // Host class: the link needs only about its bandwidth-delay product in
-    // flight; 12 workgroups x 32 KiB keep a PCIe 5.0 x16 link at its measured
-    // peak, while more of them only queue reads in the shared memory path and
-    // slow the HBM kernel running beside them.  Staging class: 8192
-    // workgroups (32 per CU) so the HBM kernel keeps its share of the memory
-    // queues while the host kernel runs.
-    return cls == KVP_CLASS_HOST ? 12u : 8192u;
-}
-
 }  // namespace kvp

@@ -37,6 +37,7 @@ namespace {
 constexpr uint64_t kSector = 4096;
 constexpr uint32_t kRingSlots = 8;
 constexpr size_t kSlotMin = 64 * 1024;
+constexpr uint64_t kCreateProbeBytes = 256ull << 20;   // per-region read probe when no bandwidths are given
 
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -182,26 +183,57 @@ void check_spec(const kvp_kv_spec &s, uint64_t &chunk, uint64_t &block)
     block = 2ull * s.num_layers * chunk;
 }
 
+void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps);
+
 }  // namespace
+
+// ---------------------------------------------------------------- launch policy
+
+uint32_t default_grid(uint32_t cls, uint32_t op)
+{
+    (void)op;
+    // Host class: the link needs only about its bandwidth-delay product in
+    // flight; 12 workgroups x 32 KiB keep a PCIe 5.0 x16 link at its measured
+    // peak, while more of them only queue reads in the shared memory path and
+    // slow the HBM kernel running beside them.  Staging class: 8192
+    // workgroups (32 per CU) so the HBM kernel keeps its share of the memory
+    // queues while the host kernel runs.
+    return cls == KVP_CLASS_HOST ? 12u : 8192u;
+}
+
+uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
+{
+    uint32_t f = 0;
+    // token-major pools stage each chunk through LDS (contiguous on both sides)
+    if (spec.pool_layout == 1) f |= KVP_LAUNCH_LDS;
+    // zero-copy writes to host memory: non-temporal stores measured 0.5 %
+    // faster and left the HBM kernel beside them less delayed
+    if (cls == KVP_CLASS_HOST && op == KVP_OP_STORE) f |= KVP_LAUNCH_NT_STORE;
+    return f;
+}
 
 // ---------------------------------------------------------------- create / destroy
 
 Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, uint32_t n_regions,
                   const kvp_kv_spec *spec, int hip_device)
 {
-    if (!regions || !bandwidths || !spec) fail(KVP_ERR_INVALID, "null argument");
+    if (!regions || !spec) fail(KVP_ERR_INVALID, "null argument");
+    if (!bandwidths && hip_device < 0) fail(KVP_ERR_INVALID, "a placement-only pool needs bandwidths");
     if (n_regions == 0 || n_regions > 4096) fail(KVP_ERR_INVALID, "n_regions must be in [1, 4096]");
     if (hip_device < -1) fail(KVP_ERR_INVALID, "hip_device must be >= -1");
     auto p = std::make_unique<Pool>();
     p->spec = *spec;
     check_spec(p->spec, p->chunk_bytes, p->block_bytes);
     p->regions.resize(n_regions);
-    p->bandwidth.assign(bandwidths, bandwidths + n_regions);
+    if (bandwidths)
+        p->bandwidth.assign(bandwidths, bandwidths + n_regions);
+    else
+        p->bandwidth.assign(n_regions, 1);   // replaced by the measurement below
     for (uint32_t i = 0; i < n_regions; ++i) {
         const kvp_region_desc &d = regions[i];
         const std::string who = "region " + std::to_string(i) + ": ";
         if (d.type != KVP_REGION_HOST && d.type != KVP_REGION_STAGING) fail(KVP_ERR_INVALID, who + "bad type");
-        if (bandwidths[i] == 0) fail(KVP_ERR_INVALID, who + "bandwidth must be positive");
+        if (p->bandwidth[i] == 0) fail(KVP_ERR_INVALID, who + "bandwidth must be positive");
         if (d.capacity_bytes < kSector) fail(KVP_ERR_INVALID, who + "capacity below one 4096-byte sector");
         if (d.numa_node < -1) fail(KVP_ERR_INVALID, who + "numa_node must be >= -1");
         if (d.type == KVP_REGION_HOST && d.flags > KVP_HOST_NONCOHERENT) fail(KVP_ERR_INVALID, who + "bad flags");
@@ -210,14 +242,12 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         if (d.reserved != 0) fail(KVP_ERR_INVALID, who + "reserved must be 0");
         Region &r = p->regions[i];
         r.desc = d;
-        r.bandwidth = bandwidths[i];
+        r.bandwidth = p->bandwidth[i];
         r.capacity = d.capacity_bytes / kSector * kSector;
         r.alloc = RangeAllocator(r.capacity);
     }
-    // token-major pools stage each chunk through LDS by default (contiguous on both sides)
-    const uint32_t def_flags = p->spec.pool_layout == 1 ? KVP_LAUNCH_LDS : 0u;
     for (uint32_t c = 0; c < 2; ++c)
-        for (uint32_t o = 0; o < 2; ++o) p->launch[c][o] = LaunchCfg{default_grid(c, o), def_flags};
+        for (uint32_t o = 0; o < 2; ++o) p->launch[c][o] = LaunchCfg{default_grid(c, o), default_flags(c, o, p->spec)};
 
     p->device = hip_device;
     p->placement_only = hip_device < 0;
@@ -240,6 +270,12 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         }
         p->ring.resize(kRingSlots);
         for (auto &s : p->ring) check_hip(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreate");
+        if (!bandwidths) {
+            // Eq. 1 from measured bandwidths: each region's read rate into HBM
+            std::vector<uint64_t> mbps(n_regions);
+            measure_regions(*p, kCreateProbeBytes, 0, mbps.data());
+            for (uint32_t i = 0; i < n_regions; ++i) p->bandwidth[i] = p->regions[i].bandwidth = mbps[i];
+        }
     } catch (...) {
         release_gpu(*p);
         throw;
@@ -533,6 +569,86 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     }
 }
 
+// ---------------------------------------------------------------- measured bandwidths (Sec. 4.1.2)
+
+namespace {
+
+// Read rate of every region (bytes from the region into HBM per second, in
+// MB/s): the region-class kernel's launch shape streams min(probe_bytes,
+// capacity) bytes from the region into a scratch buffer; best of 3 after one
+// warm-up.  Caller holds the pool lock and the device scope.
+void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps)
+{
+    probe_bytes &= ~15ull;
+    void *scratch = nullptr;
+    if (hipMalloc(&scratch, probe_bytes) != hipSuccess || !scratch)
+        fail(KVP_ERR_NOMEM, "probe scratch of " + std::to_string(probe_bytes) + " bytes");
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    try {
+        check_hip(hipEventCreate(&e0), "hipEventCreate");
+        check_hip(hipEventCreate(&e1), "hipEventCreate");
+        uint32_t n_host = 0;
+        for (size_t r = 0; r < p.regions.size(); ++r) {
+            const Region &reg = p.regions[r];
+            const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
+            n_host += cls == KVP_CLASS_HOST;
+            hipStream_t st = cls == KVP_CLASS_HOST ? p.s_host : p.s_stage;
+            const uint64_t n = std::min<uint64_t>(probe_bytes, reg.capacity) & ~15ull;
+            const LaunchCfg &lc = p.launch[cls][KVP_OP_RETRIEVE];
+            float best = 0.f;
+            for (int it = 0; it < 4; ++it) {
+                check_hip(hipEventRecord(e0, st), "hipEventRecord");
+                check_hip(launch_probe_copy(scratch, reg.dev, n, lc.grid, lc.flags & KVP_LAUNCH_NT_LOAD, st),
+                          "probe launch");
+                check_hip(hipEventRecord(e1, st), "hipEventRecord");
+                check_hip(hipEventSynchronize(e1), "hipEventSynchronize");
+                float ms = 0.f;
+                check_hip(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
+                if (it > 0 && (best == 0.f || ms < best)) best = ms;
+            }
+            const double rate = best > 0.f ? static_cast<double>(n) / (best * 1e3) : 1.0;   // MB/s
+            mbps[r] = std::max<uint64_t>(1, static_cast<uint64_t>(rate + 0.5));
+        }
+        // host regions reach the GPU over one shared link: split what one measured alone
+        if ((flags & KVP_MEASURE_SHARED_LINK) && n_host > 1)
+            for (size_t r = 0; r < p.regions.size(); ++r)
+                if (p.regions[r].desc.type == KVP_REGION_HOST) mbps[r] = std::max<uint64_t>(1, mbps[r] / n_host);
+    } catch (...) {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+        (void)hipFree(scratch);
+        throw;
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    (void)hipFree(scratch);
+}
+
+}  // namespace
+
+void pool_measure(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_out)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to measure");
+    if (!mbps_out) fail(KVP_ERR_INVALID, "null output");
+    if (flags & ~KVP_MEASURE_SHARED_LINK) fail(KVP_ERR_INVALID, "unknown flags");
+    if (probe_bytes < (1u << 16) || probe_bytes > (1ull << 36)) fail(KVP_ERR_INVALID, "probe_bytes outside [64 KiB, 64 GiB]");
+    std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+    measure_regions(p, probe_bytes, flags, mbps_out);
+}
+
+void pool_set_bandwidths(Pool &p, const uint64_t *bw)
+{
+    if (!bw) fail(KVP_ERR_INVALID, "null bandwidths");
+    for (size_t i = 0; i < p.regions.size(); ++i)
+        if (bw[i] == 0) fail(KVP_ERR_INVALID, "bandwidth of region " + std::to_string(i) + " is 0");
+    std::lock_guard<std::mutex> lock(p.mu);
+    for (size_t i = 0; i < p.regions.size(); ++i) {
+        p.bandwidth[i] = bw[i];
+        p.regions[i].bandwidth = bw[i];
+    }
+}
+
 // ---------------------------------------------------------------- introspection, launch config, timing
 
 void pool_region_info(const Pool &p, uint32_t region, kvp_region_info *out)
@@ -567,7 +683,7 @@ void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t
     if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS)) fail(KVP_ERR_INVALID, "unknown flags");
     if (grid > (1u << 20)) fail(KVP_ERR_INVALID, "grid too large");
     std::lock_guard<std::mutex> lock(p.mu);
-    p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op), flags};
+    p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op), flags};  // flags taken as given
 }
 
 void pool_set_timing(Pool &p, int enable)

@@ -25,6 +25,7 @@ ABSENT = 0xFFFFFFFF
 CLASS_HOST, CLASS_STAGING = 0, 1
 OP_RETRIEVE, OP_STORE = 0, 1
 LAUNCH_NT_LOAD, LAUNCH_NT_STORE, LAUNCH_LDS = 1, 2, 4
+MEASURE_SHARED_LINK = 1
 
 LOC_DTYPE = np.dtype([("region", "<u4"), ("gen", "<u4"), ("offset", "<u8")])
 
@@ -85,6 +86,8 @@ _SIGS = {
     "kv_pool_region_info": (_i32, [_vp, _u32, _vp]),
     "kv_pool_region_read": (_i32, [_vp, _u32, _u64, _u64, _vp]),
     "kv_pool_counts": (_i32, [_vp, _u32, _u64, _vp]),
+    "kv_pool_measure_bandwidth": (_i32, [_vp, _u64, _u32, _vp]),
+    "kv_pool_set_bandwidths": (_i32, [_vp, _vp]),
     "kv_pool_set_launch": (_i32, [_vp, _u32, _u32, _u32, _u32]),
     "kv_pool_set_timing": (_i32, [_vp, _i32]),
     "kv_pool_last_timing": (_i32, [_vp, _vp]),
@@ -171,16 +174,16 @@ class KVPool:
         for i, r in enumerate(regions):
             kind = {"host": REGION_HOST, "staging": REGION_STAGING}[r.kind]
             descs[i] = _RegionDesc(kind, r.numa_node, r.capacity_bytes, r.coherence, 0)
-        bw = np.ascontiguousarray(bandwidths, dtype=np.uint64)
-        if len(bw) != n:
+        bw = None if bandwidths is None else np.ascontiguousarray(bandwidths, dtype=np.uint64)
+        if bw is not None and len(bw) != n:
             raise ValueError("one bandwidth per region")
         self.spec = spec
         self.n_regions = n
         cs = _KVSpec(spec.num_layers, spec.num_kv_heads, spec.head_dim, spec.block_size,
                      spec.elem_bytes, spec.pool_layout)
         h = ctypes.c_void_p()
-        _check(_lib.kv_pool_create(ctypes.addressof(descs), bw.ctypes.data, n, ctypes.addressof(cs),
-                                   device, ctypes.byref(h)))
+        _check(_lib.kv_pool_create(ctypes.addressof(descs), None if bw is None else bw.ctypes.data, n,
+                                   ctypes.addressof(cs), device, ctypes.byref(h)))
         self._h = h
 
     def close(self):
@@ -253,6 +256,18 @@ class KVPool:
         assert out.flags.c_contiguous and out.nbytes >= nbytes
         _check(_lib.kv_pool_region_read(self._h, region, offset, nbytes, out.ctypes.data))
         return out
+
+    # ---- measured bandwidths
+    def measure_bandwidth(self, probe_bytes: int = 256 << 20, flags: int = 0) -> np.ndarray:
+        out = np.zeros(self.n_regions, dtype=np.uint64)
+        _check(_lib.kv_pool_measure_bandwidth(self._h, probe_bytes, flags, out.ctypes.data))
+        return out
+
+    def set_bandwidths(self, bandwidths) -> None:
+        bw = np.ascontiguousarray(bandwidths, dtype=np.uint64)
+        if len(bw) != self.n_regions:
+            raise ValueError("one bandwidth per region")
+        _check(_lib.kv_pool_set_bandwidths(self._h, bw.ctypes.data))
 
     # ---- launch configuration and timing
     def set_launch(self, cls: int, op: int, grid: int = 0, flags: int = 0) -> None:

@@ -165,3 +165,17 @@ def test_glt_survives_many_requests():
     for r, m in maps.items():
         assert np.array_equal(p.lookup(r, len(m)), m)
     p.close()
+
+
+def test_set_bandwidths_changes_later_placements():
+    p, spec = _pool([1, 1, 1], [1 << 24] * 3)
+    p.set_bandwidths([5, 1, 2])
+    ora = oracle.Pool([5, 1, 2], [1 << 24] * 3, spec.block_bytes)
+    assert np.array_equal(p.place(1, 41), ora.place(1, 41))
+    assert _err(p.set_bandwidths, [1, 0, 1]) == "INVALID"
+    with pytest.raises(ValueError):
+        p.set_bandwidths([1, 1])
+    assert _err(p.measure_bandwidth) == "INVALID"          # no memory to measure
+    p.close()
+    with pytest.raises(K.KVPoolError):
+        K.KVPool([K.Region("host", 1 << 20)], None, K.KVSpec(1, 1, 8), device=-1)

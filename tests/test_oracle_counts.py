@@ -49,7 +49,18 @@ def test_counts_closed_form(weights, n):
     assert sum(c) == n                                       # sum constraint of Eq. (2)
     assert all(ci - fi in (0, 1) for ci, fi in zip(c, fl))   # r_i in {0, 1}
     W = sum(weights)
-    assert all(abs(Fraction(ci) - Fraction(w * n, W)) < 1 for ci, w in zip(c, weights))
+    # within one block: the deviation reaches exactly 1 only when a device
+    # whose share p_i*n is an integer receives one of the leftovers
+    assert all(abs(Fraction(ci) - Fraction(w * n, W)) <= 1 for ci, w in zip(c, weights))
+    for ci, w in zip(c, weights):
+        if abs(Fraction(ci) - Fraction(w * n, W)) == 1:
+            assert (w * n) % W == 0 and ci == w * n // W + 1
+
+
+def test_leftover_to_device_with_integral_share():
+    """2:1:1 at n = 2: shares 1, 1/2, 1/2; the one leftover goes to the largest p_i
+    (device 0), whose share was already whole -- one block above its share."""
+    assert list(oracle.counts([2, 1, 1], 2)) == [2, 0, 0]
 
 
 @settings(max_examples=100, deadline=None)
