@@ -184,6 +184,17 @@ int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
                      void *const *k_layers, void *const *v_layers, void *stream);
 
 /*
+ * Retrieve by request (Sec. 4.3 as one call): read the GLT entries of blocks
+ * 0..n_blocks-1 of request_id, then retrieve them exactly as kv_pool_retrieve
+ * does with that map.  n_blocks must equal the placed count.
+ *   dst_block_table[n_blocks]  destination slot of every block.
+ * Errors: NOTFOUND, INVALID, HIP.
+ */
+int kv_pool_retrieve_request(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks,
+                             const int32_t *dst_block_table, uint32_t dst_num_slots,
+                             void *const *k_layers, void *const *v_layers, void *stream);
+
+/*
  * Layer-range variants for layerwise pipelining (Sec. 2.2.1: the engine
  * computes layer N while the KV cache of layer N+1 is fetched).  They move
  * only layers [layer_begin, layer_end) of every present block -- chunks

@@ -3,6 +3,7 @@
 
 #include <new>
 #include <string>
+#include <vector>
 
 #include "internal.hpp"
 
@@ -11,6 +12,7 @@ Pool *pool_create(const kvp_region_desc *, const uint64_t *, uint32_t, const kvp
 void pool_destroy(Pool *);
 void pool_place(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_lookup(Pool &, uint64_t, uint32_t, kvp_loc *);
+void pool_lookup_vector(Pool &, uint64_t, uint32_t, std::vector<kvp_loc> &);
 void pool_release(Pool &, uint64_t);
 void pool_transfer(Pool &, const kvp_loc *, uint32_t, const int32_t *, uint32_t, uint32_t, uint32_t,
                    void *const *, void *const *, void *, bool);
@@ -120,6 +122,19 @@ int kv_pool_retrieve_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_block
 {
     return guarded([&] {
         kvp::pool_transfer(impl(pool), map, n_blocks, dst_block_table, dst_num_slots, layer_begin, layer_end,
+                           k_layers, v_layers, stream, true);
+    });
+}
+
+int kv_pool_retrieve_request(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks,
+                             const int32_t *dst_block_table, uint32_t dst_num_slots, void *const *k_layers,
+                             void *const *v_layers, void *stream)
+{
+    return guarded([&] {
+        kvp::Pool &p = impl(pool);
+        std::vector<kvp_loc> map;
+        kvp::pool_lookup_vector(p, request_id, n_blocks, map);
+        kvp::pool_transfer(p, map.data(), n_blocks, dst_block_table, dst_num_slots, 0, p.spec.num_layers,
                            k_layers, v_layers, stream, true);
     });
 }

@@ -351,10 +351,10 @@ void pool_place(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
     p.requests.emplace(request, std::move(rec));
 }
 
-void pool_lookup(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
+namespace {
+
+void lookup_locked(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
 {
-    if (!out && n_blocks) fail(KVP_ERR_INVALID, "map_out is null");
-    std::lock_guard<std::mutex> lock(p.mu);
     auto it = p.requests.find(request);
     if (it == p.requests.end()) fail(KVP_ERR_NOTFOUND, "request " + std::to_string(request) + " is not placed");
     if (it->second->n_blocks != n_blocks)
@@ -365,6 +365,22 @@ void pool_lookup(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
         if (!e) fail(KVP_ERR_NOTFOUND, "GLT entry missing");
         out[j] = kvp_loc{e->region, e->gen, e->offset};
     }
+}
+
+}  // namespace
+
+void pool_lookup(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
+{
+    if (!out && n_blocks) fail(KVP_ERR_INVALID, "map_out is null");
+    std::lock_guard<std::mutex> lock(p.mu);
+    lookup_locked(p, request, n_blocks, out);
+}
+
+void pool_lookup_vector(Pool &p, uint64_t request, uint32_t n_blocks, std::vector<kvp_loc> &out)
+{
+    out.resize(n_blocks);
+    std::lock_guard<std::mutex> lock(p.mu);
+    lookup_locked(p, request, n_blocks, out.data());
 }
 
 void pool_release(Pool &p, uint64_t request)

@@ -78,6 +78,7 @@ _SIGS = {
     "kv_pool_lookup": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_store": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
+    "kv_pool_retrieve_request": (_i32, [_vp, _u64, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve_layers": (_i32, [_vp, _vp, _u32, _vp, _u32, _u32, _u32, _vp, _vp, _vp]),
     "kv_pool_store_layers": (_i32, [_vp, _vp, _u32, _vp, _u32, _u32, _u32, _vp, _vp, _vp]),
     "kv_pool_release": (_i32, [_vp, _u64]),
@@ -233,6 +234,15 @@ class KVPool:
 
     def retrieve(self, loc_map, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
         self._transfer(_lib.kv_pool_retrieve, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream)
+
+    def retrieve_request(self, request: int, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
+        t = np.ascontiguousarray(dst_table, dtype=np.int32)
+        ks, vs = _ptrs(k_ptrs), _ptrs(v_ptrs)
+        if len(ks) != self.spec.num_layers or len(vs) != self.spec.num_layers:
+            raise ValueError("one K and one V pointer per layer")
+        _check(_lib.kv_pool_retrieve_request(self._h, request, len(t), t.ctypes.data if len(t) else None,
+                                             dst_num_slots, ctypes.addressof(ks), ctypes.addressof(vs),
+                                             stream or None))
 
     def retrieve_layers(self, loc_map, dst_table, dst_num_slots: int, layer_begin: int, layer_end: int,
                         k_ptrs, v_ptrs, stream: int = 0):

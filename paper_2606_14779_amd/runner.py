@@ -3,7 +3,8 @@
 A ``WorkloadRun`` owns the pool (``kv_pool_create``), the engine's source and
 destination paged caches (torch tensors: device memory only), the placement
 maps (``kv_pool_place``) and the offload (``kv_pool_store``).  Retrieval is a
-single ``kv_pool_retrieve`` call per request.  The tests and the bench drive
+single ``kv_pool_retrieve_request`` call per request (``kv_pool_retrieve``
+with an explicit map when part of the context is absent).  The tests and the bench drive
 the hot path through this class; it performs no copy of its own besides
 putting the seeded source values into GPU memory.
 """
@@ -20,8 +21,7 @@ SENTINEL = 0x7FA5  # a bf16 NaN pattern that the generator never produces
 
 
 class WorkloadRun:
-    def __init__(self, wl: Workload, device: int = 0, coherence: int = K.HOST_DEFAULT,
-                 numa_nodes=None, retrieve_grid: int = 0, retrieve_flags: int = 0):
+    def __init__(self, wl: Workload, device: int = 0, coherence: int = K.HOST_DEFAULT, numa_nodes=None):
         import torch
         self.torch = torch
         self.wl = wl
@@ -86,10 +86,15 @@ class WorkloadRun:
             self.pool.store(self.maps[q.request_id], q.src_slots, self.wl.src_num_slots, kp, vp, s.cuda_stream)
 
     def retrieve(self, q, stream=None):
+        """One request: by request id (GLT lookup inside the library) when the
+        whole context is present, else with the map whose tail is absent."""
         kp, vp = self.layer_ptrs(self.dst)
         s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
-        self.pool.retrieve(self.retrieve_maps[q.request_id], q.dst_slots, self.wl.dst_num_slots, kp, vp,
-                           s.cuda_stream)
+        if q.n_present == q.n_blocks:
+            self.pool.retrieve_request(q.request_id, q.dst_slots, self.wl.dst_num_slots, kp, vp, s.cuda_stream)
+        else:
+            self.pool.retrieve(self.retrieve_maps[q.request_id], q.dst_slots, self.wl.dst_num_slots, kp, vp,
+                               s.cuda_stream)
 
     def retrieve_all(self):
         """One retrieve per request; request i on stream i % n_streams (forked from the current stream)."""

@@ -377,3 +377,51 @@ def test_measured_bandwidths_drive_placement():
         import oracle
         ora = oracle.Pool(bw, [r.capacity_bytes for r in regions], spec.block_bytes)
         assert np.array_equal(p.place(1, 300), ora.place(1, 300))
+
+
+def test_concurrent_retrieves_from_threads():
+    """store/retrieve may be called from several threads on different streams."""
+    import threading
+    wl = workloads.make(5, max_blocks=80)
+    say("case threads")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        streams = [torch.cuda.Stream() for _ in wl.requests]
+        cur = torch.cuda.current_stream()
+        for s in streams:
+            s.wait_stream(cur)
+        errs = []
+
+        def work(i, q):
+            try:
+                for _ in range(3):                           # idempotent: same blocks, same slots
+                    run.retrieve(q, streams[i])
+            except Exception as e:                           # reported below
+                errs.append(e)
+
+        ts = [threading.Thread(target=work, args=(i, q)) for i, q in enumerate(wl.requests)]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        torch.cuda.synchronize()
+        assert not errs, errs
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def test_retrieve_request_by_id_errors():
+    wl = workloads.make(1, max_blocks=8)
+    run = make_run(wl)
+    try:
+        run.setup()
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        for req, n, name in [(99, q.n_blocks, "NOTFOUND"), (q.request_id, q.n_blocks - 1, "INVALID")]:
+            with pytest.raises(K.KVPoolError) as ei:
+                run.pool.retrieve_request(req, q.dst_slots[:n], wl.dst_num_slots, kp, vp, 0)
+            assert ei.value.name == name
+    finally:
+        run.close()

@@ -179,3 +179,56 @@ def test_set_bandwidths_changes_later_placements():
     p.close()
     with pytest.raises(K.KVPoolError):
         K.KVPool([K.Region("host", 1 << 20)], None, K.KVSpec(1, 1, 8), device=-1)
+
+
+def test_placement_from_threads_keeps_invariants():
+    """place / lookup / release from several threads: every live map stays valid."""
+    import threading
+    weights = [4, 4, 1, 1, 1, 1]
+    bb = 512
+    caps = [1 << 26] * 6
+    p = K.KVPool([K.Region("host", c) for c in caps], weights, K.KVSpec(1, 1, 8), device=-1)
+    live, lock, errs = {}, threading.Lock(), []
+
+    def work(t):
+        rng = np.random.default_rng(t)
+        try:
+            for i in range(150):
+                req = t * 100000 + i
+                n = int(rng.integers(1, 300))
+                m = p.place(req, n)
+                assert np.array_equal(p.lookup(req, n), m)
+                with lock:
+                    live[req] = m
+                if rng.random() < 0.4:
+                    with lock:
+                        victim = live.pop(req)
+                    p.release(req)
+                    assert len(victim) == n
+        except Exception as e:            # reported below
+            errs.append(e)
+
+    ts = [threading.Thread(target=work, args=(t,)) for t in range(6)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert not errs, errs
+    spans = [[] for _ in weights]
+    gens = set()
+    for req, m in live.items():
+        c = oracle.counts(weights, len(m))
+        reg = m["region"].astype(np.int64)
+        assert list(np.bincount(reg, minlength=6)) == [int(x) for x in c]
+        gens.add(int(m["gen"][0]))
+        for i in range(6):
+            offs = np.sort(m["offset"][reg == i].astype(np.int64))
+            if len(offs):
+                assert np.all(offs == offs[0] + bb * np.arange(len(offs)))
+                spans[i].append((int(offs[0]), int(offs[-1]) + bb))
+        assert np.array_equal(p.lookup(req, len(m)), m)
+    assert len(gens) == len(live)
+    for s in spans:
+        s.sort()
+        assert all(a[1] <= b[0] for a, b in zip(s, s[1:]))
+    p.close()
