@@ -305,30 +305,35 @@ def main():
     host_bytes, stage_bytes = host_blocks * sh.block_bytes, stage_blocks * sh.block_bytes
 
     cur = torch.cuda.current_stream()
+    run.pool.set_timing(False)
     for _ in range(args.warmup):
         run.retrieve_all()
-        run.pool.last_timing()
     torch.cuda.synchronize()
 
+    # timed region: K retrieves back to back; the library records HIP events
+    # around each kernel on the stream it runs on, summarised afterwards
     log("warm-up done; timing %d steps" % args.steps)
-    spans, host_ms, stage_ms = [], [], []
+    run.pool.set_timing(True)
+    spans, enqueue_ms = [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.record(cur)
+        tq = time.perf_counter()
         run.retrieve_all()
+        enqueue_ms.append((time.perf_counter() - tq) * 1e3)
         e.record(cur)
-        tm = run.pool.last_timing()       # waits for this step's kernels
-        host_ms.append(tm["host_ms"])
-        stage_ms.append(tm["staging_ms"])
         spans.append((s, e))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    summ = run.pool.timing_summary()
+    run.pool.set_timing(False)
     span_ms = [s.elapsed_time(e) for s, e in spans]
     ms_per_step = wall / args.steps * 1e3
     gbps = wl.retrieved_bytes / (ms_per_step / 1e3) / 1e9
-    run.pool.set_timing(False)
+    host_avg = summ["host_ms_sum"] / summ["host_calls"] if summ["host_calls"] else None
+    stage_avg = summ["staging_ms_sum"] / summ["staging_calls"] if summ["staging_calls"] else None
 
     # staging-side gather alone (HBM->HBM), from a map without the host blocks
     stage_only = None
@@ -338,38 +343,39 @@ def main():
         host_idx = [i for i, r in enumerate(wl.regions) if r.kind == "host"]
         m["region"][np.isin(m["region"], host_idx)] = K.ABSENT
         kp, vp = run.layer_ptrs(run.dst)
-        run.pool.set_timing(True)
-        ks = []
-        for _ in range(args.warmup + args.steps):
+        for _ in range(args.warmup):
             run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
-            ks.append(run.pool.last_timing()["staging_ms"])
+        torch.cuda.synchronize()
+        run.pool.set_timing(True)
+        for _ in range(args.steps):
+            run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
+        ss = run.pool.timing_summary()
         run.pool.set_timing(False)
-        ks = ks[args.warmup:]
-        stage_only = {"ms_median": round(statistics.median(ks), 3), "ms_min": round(min(ks), 3),
-                      "copied_gbps": round(stage_bytes / (statistics.median(ks) / 1e3) / 1e9, 1)}
+        avg = ss["staging_ms_sum"] / ss["staging_calls"]
+        stage_only = {"ms_avg": round(avg, 3), "ms_min": round(ss["staging_ms_min"], 3),
+                      "copied_gbps": round(stage_bytes / (avg / 1e3) / 1e9, 1)}
 
     log("timed region done: %.3f ms per retrieve" % ms_per_step)
     # store (offload) direction: the same request written back into its placed ranges
     store = None
     if len(wl.requests) == 1:
-        run.pool.set_timing(True)
-        hs, ss, walls = [], [], []
-        for i in range(args.warmup + args.steps):
-            torch.cuda.synchronize()
-            t = time.perf_counter()
+        for _ in range(args.warmup):
             run.store_all()
-            tm = run.pool.last_timing()
-            torch.cuda.synchronize()
-            if i >= args.warmup:
-                walls.append((time.perf_counter() - t) * 1e3)
-                hs.append(tm["host_ms"])
-                ss.append(tm["staging_ms"])
+        torch.cuda.synchronize()
+        run.pool.set_timing(True)
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            run.store_all()
+        torch.cuda.synchronize()
+        st_ms = (time.perf_counter() - t) / args.steps * 1e3
+        sm = run.pool.timing_summary()
         run.pool.set_timing(False)
-        store = {"ms_median": round(statistics.median(walls), 3),
-                 "gbps": round(wl.retrieved_bytes / statistics.median(walls) / 1e6, 2),
-                 "host_kernel_ms_median": round(statistics.median(hs), 3) if host_blocks else None,
-                 "staging_kernel_ms_median": round(statistics.median(ss), 3) if stage_blocks else None}
-        log("store timed: %.3f ms" % store["ms_median"])
+        store = {"ms_per_store": round(st_ms, 3),
+                 "gbps": round(wl.retrieved_bytes / st_ms / 1e6, 2),
+                 "host_kernel_ms_avg": round(sm["host_ms_sum"] / sm["host_calls"], 3) if sm["host_calls"] else None,
+                 "staging_kernel_ms_avg":
+                     round(sm["staging_ms_sum"] / sm["staging_calls"], 3) if sm["staging_calls"] else None}
+        log("store timed: %.3f ms" % st_ms)
 
     # layerwise retrieval (one call per layer, as an engine overlapping attention on layer l with the
     # fetch of layer l+1 would issue it): total time and per-layer completion spacing
@@ -402,9 +408,7 @@ def main():
     if cpu:
         log("cpu baseline done")
 
-    host_med = statistics.median(host_ms) if host_blocks else None
-    stage_med = statistics.median(stage_ms) if stage_blocks else None
-    dominant_ms = statistics.mean(host_ms) if host_blocks else statistics.mean(stage_ms)
+    dominant_ms = host_avg if host_blocks else stage_avg
     if host_blocks:
         achieved = host_bytes / (dominant_ms / 1e3) / 1e9
         tr = pmc_traffic(wl.name, "host_region_copy<true, 0,")
@@ -424,7 +428,7 @@ def main():
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None}
     hbm_roof = None
     if stage_only:
-        a = 2 * stage_bytes / (stage_only["ms_median"] / 1e3) / 1e9      # bytes read + written in HBM
+        a = 2 * stage_bytes / (stage_only["ms_avg"] / 1e3) / 1e9         # bytes read + written in HBM
         trs = pmc_traffic(wl.name, "staging_region_copy<true, 0,")
         hbm_roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather, alone)", "achieved": round(a, 1),
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(a / HBM_PEAK_GBPS, 4),
@@ -436,7 +440,7 @@ def main():
 
     store_roof = None
     if store and host_blocks:
-        a = host_bytes / (store["host_kernel_ms_median"] / 1e3) / 1e9
+        a = host_bytes / (store["host_kernel_ms_avg"] / 1e3) / 1e9
         store_roof = {"bound": "pcie", "kernel": "host_region_copy<false,...> (zero-copy store to pinned host regions)",
                       "achieved": round(a, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
                       "frac": round(a / PCIE5_X16_GBPS, 4),
@@ -461,9 +465,10 @@ def main():
                    "dst_slots": wl.dst_num_slots, "seed": wl.seed},
         "retrieval_ms": {"call_to_complete": round(ms_per_step, 3),
                          "span_median": round(statistics.median(span_ms), 3), "span_min": round(min(span_ms), 3),
-                         "host_kernel_median": round(host_med, 3) if host_med else None,
-                         "staging_kernel_median": round(stage_med, 3) if stage_med else None,
-                         "ideal_at_measured_peaks": round(ideal_ms, 3) if ideal_ms else None},
+                         "host_kernel_avg": round(host_avg, 3) if host_avg else None,
+                         "staging_kernel_avg": round(stage_avg, 3) if stage_avg else None,
+                         "ideal_at_measured_peaks": round(ideal_ms, 3) if ideal_ms else None,
+                         "host_enqueue_median": round(statistics.median(enqueue_ms), 3)},
         "roofline": roof,
         "roofline_staging": hbm_roof,
         "probes": pr,

@@ -304,13 +304,29 @@ typedef struct {
 } kvp_timing;
 
 /* Enable (1) or disable (0) HIP-event timing of the kernels store/retrieve
- * launch.  Timing events are recorded on the internal stream each kernel
- * runs on.  Errors: INVALID. */
+ * launch; either way the recorded history is cleared.  Timing events are
+ * recorded on the internal stream each kernel runs on.  Errors: INVALID. */
 int kv_pool_set_timing(kvp_pool *pool, int enable);
 
 /* Durations of the kernels of the last timed store or retrieve; waits for
  * them to finish.  Errors: INVALID (timing off or nothing timed), HIP. */
 int kv_pool_last_timing(kvp_pool *pool, kvp_timing *out);
+
+typedef struct {
+    uint32_t calls;           /* timed store / retrieve calls summarised */
+    uint32_t host_calls;      /* of which launched a host-class kernel */
+    uint32_t staging_calls;   /* of which launched a staging-class kernel */
+    uint32_t reserved;
+    float    host_ms_sum, host_ms_min, host_ms_max;          /* -1 when no such kernel ran */
+    float    staging_ms_sum, staging_ms_min, staging_ms_max;
+} kvp_timing_summary;
+
+/* Kernel durations of every store / retrieve timed since timing was enabled
+ * or since the previous summary (at most the last 4096 calls), then clears
+ * that history; waits for the kernels.  Lets a caller time calls issued back
+ * to back without synchronising between them.  Errors: INVALID (timing off),
+ * HIP. */
+int kv_pool_timing_summary(kvp_pool *pool, kvp_timing_summary *out);
 
 /* ---- bandwidth probes (the measured peaks that bound the two kernels) ---- */
 

@@ -21,6 +21,7 @@ void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
 void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
 void pool_set_timing(Pool &, int);
 void pool_last_timing(Pool &, kvp_timing *);
+void pool_timing_summary(Pool &, kvp_timing_summary *);
 void pool_measure(Pool &, uint64_t, uint32_t, uint64_t *);
 void pool_set_bandwidths(Pool &, const uint64_t *);
 }  // namespace kvp
@@ -197,6 +198,11 @@ int kv_pool_set_timing(kvp_pool *pool, int enable)
 int kv_pool_last_timing(kvp_pool *pool, kvp_timing *out)
 {
     return guarded([&] { kvp::pool_last_timing(impl(pool), out); });
+}
+
+int kv_pool_timing_summary(kvp_pool *pool, kvp_timing_summary *out)
+{
+    return guarded([&] { kvp::pool_timing_summary(impl(pool), out); });
 }
 
 int kv_probe_copy_kernel(void *dst, const void *src, uint64_t bytes, uint32_t grid, uint32_t flags, void *stream)

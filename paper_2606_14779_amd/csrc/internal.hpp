@@ -123,6 +123,13 @@ struct Slot {                    // one work-list buffer of the upload ring
     bool pending = false;
 };
 
+struct TimedCall {                // one store / retrieve recorded while timing is on
+    hipEvent_t t0[2] = {nullptr, nullptr};
+    hipEvent_t t1[2] = {nullptr, nullptr};
+    uint32_t blocks[2] = {0, 0};
+    bool ran[2] = {false, false};
+};
+
 struct Pool {
     int device = -1;
     bool placement_only = true;
@@ -143,10 +150,8 @@ struct Pool {
     LaunchCfg launch[2][2];      // [class][op]
 
     bool timing = false;
-    bool timed_valid = false;
-    hipEvent_t t0[2] = {nullptr, nullptr}, t1[2] = {nullptr, nullptr};
-    uint32_t timed_blocks[2] = {0, 0};
-    bool timed_ran[2] = {false, false};
+    std::vector<TimedCall> timed;      // calls recorded since timing was enabled or last summarised
+    std::vector<hipEvent_t> spare;     // timing events ready for reuse
 };
 
 // ---------------------------------------------------------------- kernels (kernels.hip)

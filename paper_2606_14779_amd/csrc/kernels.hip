@@ -182,26 +182,54 @@ __device__ __forceinline__ void wg_convert_lds(const v4u *__restrict__ src, v4u 
 
 enum Form { kPlain = 0, kConvert = 1, kConvertLds = 2 };
 
+// The work list and the engine pointer table are written by the host before
+// the launch and only read here; reading them through the constant address
+// space lets the compiler use scalar loads (uniform per workgroup) instead
+// of vector loads, and the next unit's entries are fetched while the current
+// chunk is copied.
+typedef __attribute__((address_space(4))) const CopyItem citem_t;
+typedef __attribute__((address_space(4))) const uint64_t cptr_t;
+
+struct Unit {
+    uint64_t pool;   // device address of the chunk in its region
+    uint64_t cache;  // device address of the chunk in the engine cache
+};
+
+__device__ __forceinline__ Unit unit_at(const CopyArgs &a, uint32_t u)
+{
+    citem_t *items = (citem_t *)a.items;
+    cptr_t *table = (cptr_t *)a.cache;
+    const uint32_t item = u / a.chunks;
+    const uint32_t c = a.chunk0 + (u - item * a.chunks);
+    const uint64_t pool = items[item].pool;
+    const uint64_t slot = items[item].slot;
+    return Unit{pool + static_cast<uint64_t>(c) * a.chunk_bytes, table[c] + slot * a.chunk_bytes};
+}
+
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
 {
     extern __shared__ v4u lds[];
     const uint32_t units = a.n_items * a.chunks;
     const uint32_t nvec = static_cast<uint32_t>(a.chunk_bytes >> 4);
-    for (uint32_t u = blockIdx.x; u < units; u += gridDim.x) {
-        const uint32_t item = u / a.chunks;
-        const uint32_t c = a.chunk0 + (u - item * a.chunks);
-        const CopyItem it = a.items[item];
-        char *pool = reinterpret_cast<char *>(it.pool) + static_cast<uint64_t>(c) * a.chunk_bytes;
-        char *cache = reinterpret_cast<char *>(a.cache[c]) + static_cast<uint64_t>(it.slot) * a.chunk_bytes;
-        const v4u *src = reinterpret_cast<const v4u *>(GATHER ? pool : cache);
-        v4u *dst = reinterpret_cast<v4u *>(GATHER ? cache : pool);
+    uint32_t u = blockIdx.x;
+    if (u >= units) return;
+    Unit cur = unit_at(a, u);
+    for (;;) {
+        const uint32_t nu = u + gridDim.x;
+        const bool more = nu < units;
+        const Unit next = more ? unit_at(a, nu) : cur;   // fetched while this chunk is copied
+        const v4u *src = reinterpret_cast<const v4u *>(GATHER ? cur.pool : cur.cache);
+        v4u *dst = reinterpret_cast<v4u *>(GATHER ? cur.cache : cur.pool);
         if constexpr (FORM == kPlain)
             wg_copy<UNROLL, NTL, NTS>(src, dst, nvec);
         else if constexpr (FORM == kConvert)
             wg_convert<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec);
         else
             wg_convert_lds<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec, lds);
+        if (!more) break;
+        u = nu;
+        cur = next;
     }
 }
 

@@ -155,9 +155,17 @@ void release_gpu(Pool &p)
         if (kv.second->stored) (void)hipEventDestroy(kv.second->stored);
         if (kv.second->busy) (void)hipEventDestroy(kv.second->busy);
     }
-    hipEvent_t *evs[] = {&p.fork, &p.host_done, &p.stage_done, &p.t0[0], &p.t0[1], &p.t1[0], &p.t1[1]};
+    hipEvent_t *evs[] = {&p.fork, &p.host_done, &p.stage_done};
     for (auto e : evs)
         if (*e) (void)hipEventDestroy(*e), *e = nullptr;
+    for (auto &tc : p.timed)
+        for (int c = 0; c < 2; ++c) {
+            if (tc.t0[c]) (void)hipEventDestroy(tc.t0[c]);
+            if (tc.t1[c]) (void)hipEventDestroy(tc.t1[c]);
+        }
+    p.timed.clear();
+    for (auto e : p.spare) (void)hipEventDestroy(e);
+    p.spare.clear();
     if (p.s_host) (void)hipStreamDestroy(p.s_host);
     if (p.s_stage) (void)hipStreamDestroy(p.s_stage);
     p.s_host = p.s_stage = nullptr;
@@ -264,10 +272,6 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         check_hip(hipEventCreateWithFlags(&p->fork, hipEventDisableTiming), "hipEventCreate");
         check_hip(hipEventCreateWithFlags(&p->host_done, hipEventDisableTiming), "hipEventCreate");
         check_hip(hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming), "hipEventCreate");
-        for (int c = 0; c < 2; ++c) {
-            check_hip(hipEventCreate(&p->t0[c]), "hipEventCreate");
-            check_hip(hipEventCreate(&p->t1[c]), "hipEventCreate");
-        }
         p->ring.resize(kRingSlots);
         for (auto &s : p->ring) check_hip(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreate");
         if (!bandwidths) {
@@ -430,6 +434,50 @@ const Allocation *resolve(const Pool &p, const kvp_loc &e, uint32_t b, const All
     return a;
 }
 
+constexpr size_t kMaxTimedCalls = 4096;
+
+hipEvent_t timing_event(Pool &p)
+{
+    if (!p.spare.empty()) {
+        hipEvent_t e = p.spare.back();
+        p.spare.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    check_hip(hipEventCreate(&e), "hipEventCreate");
+    return e;
+}
+
+// Wait for every recorded call, optionally summarise it, and recycle its events.
+void drain_timed(Pool &p, kvp_timing_summary *sum)
+{
+    kvp_timing_summary s{};
+    s.host_ms_min = s.staging_ms_min = -1.f;
+    s.host_ms_max = s.staging_ms_max = -1.f;
+    for (auto &tc : p.timed) {
+        ++s.calls;
+        for (int c = 0; c < 2; ++c) {
+            if (!tc.ran[c]) continue;
+            check_hip(hipEventSynchronize(tc.t1[c]), "hipEventSynchronize");
+            float ms = 0.f;
+            check_hip(hipEventElapsedTime(&ms, tc.t0[c], tc.t1[c]), "hipEventElapsedTime");
+            float &mn = c == 0 ? s.host_ms_min : s.staging_ms_min;
+            float &mx = c == 0 ? s.host_ms_max : s.staging_ms_max;
+            (c == 0 ? s.host_ms_sum : s.staging_ms_sum) += ms;
+            (c == 0 ? s.host_calls : s.staging_calls) += 1;
+            mn = mn < 0.f ? ms : std::min(mn, ms);
+            mx = std::max(mx, ms);
+        }
+    }
+    for (auto &tc : p.timed)
+        for (int c = 0; c < 2; ++c) {
+            if (tc.t0[c]) p.spare.push_back(tc.t0[c]);
+            if (tc.t1[c]) p.spare.push_back(tc.t1[c]);
+        }
+    p.timed.clear();
+    if (sum) *sum = s;
+}
+
 Slot &acquire_slot(Pool &p, size_t bytes)
 {
     Slot &s = p.ring[p.ring_next];
@@ -484,11 +532,14 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::vector<uint64_t> targets;
     std::vector<uint8_t> slot_used;
     if (gather) slot_used.assign(num_slots, 0);
-    const Allocation *hint = nullptr;
+    // one hint per region: a request's blocks in a region share one range,
+    // while consecutive blocks of a striped map alternate between regions
+    std::vector<const Allocation *> hints(p.regions.size(), nullptr);
     for (uint32_t b = 0; b < n_blocks; ++b) {
         const kvp_loc &e = map[b];
         if (e.region == KVP_ABSENT) continue;
-        hint = resolve(p, e, b, hint);
+        const Allocation *hint = resolve(p, e, b, e.region < hints.size() ? hints[e.region] : nullptr);
+        hints[e.region] = hint;
         const int32_t slot = table[b];
         if (slot < 0 || static_cast<uint32_t>(slot) >= num_slots)
             fail(KVP_ERR_INVALID, "block table entry " + std::to_string(b) + " = " + std::to_string(slot) +
@@ -512,11 +563,16 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     const size_t n_items = items[0].size() + items[1].size();
     const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
     if (p.timing) {
-        p.timed_valid = true;
+        if (p.timed.size() >= kMaxTimedCalls) drain_timed(p, nullptr);   // bound the history
+        TimedCall tc;
         for (int c = 0; c < 2; ++c) {
-            p.timed_ran[c] = false;
-            p.timed_blocks[c] = static_cast<uint32_t>(items[c].size());
+            tc.blocks[c] = static_cast<uint32_t>(items[c].size());
+            if (!items[c].empty()) {
+                tc.t0[c] = timing_event(p);
+                tc.t1[c] = timing_event(p);
+            }
         }
+        p.timed.push_back(tc);
     }
     if (n_items == 0) return;
 
@@ -565,11 +621,12 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         first += items[c].size();
         const LaunchCfg &lc = p.launch[c][op];
         check_hip(hipStreamWaitEvent(cls_stream[c], p.fork, 0), "hipStreamWaitEvent");
-        if (p.timing) check_hip(hipEventRecord(p.t0[c], cls_stream[c]), "hipEventRecord");
+        TimedCall *tc = p.timing ? &p.timed.back() : nullptr;
+        if (tc) check_hip(hipEventRecord(tc->t0[c], cls_stream[c]), "hipEventRecord");
         check_hip(launch_chunk_copy(a, c, gather, lc.grid, lc.flags, cls_stream[c]), "kernel launch");
-        if (p.timing) {
-            check_hip(hipEventRecord(p.t1[c], cls_stream[c]), "hipEventRecord");
-            p.timed_ran[c] = true;
+        if (tc) {
+            check_hip(hipEventRecord(tc->t1[c], cls_stream[c]), "hipEventRecord");
+            tc->ran[c] = true;
         }
         check_hip(hipEventRecord(cls_done[c], cls_stream[c]), "hipEventRecord");
         check_hip(hipStreamWaitEvent(s, cls_done[c], 0), "hipStreamWaitEvent");
@@ -706,23 +763,34 @@ void pool_set_timing(Pool &p, int enable)
 {
     if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
     std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+    drain_timed(p, nullptr);
     p.timing = enable != 0;
-    p.timed_valid = false;
 }
 
 void pool_last_timing(Pool &p, kvp_timing *out)
 {
     if (!out) fail(KVP_ERR_INVALID, "null output");
     std::lock_guard<std::mutex> lock(p.mu);
-    if (!p.timing || !p.timed_valid) fail(KVP_ERR_INVALID, "no timed call");
+    if (!p.timing || p.timed.empty()) fail(KVP_ERR_INVALID, "no timed call");
     DeviceScope dev(p.device);
+    const TimedCall &tc = p.timed.back();
     float ms[2] = {-1.f, -1.f};
     for (int c = 0; c < 2; ++c) {
-        if (!p.timed_ran[c]) continue;
-        check_hip(hipEventSynchronize(p.t1[c]), "hipEventSynchronize");
-        check_hip(hipEventElapsedTime(&ms[c], p.t0[c], p.t1[c]), "hipEventElapsedTime");
+        if (!tc.ran[c]) continue;
+        check_hip(hipEventSynchronize(tc.t1[c]), "hipEventSynchronize");
+        check_hip(hipEventElapsedTime(&ms[c], tc.t0[c], tc.t1[c]), "hipEventElapsedTime");
     }
-    *out = kvp_timing{ms[0], ms[1], p.timed_blocks[0], p.timed_blocks[1]};
+    *out = kvp_timing{ms[0], ms[1], tc.blocks[0], tc.blocks[1]};
+}
+
+void pool_timing_summary(Pool &p, kvp_timing_summary *out)
+{
+    if (!out) fail(KVP_ERR_INVALID, "null output");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (!p.timing) fail(KVP_ERR_INVALID, "timing is off");
+    DeviceScope dev(p.device);
+    drain_timed(p, out);
 }
 
 }  // namespace kvp

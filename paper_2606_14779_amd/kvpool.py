@@ -54,6 +54,14 @@ class _Timing(ctypes.Structure):
                 ("host_blocks", ctypes.c_uint32), ("staging_blocks", ctypes.c_uint32)]
 
 
+class _TimingSummary(ctypes.Structure):
+    _fields_ = [("calls", ctypes.c_uint32), ("host_calls", ctypes.c_uint32),
+                ("staging_calls", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("host_ms_sum", ctypes.c_float), ("host_ms_min", ctypes.c_float), ("host_ms_max", ctypes.c_float),
+                ("staging_ms_sum", ctypes.c_float), ("staging_ms_min", ctypes.c_float),
+                ("staging_ms_max", ctypes.c_float)]
+
+
 assert ctypes.sizeof(_RegionDesc) == 24 and ctypes.sizeof(_KVSpec) == 24
 assert LOC_DTYPE.itemsize == 16
 
@@ -92,6 +100,7 @@ _SIGS = {
     "kv_pool_set_launch": (_i32, [_vp, _u32, _u32, _u32, _u32]),
     "kv_pool_set_timing": (_i32, [_vp, _i32]),
     "kv_pool_last_timing": (_i32, [_vp, _vp]),
+    "kv_pool_timing_summary": (_i32, [_vp, _vp]),
     "kv_probe_copy_kernel": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp]),
     "kv_probe_memcpy": (_i32, [_vp, _vp, _u64, _vp]),
 }
@@ -290,6 +299,11 @@ class KVPool:
         t = _Timing()
         _check(_lib.kv_pool_last_timing(self._h, ctypes.byref(t)))
         return {k: getattr(t, k) for k, _ in _Timing._fields_}
+
+    def timing_summary(self) -> dict:
+        t = _TimingSummary()
+        _check(_lib.kv_pool_timing_summary(self._h, ctypes.byref(t)))
+        return {k: getattr(t, k) for k, _ in _TimingSummary._fields_ if k != "reserved"}
 
 
 def allowed_numa_nodes() -> list[int]:

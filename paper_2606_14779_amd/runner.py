@@ -43,15 +43,20 @@ class WorkloadRun:
         tail = (sh.kv_heads, sh.block_size, sh.head_dim)
         self.src = torch.empty(shape + (wl.src_num_slots,) + tail, dtype=torch.int16, device=dev)
         self.dst = torch.empty(shape + (wl.dst_num_slots,) + tail, dtype=torch.int16, device=dev)
+        self._ptrs = {}           # id(cache) -> (K pointers, V pointers), computed once
         self.maps = {}            # request_id -> placed map (present prefix)
         self.retrieve_maps = {}   # request_id -> map of the whole context (absent tail)
         self.streams = [torch.cuda.Stream(device=dev) for _ in range(wl.n_streams)]
 
     # ---- pointers
-    @staticmethod
-    def layer_ptrs(cache):
-        L = cache.shape[0]
-        return [cache[l, 0].data_ptr() for l in range(L)], [cache[l, 1].data_ptr() for l in range(L)]
+    def layer_ptrs(self, cache):
+        """Per-layer K and V base addresses of a [L][2][slots][H][bs][D] cache (cached per tensor)."""
+        key = (cache.data_ptr(), tuple(cache.shape))
+        if key not in self._ptrs:
+            L = cache.shape[0]
+            self._ptrs[key] = (tuple(cache[l, 0].data_ptr() for l in range(L)),
+                               tuple(cache[l, 1].data_ptr() for l in range(L)))
+        return self._ptrs[key]
 
     # ---- setup steps
     def fill_source(self, threads=None, keep_host=False):
