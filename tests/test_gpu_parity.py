@@ -425,3 +425,17 @@ def test_retrieve_request_by_id_errors():
             assert ei.value.name == name
     finally:
         run.close()
+
+
+def test_allocation_failure_reports_nomem_and_cleans_up():
+    """A staging region larger than HBM fails with NOMEM; the regions already
+    allocated are released (a following normal pool still fits)."""
+    spec = K.KVSpec(2, 2, 64)
+    free_before = torch.cuda.mem_get_info()[0]
+    with pytest.raises(K.KVPoolError) as ei:
+        K.KVPool([K.Region("staging", 1 << 30), K.Region("staging", 1 << 46)], [1, 1], spec, 0)
+    assert ei.value.name == "NOMEM"
+    torch.cuda.synchronize()
+    assert torch.cuda.mem_get_info()[0] >= free_before - (64 << 20)
+    with K.KVPool([K.Region("staging", 1 << 30)], [1], spec, 0) as p:
+        assert p.region_info(0)["device_ptr"]
