@@ -292,8 +292,9 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
- * class 12 workgroups, staging class 8192; KVP_LAUNCH_LDS for pool_layout 1;
- * KVP_LAUNCH_NT_STORE for the host-class store.  Errors: INVALID. */
+ * class 12 workgroups (16 for the token-major store), staging class 8192;
+ * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
+ * pool_layout 1 except the host-class store.  Errors: INVALID. */
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
 
 typedef struct {

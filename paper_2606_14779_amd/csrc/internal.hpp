@@ -181,7 +181,7 @@ hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint3
                              hipStream_t s);
 hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid,
                              uint32_t flags, hipStream_t s);
-uint32_t default_grid(uint32_t cls, uint32_t op);
+uint32_t default_grid(uint32_t cls, uint32_t op, const kvp_kv_spec &spec);
 uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec);
 
 }  // namespace kvp
