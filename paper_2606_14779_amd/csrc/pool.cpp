@@ -92,8 +92,13 @@ private:
     unsigned long old_mask_[kWords] = {};
 };
 
+// NUMA node backing the page at p: move_pages() in query mode (no nodes
+// given) reports where each page lives; get_mempolicy() is the fallback.
 int page_node(void *p)
 {
+    void *pages[1] = {p};
+    int status[1] = {-1};
+    if (syscall(SYS_move_pages, 0, 1ul, pages, nullptr, status, 0) == 0 && status[0] >= 0) return status[0];
     int node = -1;
     if (syscall(SYS_get_mempolicy, &node, nullptr, 0, p, MPOL_F_NODE | MPOL_F_ADDR) != 0) return -1;
     return node;
