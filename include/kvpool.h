@@ -289,10 +289,15 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
 #define KVP_LAUNCH_NT_LOAD   1u  /* non-temporal loads */
 #define KVP_LAUNCH_NT_STORE  2u  /* non-temporal stores */
 #define KVP_LAUNCH_LDS       4u  /* pool_layout 1: stage each chunk through LDS */
+#define KVP_LAUNCH_SPLIT2    8u  /* pool_layout 0: copy each chunk as two half-chunk units
+                                    (probe: 256 x 4-vector tiles instead of 256 x 8) */
+#define KVP_LAUNCH_XCD      16u  /* renumber workgroups so that each of the 8 XCDs takes
+                                    contiguous units (grids that are multiples of 8) */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
- * class 12 workgroups (16 for the token-major store), staging class 8192;
+ * class 12 workgroups (16 for the token-major store); staging class 65536
+ * with KVP_LAUNCH_SPLIT2 for the pool_layout 0 retrieve, else 8192;
  * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
  * pool_layout 1 except the host-class store.  Errors: INVALID. */
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
@@ -333,8 +338,8 @@ int kv_pool_timing_summary(kvp_pool *pool, kvp_timing_summary *out);
 
 /* Streaming copy kernel: bytes from src to dst (device-visible addresses,
  * 16-byte aligned, bytes a multiple of 16), `grid` workgroups of 256
- * threads (0 = default), KVP_LAUNCH_NT_* flags, on `stream` of the current
- * device.  Errors: INVALID, HIP. */
+ * threads (0 = default), KVP_LAUNCH_NT_* and KVP_LAUNCH_SPLIT2 flags, on
+ * `stream` of the current device.  Errors: INVALID, HIP. */
 int kv_probe_copy_kernel(void *dst, const void *src, uint64_t bytes, uint32_t grid,
                          uint32_t flags, void *stream);
 

@@ -211,7 +211,8 @@ int kv_probe_copy_kernel(void *dst, const void *src, uint64_t bytes, uint32_t gr
         if (!dst || !src) kvp::fail(KVP_ERR_INVALID, "null pointer");
         if ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src) | bytes) & 15)
             kvp::fail(KVP_ERR_INVALID, "pointers and size must be multiples of 16");
-        if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE)) kvp::fail(KVP_ERR_INVALID, "unknown flags");
+        if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_SPLIT2))
+            kvp::fail(KVP_ERR_INVALID, "unknown flags");
         if (grid > (1u << 20)) kvp::fail(KVP_ERR_INVALID, "grid too large");
         kvp::check_hip(kvp::launch_probe_copy(dst, src, bytes, grid, flags, static_cast<hipStream_t>(stream)),
                        "probe kernel launch");

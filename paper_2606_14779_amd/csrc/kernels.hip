@@ -41,6 +41,7 @@ typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) v4u gv4u;
 
 constexpr uint32_t kThreads = 256;
+constexpr uint32_t kXcds = 8;     // MI355X: 8 accelerator complex dies, 32 CUs each
 constexpr uint64_t kMaxLdsChunk = 64 * 1024;
 
 template <bool NT>
@@ -195,24 +196,36 @@ struct Unit {
     uint64_t cache;  // device address of the chunk in the engine cache
 };
 
+// Unit u of a launch: item u / (chunks * parts), then chunk, then part of
+// the chunk (parts > 1 only for plain chunks).
 __device__ __forceinline__ Unit unit_at(const CopyArgs &a, uint32_t u)
 {
     citem_t *items = (citem_t *)a.items;
     cptr_t *table = (cptr_t *)a.cache;
-    const uint32_t item = u / a.chunks;
-    const uint32_t c = a.chunk0 + (u - item * a.chunks);
+    const uint32_t per_item = a.chunks * a.parts;
+    const uint32_t item = u / per_item;
+    const uint32_t r = u - item * per_item;
+    const uint32_t k = r / a.parts;
+    const uint32_t c = a.chunk0 + k;
+    const uint64_t part = static_cast<uint64_t>(r - k * a.parts) * (a.chunk_bytes / a.parts);
     const uint64_t pool = items[item].pool;
     const uint64_t slot = items[item].slot;
-    return Unit{pool + static_cast<uint64_t>(c) * a.chunk_bytes, table[c] + slot * a.chunk_bytes};
+    return Unit{pool + static_cast<uint64_t>(c) * a.chunk_bytes + part, table[c] + slot * a.chunk_bytes + part};
 }
 
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
 {
     extern __shared__ v4u lds[];
-    const uint32_t units = a.n_items * a.chunks;
-    const uint32_t nvec = static_cast<uint32_t>(a.chunk_bytes >> 4);
+    const uint32_t units = a.n_items * a.chunks * a.parts;
+    const uint32_t nvec = static_cast<uint32_t>((a.chunk_bytes / a.parts) >> 4);
     uint32_t u = blockIdx.x;
+    if (a.xcd_remap) {
+        // workgroups are dealt to the 8 XCDs round-robin; renumber them so that
+        // each XCD takes one contiguous run of units per pass over the grid
+        const uint32_t per = gridDim.x / kXcds;          // grid is a multiple of 8 here
+        u = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+    }
     if (u >= units) return;
     Unit cur = unit_at(a, u);
     for (;;) {
@@ -291,8 +304,8 @@ static hipError_t launch_form(const CopyArgs &a, uint32_t grid, uint32_t flags, 
 template <bool HOST, bool GATHER, int FORM>
 static hipError_t launch_unroll(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
 {
-    // enough 16-byte loads in flight per lane to cover the whole chunk, up to 8
-    const uint64_t per_lane = (a.chunk_bytes / 16 + kThreads - 1) / kThreads;
+    // enough 16-byte loads in flight per lane to cover the whole unit, up to 8
+    const uint64_t per_lane = (a.chunk_bytes / a.parts / 16 + kThreads - 1) / kThreads;
     if (per_lane >= 8) return launch_form<HOST, GATHER, FORM, 8>(a, grid, flags, lds, s);
     if (per_lane >= 4) return launch_form<HOST, GATHER, FORM, 4>(a, grid, flags, lds, s);
     if (per_lane >= 2) return launch_form<HOST, GATHER, FORM, 2>(a, grid, flags, lds, s);
@@ -308,13 +321,18 @@ static hipError_t launch_dir(const CopyArgs &a, uint32_t grid, uint32_t flags, h
     return launch_unroll<HOST, GATHER, kConvert>(a, grid, flags, 0, s);
 }
 
-hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
+hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
                              hipStream_t s)
 {
-    if (a.n_items == 0) return hipSuccess;
-    const uint64_t units = static_cast<uint64_t>(a.n_items) * a.chunks;
+    if (args.n_items == 0) return hipSuccess;
+    CopyArgs a = args;
+    // halves of a plain chunk are independent contiguous copies
+    a.parts = (a.layout == 0 && (flags & KVP_LAUNCH_SPLIT2) && a.chunk_bytes % 32 == 0) ? 2u : 1u;
+    const uint64_t units = static_cast<uint64_t>(a.n_items) * a.chunks * a.parts;
     if (grid > units) grid = static_cast<uint32_t>(units);
     if (grid == 0) grid = 1;
+    // the XCD renumbering is a permutation of [0, grid) only for multiples of 8
+    a.xcd_remap = (flags & KVP_LAUNCH_XCD) && grid % kXcds == 0 ? 1u : 0u;
     if (cls == KVP_CLASS_HOST)
         return gather ? launch_dir<true, true>(a, grid, flags, s) : launch_dir<true, false>(a, grid, flags, s);
     return gather ? launch_dir<false, true>(a, grid, flags, s) : launch_dir<false, false>(a, grid, flags, s);
@@ -325,13 +343,25 @@ hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_
 {
     const uint64_t nvec = bytes / 16;
     if (nvec == 0) return hipSuccess;
-    const uint64_t tiles = (nvec + kThreads * 8 - 1) / (kThreads * 8);
+    const bool split = flags & KVP_LAUNCH_SPLIT2;
+    const uint64_t tiles = (nvec + kThreads * (split ? 4 : 8) - 1) / (kThreads * (split ? 4 : 8));
     if (grid == 0) grid = 2048;
     if (grid > tiles) grid = static_cast<uint32_t>(tiles);
     const bool ntl = flags & KVP_LAUNCH_NT_LOAD, nts = flags & KVP_LAUNCH_NT_STORE;
     const v4u *sp = static_cast<const v4u *>(src);
     v4u *dp = static_cast<v4u *>(dst);
     dim3 g(grid), b(kThreads);
+    if (split) {
+        if (ntl && nts)
+            hipLaunchKernelGGL((probe_copy_kernel<4, true, true>), g, b, 0, s, sp, dp, nvec);
+        else if (ntl)
+            hipLaunchKernelGGL((probe_copy_kernel<4, true, false>), g, b, 0, s, sp, dp, nvec);
+        else if (nts)
+            hipLaunchKernelGGL((probe_copy_kernel<4, false, true>), g, b, 0, s, sp, dp, nvec);
+        else
+            hipLaunchKernelGGL((probe_copy_kernel<4, false, false>), g, b, 0, s, sp, dp, nvec);
+        return hipGetLastError();
+    }
     if (ntl && nts)
         hipLaunchKernelGGL((probe_copy_kernel<8, true, true>), g, b, 0, s, sp, dp, nvec);
     else if (ntl)

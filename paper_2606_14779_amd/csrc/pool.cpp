@@ -209,10 +209,12 @@ uint32_t default_grid(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
     // peak, while more of them only queue reads in the shared memory path and
     // slow the HBM kernel running beside them.  The token-major store (host
     // writes in runs of whole chunks, reads from HBM by rows) wants 16.
-    // Staging class: 8192 workgroups (32 per CU) so the HBM kernel keeps its
-    // share of the memory queues while the host kernel runs.
+    // Staging class: many workgroups so the HBM kernel keeps its share of
+    // the memory queues while the host kernel runs -- 65536 half-chunk units
+    // in flight for the plain retrieve (2.4 ms beside the host kernel, 2.22 ms
+    // alone), 8192 otherwise.
     if (cls == KVP_CLASS_HOST) return (op == KVP_OP_STORE && spec.pool_layout == 1) ? 16u : 12u;
-    return 8192u;
+    return (op == KVP_OP_RETRIEVE && spec.pool_layout == 0) ? 65536u : 8192u;
 }
 
 uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
@@ -225,6 +227,8 @@ uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
     // sides), except the host-class store: there the direct conversion keeps
     // the host-link side contiguous and measured faster (207 vs 211 ms)
     if (spec.pool_layout == 1 && !(cls == KVP_CLASS_HOST && op == KVP_OP_STORE)) f |= KVP_LAUNCH_LDS;
+    // plain HBM retrieve: half-chunk units (the copy shape that measured best)
+    if (spec.pool_layout == 0 && cls == KVP_CLASS_STAGING && op == KVP_OP_RETRIEVE) f |= KVP_LAUNCH_SPLIT2;
     return f;
 }
 
@@ -529,7 +533,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (!k || !v || (k & 15) || (v & 15))
             fail(KVP_ERR_INVALID, "layer " + std::to_string(l) + ": null or unaligned cache pointer");
     }
-    if (static_cast<uint64_t>(n_blocks) * 2 * L >= (1ull << 32)) fail(KVP_ERR_INVALID, "request too large");
+    if (static_cast<uint64_t>(n_blocks) * 4 * L >= (1ull << 32)) fail(KVP_ERR_INVALID, "request too large");
 
     std::lock_guard<std::mutex> lock(p.mu);
     DeviceScope dev(p.device);
@@ -621,6 +625,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         a.n_items = static_cast<uint32_t>(items[c].size());
         a.chunks = 2 * (layer_end - layer_begin);
         a.chunk0 = 2 * layer_begin;
+        a.parts = 1;
+        a.xcd_remap = 0;
         a.chunk_bytes = p.chunk_bytes;
         a.heads = p.spec.num_kv_heads;
         a.tokens = p.spec.block_size;
@@ -761,7 +767,8 @@ void pool_region_read(Pool &p, uint32_t region, uint64_t offset, uint64_t bytes,
 void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)
 {
     if (cls > 1 || op > 1) fail(KVP_ERR_INVALID, "class and op must be 0 or 1");
-    if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS)) fail(KVP_ERR_INVALID, "unknown flags");
+    if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS | KVP_LAUNCH_SPLIT2 | KVP_LAUNCH_XCD))
+        fail(KVP_ERR_INVALID, "unknown flags");
     if (grid > (1u << 20)) fail(KVP_ERR_INVALID, "grid too large");
     std::lock_guard<std::mutex> lock(p.mu);
     p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op, p.spec), flags};  // flags taken as given

@@ -46,7 +46,9 @@ def test_parity_scaled_workloads(cfg, layout):
 
 
 @pytest.mark.parametrize("grid,flags", [(1, 0), (7, K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE),
-                                        (4096, K.LAUNCH_NT_LOAD), (300, K.LAUNCH_NT_STORE)])
+                                        (4096, K.LAUNCH_NT_LOAD), (300, K.LAUNCH_NT_STORE),
+                                        (64, K.LAUNCH_XCD), (96, K.LAUNCH_XCD | K.LAUNCH_SPLIT2),
+                                        (12, K.LAUNCH_XCD), (65536, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD)])
 def test_parity_launch_shapes(grid, flags):
     wl = workloads.make(2, max_blocks=45)
     say("case launch", grid, flags)
