@@ -62,6 +62,17 @@ def build(verbose: bool = False, extra: list[str] | None = None) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))
     os.replace(tmp, LIB)
+    # a plain C++ client of the ABI (used by the tests): links the library, no Python
+    client_src = os.path.join(ROOT, "tests", "abi_client", "abi_client.cpp")
+    if os.path.exists(client_src):
+        exe = os.path.join(ROOT, "tests", "abi_client", "abi_client")
+        cmd = ["g++"] + CXX_FLAGS + ["-I", INCLUDE, client_src, "-o", exe + ".tmp", "-L" + PKG, "-lkvpool",
+                                     "-Wl,-rpath,$ORIGIN/../../paper_2606_14779_amd", "-L" + os.path.join(ROCM, "lib"), "-lamdhip64",
+                                     "-Wl,-rpath," + os.path.join(ROCM, "lib")]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError("abi client build failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))
+        os.replace(exe + ".tmp", exe)
     if verbose:
         print("built", LIB)
     return LIB

@@ -541,9 +541,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     // GLT-resolved locations, grouped by region class (Sec. 4.3)
     std::vector<CopyItem> items[2];
     std::vector<RequestRec *> touched;
-    std::vector<uint64_t> targets;
-    std::vector<uint8_t> slot_used;
-    if (gather) slot_used.assign(num_slots, 0);
+    std::vector<uint64_t> targets;   // store: (region, offset) keys; retrieve: destination slots
     // one hint per region: a request's blocks in a region share one range,
     // while consecutive blocks of a striped map alternate between regions
     std::vector<const Allocation *> hints(p.regions.size(), nullptr);
@@ -556,22 +554,20 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (slot < 0 || static_cast<uint32_t>(slot) >= num_slots)
             fail(KVP_ERR_INVALID, "block table entry " + std::to_string(b) + " = " + std::to_string(slot) +
                                       " outside [0, " + std::to_string(num_slots) + ")");
-        if (gather) {
-            if (slot_used[slot]) fail(KVP_ERR_INVALID, "destination slot " + std::to_string(slot) + " named twice");
-            slot_used[slot] = 1;
-        } else {
-            targets.push_back((static_cast<uint64_t>(e.region) << 48) | (e.offset >> 4));
-        }
+        targets.push_back(gather ? static_cast<uint64_t>(slot)
+                                 : (static_cast<uint64_t>(e.region) << 48) | (e.offset >> 4));
         if (std::find(touched.begin(), touched.end(), hint->owner) == touched.end()) touched.push_back(hint->owner);
         const Region &r = p.regions[e.region];
         const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
         items[cls].push_back(CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
     }
-    if (!gather) {
-        std::sort(targets.begin(), targets.end());
-        if (std::adjacent_find(targets.begin(), targets.end()) != targets.end())
-            fail(KVP_ERR_INVALID, "two map entries name the same pool block");
-    }
+    // no two present entries may write the same place (a destination slot on
+    // retrieve, a pool block on store): sorted keys, independent of num_slots
+    std::sort(targets.begin(), targets.end());
+    auto dup = std::adjacent_find(targets.begin(), targets.end());
+    if (dup != targets.end())
+        fail(KVP_ERR_INVALID, gather ? "destination slot " + std::to_string(*dup) + " named twice"
+                                     : std::string("two map entries name the same pool block"));
     const size_t n_items = items[0].size() + items[1].size();
     const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
     if (p.timing) {

@@ -1,0 +1,100 @@
+// A plain C++ client of libkvpool.so: no Python, no PyTorch.  Creates a pool
+// of one host and one HBM staging region, places a request, stores a source
+// cache filled with a per-element tag, retrieves it into a destination cache
+// under a permuted block table, and checks every element on the host.
+// Built by the package build step; run by tests/test_abi_client.py (GPU).
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "kvpool.h"
+
+#define TRY(x)                                                                               \
+    do {                                                                                     \
+        int rc_ = (x);                                                                       \
+        if (rc_ != KVP_OK) {                                                                 \
+            std::fprintf(stderr, "%s failed: %d (%s)\n", #x, rc_, kv_pool_last_error());     \
+            return 1;                                                                        \
+        }                                                                                    \
+    } while (0)
+#define HIPTRY(x)                                                                            \
+    do {                                                                                     \
+        if ((x) != hipSuccess) {                                                             \
+            std::fprintf(stderr, "%s failed\n", #x);                                         \
+            return 1;                                                                        \
+        }                                                                                    \
+    } while (0)
+
+int main()
+{
+    const uint32_t L = 4, H = 2, bs = 16, D = 64, n = 37, slots = 45;
+    const uint64_t chunk_elems = uint64_t(H) * bs * D;                 // bf16 words per (layer, K/V) chunk
+    const uint64_t layer_bytes = uint64_t(slots) * chunk_elems * 2;
+    kvp_kv_spec spec = {L, H, D, bs, 2, 0};
+    const uint64_t block_bytes = 2ull * L * chunk_elems * 2;
+    kvp_region_desc regions[2] = {{KVP_REGION_HOST, -1, 64 * block_bytes, KVP_HOST_DEFAULT, 0},
+                                  {KVP_REGION_STAGING, -1, 64 * block_bytes, 0, 0}};
+    uint64_t bw[2] = {3, 1};
+    kvp_pool *pool = nullptr;
+    TRY(kv_pool_create(regions, bw, 2, &spec, 0, &pool));
+
+    // engine caches: one buffer per layer and K/V
+    std::vector<void *> src(2 * L), dst(2 * L);
+    std::vector<uint16_t> host(slots * chunk_elems);
+    for (uint32_t i = 0; i < 2 * L; ++i) {
+        HIPTRY(hipMalloc(&src[i], layer_bytes));
+        HIPTRY(hipMalloc(&dst[i], layer_bytes));
+        for (uint64_t e = 0; e < host.size(); ++e) host[e] = uint16_t(e * 2654435761u + i * 40503u);
+        HIPTRY(hipMemcpy(src[i], host.data(), layer_bytes, hipMemcpyHostToDevice));
+        HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
+    }
+    std::vector<void *> k_src(L), v_src(L), k_dst(L), v_dst(L);
+    for (uint32_t l = 0; l < L; ++l) {
+        k_src[l] = src[2 * l];
+        v_src[l] = src[2 * l + 1];
+        k_dst[l] = dst[2 * l];
+        v_dst[l] = dst[2 * l + 1];
+    }
+
+    std::vector<kvp_loc> map(n);
+    TRY(kv_pool_place(pool, 42, n, map.data()));
+    std::vector<int32_t> src_table(n), dst_table(n);
+    for (uint32_t b = 0; b < n; ++b) {
+        src_table[b] = int32_t((b * 7 + 3) % slots);      // 7 is invertible mod 45: distinct slots
+        dst_table[b] = int32_t((b * 11 + 5) % slots);
+    }
+    hipStream_t stream;
+    HIPTRY(hipStreamCreate(&stream));
+    TRY(kv_pool_store(pool, map.data(), n, src_table.data(), slots, k_src.data(), v_src.data(), stream));
+    TRY(kv_pool_retrieve_request(pool, 42, n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
+    HIPTRY(hipStreamSynchronize(stream));
+
+    std::vector<uint16_t> got(slots * chunk_elems), want(slots * chunk_elems);
+    std::vector<char> used(slots, 0);
+    for (uint32_t b = 0; b < n; ++b) used[dst_table[b]] = 1;
+    uint64_t bad = 0;
+    for (uint32_t i = 0; i < 2 * L; ++i) {
+        HIPTRY(hipMemcpy(got.data(), dst[i], layer_bytes, hipMemcpyDeviceToHost));
+        for (uint64_t e = 0; e < want.size(); ++e) want[e] = uint16_t(e * 2654435761u + i * 40503u);
+        for (uint32_t b = 0; b < n; ++b)
+            bad += std::memcmp(&got[dst_table[b] * chunk_elems], &want[src_table[b] * chunk_elems],
+                               chunk_elems * 2) != 0;
+        for (uint32_t sl = 0; sl < slots; ++sl)
+            if (!used[sl])
+                for (uint64_t e = 0; e < chunk_elems; ++e) bad += got[sl * chunk_elems + e] != 0xA5A5;
+    }
+    TRY(kv_pool_release(pool, 42));
+    kv_pool_destroy(pool);
+    HIPTRY(hipStreamDestroy(stream));
+    for (void *p : src) HIPTRY(hipFree(p));
+    for (void *p : dst) HIPTRY(hipFree(p));
+    if (bad) {
+        std::fprintf(stderr, "abi client: %llu mismatching chunks or elements\n", (unsigned long long)bad);
+        return 1;
+    }
+    std::printf("abi client: %u blocks stored and retrieved exactly\n", n);
+    return 0;
+}
