@@ -2,18 +2,22 @@
 //
 // Nothing here is a contraction, so there is no MFMA: every kernel is a bit
 // copy of 16-byte vectors.  One unit of work is one (block, layer, K/V)
-// chunk of C bytes.  A 256-thread workgroup (four 64-lane wavefronts) copies
-// a whole chunk per step; each lane holds up to UNROLL 16-byte loads in
-// flight before it stores, so a workgroup keeps 256*UNROLL*16 bytes in flight
-// (32 KiB at UNROLL = 8, one LLaMA-shaped chunk).  Loads and stores of a
-// wavefront cover 1 KiB of contiguous memory, which the memory system merges
-// into full 128-byte lines.
+// chunk of C bytes, or half of one (KVP_LAUNCH_SPLIT2, plain chunks only).
+// A 256-thread workgroup (four 64-lane wavefronts) copies a whole unit per
+// step; each lane holds up to UNROLL 16-byte loads in flight before it
+// stores, so a workgroup keeps 256*UNROLL*16 bytes in flight (32 KiB at
+// UNROLL = 8, one LLaMA-shaped chunk).  Loads and stores of a wavefront cover
+// 1 KiB of contiguous memory, which the memory system merges into full
+// 128-byte lines.
 //
 // The grid is persistent: workgroup g takes units g, g+G, g+2G, ...  Unit u
-// is chunk u % (2L) of work item u / (2L), so neighbouring workgroups read
-// neighbouring chunks of the same pool block (the pool side streams through
-// memory in address order).  There is no data reuse, so the round-robin
-// placement of workgroups on the 8 XCDs needs no remapping.
+// is part u % parts of chunk (u / parts) % (2L) of work item u / (2L*parts),
+// so neighbouring workgroups read neighbouring pieces of the same pool block
+// (the pool side streams through memory in address order).  There is no data
+// reuse; an optional renumbering that gives each of the 8 XCDs contiguous
+// units (KVP_LAUNCH_XCD) measured no better than the round-robin default.
+// The work list and the engine pointer table are read with scalar loads, and
+// the next unit's entries are fetched while the current unit is copied.
 //
 // Three copy forms:
 //   - head-major pool chunks: the chunk is [H][bs][D] on both sides; a plain
