@@ -167,9 +167,9 @@ int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
 
 /*
  * Retrieve (Sec. 4.3, "KV Retrieval"): group the present entries by region
- * type, then read the host regions (zero-copy kernel) and the staging
- * regions (HBM gather kernel) in parallel on two internal streams forked
- * from and joined back into `stream`; every chunk lands in slot
+ * type, then read the host regions (zero-copy kernel, on `stream`) and the
+ * staging regions (HBM gather kernel, on the pool's internal stream forked
+ * from `stream` and joined back into it) in parallel; every chunk lands in slot
  * dst_block_table[b] of layer l's K or V buffer in the engine layout.
  * Absent entries are skipped and every slot not named by a present entry is
  * left untouched.
@@ -311,7 +311,9 @@ typedef struct {
 
 /* Enable (1) or disable (0) HIP-event timing of the kernels store/retrieve
  * launch; either way the recorded history is cleared.  Timing events are
- * recorded on the internal stream each kernel runs on.  Errors: INVALID. */
+ * recorded on the stream each kernel runs on (the caller's stream for the
+ * host class, the pool's internal stream for the staging class).
+ * Errors: INVALID. */
 int kv_pool_set_timing(kvp_pool *pool, int enable);
 
 /* Durations of the kernels of the last timed store or retrieve; waits for

@@ -143,8 +143,8 @@ struct Pool {
     uint32_t next_gen = 1;
     std::mutex mu;
 
-    hipStream_t s_host = nullptr, s_stage = nullptr;
-    hipEvent_t fork = nullptr, host_done = nullptr, stage_done = nullptr;
+    hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's)
+    hipEvent_t fork = nullptr, stage_done = nullptr;
     std::vector<Slot> ring;
     uint32_t ring_next = 0;
     LaunchCfg launch[2][2];      // [class][op]

@@ -5,9 +5,10 @@
 // blocks by pool device, and read all devices in parallel.  Here the groups
 // are the two region classes -- pinned host regions, read by a zero-copy
 // kernel over the host link, and HBM staging regions, read by an HBM gather
-// kernel -- and "in parallel" means two internal HIP streams forked from the
-// caller's stream and joined back into it, so both kernels run at once and
-// the caller sees one stream-ordered operation.  The per-call work list (one
+// kernel -- and "in parallel" means the staging kernel is forked onto an
+// internal HIP stream while the host kernel runs on the caller's stream, and
+// the two are joined again on the caller's stream, so both kernels run at
+// once and the caller sees one stream-ordered operation.  The per-call work list (one
 // 16-byte item per block plus the 2L engine-buffer pointers) is written to a
 // pinned buffer and uploaded with one asynchronous copy; buffers come from a
 // small ring guarded by events, so a call only blocks when the ring wraps
@@ -147,7 +148,6 @@ void free_slot(Slot &s)
 void release_gpu(Pool &p)
 {
     if (p.placement_only) return;
-    if (p.s_host) (void)hipStreamSynchronize(p.s_host);
     if (p.s_stage) (void)hipStreamSynchronize(p.s_stage);
     for (auto &s : p.ring) {
         if (s.pending && s.done) (void)hipEventSynchronize(s.done);
@@ -160,7 +160,7 @@ void release_gpu(Pool &p)
         if (kv.second->stored) (void)hipEventDestroy(kv.second->stored);
         if (kv.second->busy) (void)hipEventDestroy(kv.second->busy);
     }
-    hipEvent_t *evs[] = {&p.fork, &p.host_done, &p.stage_done};
+    hipEvent_t *evs[] = {&p.fork, &p.stage_done};
     for (auto e : evs)
         if (*e) (void)hipEventDestroy(*e), *e = nullptr;
     for (auto &tc : p.timed)
@@ -171,9 +171,8 @@ void release_gpu(Pool &p)
     p.timed.clear();
     for (auto e : p.spare) (void)hipEventDestroy(e);
     p.spare.clear();
-    if (p.s_host) (void)hipStreamDestroy(p.s_host);
     if (p.s_stage) (void)hipStreamDestroy(p.s_stage);
-    p.s_host = p.s_stage = nullptr;
+    p.s_stage = nullptr;
     for (auto &r : p.regions) {
         if (r.host) (void)hipHostFree(r.host);
         else if (r.dev) (void)hipFree(r.dev);
@@ -279,10 +278,8 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
     DeviceScope dev(hip_device);
     try {
         for (auto &r : p->regions) alloc_region(r);
-        check_hip(hipStreamCreateWithFlags(&p->s_host, hipStreamNonBlocking), "hipStreamCreate");
         check_hip(hipStreamCreateWithFlags(&p->s_stage, hipStreamNonBlocking), "hipStreamCreate");
         check_hip(hipEventCreateWithFlags(&p->fork, hipEventDisableTiming), "hipEventCreate");
-        check_hip(hipEventCreateWithFlags(&p->host_done, hipEventDisableTiming), "hipEventCreate");
         check_hip(hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming), "hipEventCreate");
         p->ring.resize(kRingSlots);
         for (auto &s : p->ring) check_hip(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreate");
@@ -610,12 +607,15 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     slot.pending = true;  // from here on the slot is in use even if a launch fails
 
     const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
-    hipStream_t cls_stream[2] = {p.s_host, p.s_stage};
-    hipEvent_t cls_done[2] = {p.host_done, p.stage_done};
+    // Staging class forked onto the internal stream first, then the host
+    // class on the caller's stream itself; the caller's stream then waits for
+    // the staging kernel.  One extra stream keeps the pool within the few
+    // hardware queues a process gets, so caller streams (e.g. compute
+    // overlapping a layerwise retrieve) are not serialised behind it.
     size_t first = 0;
+    CopyArgs args[2] = {};
     for (uint32_t c = 0; c < 2; ++c) {
-        if (items[c].empty()) continue;
-        CopyArgs a{};
+        CopyArgs &a = args[c];
         a.items = dev_list + first;
         a.cache = static_cast<const uint64_t *>(slot.dev);
         a.n_items = static_cast<uint32_t>(items[c].size());
@@ -629,18 +629,25 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         a.row_vec = static_cast<uint32_t>(static_cast<uint64_t>(p.spec.head_dim) * p.spec.elem_bytes / 16);
         a.layout = p.spec.pool_layout;
         first += items[c].size();
+    }
+    TimedCall *tc = p.timing ? &p.timed.back() : nullptr;
+    auto launch = [&](uint32_t c, hipStream_t st) {
         const LaunchCfg &lc = p.launch[c][op];
-        check_hip(hipStreamWaitEvent(cls_stream[c], p.fork, 0), "hipStreamWaitEvent");
-        TimedCall *tc = p.timing ? &p.timed.back() : nullptr;
-        if (tc) check_hip(hipEventRecord(tc->t0[c], cls_stream[c]), "hipEventRecord");
-        check_hip(launch_chunk_copy(a, c, gather, lc.grid, lc.flags, cls_stream[c]), "kernel launch");
+        if (tc) check_hip(hipEventRecord(tc->t0[c], st), "hipEventRecord");
+        check_hip(launch_chunk_copy(args[c], c, gather, lc.grid, lc.flags, st), "kernel launch");
         if (tc) {
-            check_hip(hipEventRecord(tc->t1[c], cls_stream[c]), "hipEventRecord");
+            check_hip(hipEventRecord(tc->t1[c], st), "hipEventRecord");
             tc->ran[c] = true;
         }
-        check_hip(hipEventRecord(cls_done[c], cls_stream[c]), "hipEventRecord");
-        check_hip(hipStreamWaitEvent(s, cls_done[c], 0), "hipStreamWaitEvent");
+    };
+    const bool staging = !items[KVP_CLASS_STAGING].empty();
+    if (staging) {
+        check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
+        launch(KVP_CLASS_STAGING, p.s_stage);
+        check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
     }
+    if (!items[KVP_CLASS_HOST].empty()) launch(KVP_CLASS_HOST, s);
+    if (staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     check_hip(hipEventRecord(slot.done, s), "hipEventRecord");
     for (RequestRec *rec : touched) {
         check_hip(hipEventRecord(rec->busy, s), "hipEventRecord");
@@ -675,7 +682,7 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
             const Region &reg = p.regions[r];
             const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
             n_host += cls == KVP_CLASS_HOST;
-            hipStream_t st = cls == KVP_CLASS_HOST ? p.s_host : p.s_stage;
+            hipStream_t st = p.s_stage;   // one probe at a time
             const uint64_t n = std::min<uint64_t>(probe_bytes, reg.capacity) & ~15ull;
             const LaunchCfg &lc = p.launch[cls][KVP_OP_RETRIEVE];
             float best = 0.f;

@@ -46,7 +46,8 @@ class WorkloadRun:
         self._ptrs = {}           # id(cache) -> (K pointers, V pointers), computed once
         self.maps = {}            # request_id -> placed map (present prefix)
         self.retrieve_maps = {}   # request_id -> map of the whole context (absent tail)
-        self.streams = [torch.cuda.Stream(device=dev) for _ in range(wl.n_streams)]
+        # one caller stream per concurrent request; a single-stream workload uses the current stream
+        self.streams = [torch.cuda.Stream(device=dev) for _ in range(wl.n_streams)] if wl.n_streams > 1 else []
 
     # ---- pointers
     def layer_ptrs(self, cache):
@@ -105,7 +106,7 @@ class WorkloadRun:
         """One retrieve per request; request i on stream i % n_streams (forked from the current stream)."""
         torch = self.torch
         cur = torch.cuda.current_stream(self.device)
-        if len(self.streams) == 1:
+        if len(self.streams) <= 1:
             for q in self.wl.requests:
                 self.retrieve(q, cur)
             return
