@@ -268,11 +268,16 @@ def pipeline(args):
     import torch
 
     from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
     from paper_2606_14779_amd.runner import WorkloadRun
 
     wl = workloads.make(args.config)
     sh = wl.shape
     run = WorkloadRun(wl, device=0)
+    if args.sdma:
+        if args.copy_ring_mib:
+            run.pool.set_copy_ring(args.copy_ring_mib << 20)
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     run.setup()
     q = wl.requests[0]
     kp, vp = run.layer_ptrs(run.dst)
@@ -326,6 +331,7 @@ def pipeline(args):
         log(json.dumps(rows[-1]))
     print(json.dumps({"metric": "blocked I/O time with layerwise pipelining (stand-in compute)",
                       "workload": wl.name, "layers": sh.layers, "retrieve_only_ms": round(retrieve_only, 2),
+                      "host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                       "gemm_8192_ms": round(one, 3), "rows": rows}), flush=True)
     run.close()
 
@@ -345,6 +351,9 @@ def main():
     ap.add_argument("--staging-flags", type=int, default=0)
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
+    ap.add_argument("--sdma", action="store_true",
+                    help="host class through the copy engines and an HBM ring instead of the zero-copy kernel")
+    ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
     ap.add_argument("--pipeline", action="store_true",
                     help="instead of the bench line, overlap per-layer retrieval with stand-in compute")
     ap.add_argument("--ablation", action="store_true",
@@ -380,6 +389,11 @@ def main():
     t_create = time.perf_counter() - t
     if args.host_grid or args.host_flags:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
+    if args.sdma:
+        if args.copy_ring_mib:
+            run.pool.set_copy_ring(args.copy_ring_mib << 20)
+        for op in (K.OP_RETRIEVE, K.OP_STORE):
+            run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
     if args.staging_grid or args.staging_flags:
         run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
     log("pool created in %.1f s" % t_create)
@@ -512,7 +526,8 @@ def main():
     if host_blocks:
         achieved = host_bytes / (dominant_ms / 1e3) / 1e9
         tr = pmc_traffic(wl.name, "host_region_copy<true, 0,")
-        roof = {"bound": "pcie", "kernel": "host_region_copy (zero-copy gather from pinned host regions)",
+        roof = {"bound": "pcie", "kernel": "host_region_copy (zero-copy gather from pinned host regions)"
+                if not args.sdma else "host class by copy engines (hipMemcpy into an HBM ring) + HBM ring scatter",
                 "achieved": round(achieved, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PCIE5_X16_GBPS, 4),
                 "traffic": round(tr["fetch_bytes"] + tr["write_bytes"]) if tr else None,
@@ -579,7 +594,8 @@ def main():
         "store_ms": round(store_wall * 1e3, 1),
         "store_kernels_ms": store_t,
         "cpu_baseline": cpu,
-        "launch": {"host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,
+        "launch": {"host_transport": "copy engines" if args.sdma else "zero-copy kernel",
+                   "host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,
                    "host_flags": args.host_flags, "staging_flags": args.staging_flags,
                    "coherence": args.coherence},
     }

@@ -293,17 +293,51 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
                                     (probe: 256 x 4-vector tiles instead of 256 x 8) */
 #define KVP_LAUNCH_XCD      16u  /* renumber workgroups so that each of the 8 XCDs takes
                                     contiguous units (grids that are multiples of 8) */
+#define KVP_LAUNCH_SDMA     32u  /* host class only: copy-engine transport (below) */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
  * class 12 workgroups (16 for the token-major store); staging class 65536
  * with KVP_LAUNCH_SPLIT2 for the pool_layout 0 retrieve, else 8192;
  * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
- * pool_layout 1 except the host-class store.  Errors: INVALID. */
+ * pool_layout 1 except the host-class store.
+ *
+ * KVP_LAUNCH_SDMA (host class, either op) replaces the zero-copy kernel by
+ * the GPU's copy engines: a call's host-class blocks, grouped per region into
+ * runs at consecutive offsets (one run per region for a placed request, whose
+ * blocks share one range, Sec. 4.1.3), cross the host link as hipMemcpy
+ * copies (2-D with the block as pitch when only a layer range moves) on the
+ * pool's internal stream into a ring of 2 HBM slots of max(1 GiB, block
+ * bytes) each (kv_pool_set_copy_ring); the staging-class kernel (its grid and flags) moves each
+ * filled slot to or from the engine cache on `stream`, where the
+ * staging-class blocks are then moved too.  The copy engines hold no compute
+ * units while the bytes cross the link, so kernels running beside a retrieve
+ * keep the whole GPU; the price is one HBM write and read of the host bytes.
+ * (For device-to-host copies the HIP runtime may still pick a copy kernel of
+ * its own.)  The ring is allocated when the flag is first set (NOMEM if it
+ * does not fit) and kept until kv_pool_destroy; the grid and other flags of
+ * the host class are unused while it is set.  Results are identical to the
+ * kernel's.
+ * Errors: INVALID (unknown flags; KVP_LAUNCH_SDMA on the staging class or on
+ * a placement-only pool), NOMEM, HIP. */
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
 
+/* Bytes per slot of the copy-engine transport's 2-slot HBM ring (default
+ * 1 GiB); a slot always holds at least one block, so smaller requests are
+ * raised to the block size.  Each slot costs one hand-over between the copy
+ * stream and `stream` (tens to hundreds of microseconds on MI355X), so larger
+ * slots trade HBM for fewer hand-overs: a 128K-token LLaMA-shaped retrieve
+ * measured 204.6 ms with 1 GiB slots and 210-226 ms with 256 MiB ones.  An existing ring is freed after the
+ * work on it finishes and, if any host-class op uses KVP_LAUNCH_SDMA,
+ * reallocated at the new size right away.
+ *   slot_bytes   multiple of 4096 in [64 KiB, 64 GiB].
+ * Errors: INVALID (bad size, placement-only pool), NOMEM, HIP. */
+int kv_pool_set_copy_ring(kvp_pool *pool, uint64_t slot_bytes);
+
 typedef struct {
-    float    host_ms;         /* duration of the host-class kernel, -1 if none ran */
+    float    host_ms;         /* duration of the host-class kernel, -1 if none ran; with
+                                 KVP_LAUNCH_SDMA, from the first copy or kernel of the
+                                 host class to its last */
     float    staging_ms;      /* duration of the staging-class kernel, -1 if none ran */
     uint32_t host_blocks;     /* blocks read from / written to host regions */
     uint32_t staging_blocks;  /* blocks read from / written to staging regions */
@@ -312,7 +346,9 @@ typedef struct {
 /* Enable (1) or disable (0) HIP-event timing of the kernels store/retrieve
  * launch; either way the recorded history is cleared.  Timing events are
  * recorded on the stream each kernel runs on (the caller's stream for the
- * host class, the pool's internal stream for the staging class).
+ * host class, the pool's internal stream for the staging class; with
+ * KVP_LAUNCH_SDMA both classes time on the caller's stream, except a
+ * retrieve's host-class start, recorded before its first copy).
  * Errors: INVALID. */
 int kv_pool_set_timing(kvp_pool *pool, int enable);
 

@@ -19,6 +19,7 @@ void pool_transfer(Pool &, const kvp_loc *, uint32_t, const int32_t *, uint32_t,
 void pool_region_info(const Pool &, uint32_t, kvp_region_info *);
 void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
 void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
+void pool_set_copy_ring(Pool &, uint64_t);
 void pool_set_timing(Pool &, int);
 void pool_last_timing(Pool &, kvp_timing *);
 void pool_timing_summary(Pool &, kvp_timing_summary *);
@@ -188,6 +189,11 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths)
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)
 {
     return guarded([&] { kvp::pool_set_launch(impl(pool), cls, op, grid, flags); });
+}
+
+int kv_pool_set_copy_ring(kvp_pool *pool, uint64_t slot_bytes)
+{
+    return guarded([&] { kvp::pool_set_copy_ring(impl(pool), slot_bytes); });
 }
 
 int kv_pool_set_timing(kvp_pool *pool, int enable)

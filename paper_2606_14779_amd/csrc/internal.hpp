@@ -23,7 +23,8 @@ struct Error {
 };
 
 [[noreturn]] void fail(int code, const std::string &msg);
-void check_hip(hipError_t e, const char *what);
+void check_hip(hipError_t e, const char *what);   // on failure: clears the last error, throws HIP
+void clear_hip_error();                            // take a failed call's code off the thread
 
 // ---------------------------------------------------------------- placement (Sec. 4.1.2-4.1.3)
 
@@ -130,6 +131,9 @@ struct TimedCall {                // one store / retrieve recorded while timing 
     bool ran[2] = {false, false};
 };
 
+constexpr uint32_t kBounceSlots = 2;                 // copy-engine transport: ring slots
+constexpr uint64_t kBounceSlotMin = 1ull << 30;      //   default bytes per slot (one block at least)
+
 struct Pool {
     int device = -1;
     bool placement_only = true;
@@ -143,11 +147,23 @@ struct Pool {
     uint32_t next_gen = 1;
     std::mutex mu;
 
-    hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's)
+    hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's);
+                                       // with KVP_LAUNCH_SDMA the host-link copies' stream instead
     hipEvent_t fork = nullptr, stage_done = nullptr;
     std::vector<Slot> ring;
     uint32_t ring_next = 0;
     LaunchCfg launch[2][2];      // [class][op]
+
+    // copy-engine transport of the host class (KVP_LAUNCH_SDMA): hipMemcpy on
+    // s_stage between host regions and an HBM bounce ring, HBM kernel between
+    // the ring and the engine cache; allocated when first enabled
+    char *bounce = nullptr;
+    uint64_t bounce_slot_bytes = 0;
+    uint64_t bounce_slot_request = kBounceSlotMin;   // kv_pool_set_copy_ring
+    hipEvent_t bounce_filled[kBounceSlots] = {};
+    hipEvent_t bounce_free[kBounceSlots] = {};   // last reader / writer of the slot done
+    bool bounce_free_rec[kBounceSlots] = {};
+    uint32_t bounce_next = 0;
 
     bool timing = false;
     std::vector<TimedCall> timed;      // calls recorded since timing was enabled or last summarised

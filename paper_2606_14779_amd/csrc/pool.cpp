@@ -28,9 +28,15 @@ namespace kvp {
 
 void fail(int code, const std::string &msg) { throw Error{code, msg}; }
 
+// A failed HIP call also leaves its code as the thread's last error, which the
+// caller's next launch check would report as its own: the library takes it.
+void clear_hip_error() { (void)hipGetLastError(); }
+
 void check_hip(hipError_t e, const char *what)
 {
-    if (e != hipSuccess) fail(KVP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+    if (e == hipSuccess) return;
+    clear_hip_error();
+    fail(KVP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
 namespace {
@@ -121,8 +127,10 @@ void alloc_region(Region &r)
             NumaScope bind(r.desc.numa_node);
             e = hipHostMalloc(&p, r.capacity, flags);
         }
-        if (e != hipSuccess || !p)
+        if (e != hipSuccess || !p) {
+            clear_hip_error();
             fail(KVP_ERR_NOMEM, "hipHostMalloc of " + std::to_string(r.capacity) + " bytes: " + hipGetErrorString(e));
+        }
         r.host = p;
         void *d = nullptr;
         check_hip(hipHostGetDevicePointer(&d, p, 0), "hipHostGetDevicePointer");
@@ -131,8 +139,10 @@ void alloc_region(Region &r)
     } else {
         void *d = nullptr;
         hipError_t e = hipMalloc(&d, r.capacity);
-        if (e != hipSuccess || !d)
+        if (e != hipSuccess || !d) {
+            clear_hip_error();
             fail(KVP_ERR_NOMEM, "hipMalloc of " + std::to_string(r.capacity) + " bytes: " + hipGetErrorString(e));
+        }
         r.dev = d;
     }
 }
@@ -145,9 +155,51 @@ void free_slot(Slot &s)
     s.cap = 0;
 }
 
+// The copy-engine transport's ring and events (after the work on them).
+void release_bounce(Pool &p)
+{
+    if (p.s_stage) (void)hipStreamSynchronize(p.s_stage);
+    for (uint32_t j = 0; j < kBounceSlots; ++j) {
+        if (p.bounce_free_rec[j] && p.bounce_free[j]) (void)hipEventSynchronize(p.bounce_free[j]);
+        if (p.bounce_free[j]) (void)hipEventDestroy(p.bounce_free[j]);
+        if (p.bounce_filled[j]) (void)hipEventDestroy(p.bounce_filled[j]);
+        p.bounce_free[j] = p.bounce_filled[j] = nullptr;
+        p.bounce_free_rec[j] = false;
+    }
+    if (p.bounce) (void)hipFree(p.bounce);
+    p.bounce = nullptr;
+    p.bounce_slot_bytes = 0;
+    p.bounce_next = 0;
+}
+
+// Allocate the copy-engine transport's ring on first use.  Caller holds the
+// lock and the device scope.
+void ensure_bounce(Pool &p)
+{
+    if (p.bounce) return;
+    const uint64_t slot = round_up(std::max(p.bounce_slot_request, p.block_bytes), kSector);
+    try {
+        void *mem = nullptr;
+        if (hipMalloc(&mem, slot * kBounceSlots) != hipSuccess || !mem) {
+            clear_hip_error();
+            fail(KVP_ERR_NOMEM, "bounce ring of " + std::to_string(slot * kBounceSlots) + " bytes");
+        }
+        p.bounce = static_cast<char *>(mem);
+        p.bounce_slot_bytes = slot;
+        for (uint32_t j = 0; j < kBounceSlots; ++j) {
+            check_hip(hipEventCreateWithFlags(&p.bounce_filled[j], hipEventDisableTiming), "hipEventCreate");
+            check_hip(hipEventCreateWithFlags(&p.bounce_free[j], hipEventDisableTiming), "hipEventCreate");
+        }
+    } catch (...) {
+        release_bounce(p);
+        throw;
+    }
+}
+
 void release_gpu(Pool &p)
 {
     if (p.placement_only) return;
+    release_bounce(p);
     if (p.s_stage) (void)hipStreamSynchronize(p.s_stage);
     for (auto &s : p.ring) {
         if (s.pending && s.done) (void)hipEventSynchronize(s.done);
@@ -499,9 +551,12 @@ Slot &acquire_slot(Pool &p, size_t bytes)
         free_slot(s);
         const size_t cap = round_up(std::max(bytes, kSlotMin), kSlotMin);
         void *h = nullptr, *d = nullptr;
-        if (hipHostMalloc(&h, cap, hipHostMallocDefault) != hipSuccess || !h)
+        if (hipHostMalloc(&h, cap, hipHostMallocDefault) != hipSuccess || !h) {
+            clear_hip_error();
             fail(KVP_ERR_NOMEM, "work-list pinned buffer");
+        }
         if (hipMalloc(&d, cap) != hipSuccess || !d) {
+            clear_hip_error();
             (void)hipHostFree(h);
             fail(KVP_ERR_NOMEM, "work-list device buffer");
         }
@@ -510,6 +565,68 @@ Slot &acquire_slot(Pool &p, size_t bytes)
         s.cap = cap;
     }
     return s;
+}
+
+}  // namespace
+
+namespace {
+
+// One host-link copy of the copy-engine transport: `blocks` blocks of one
+// region at consecutive offsets, the moved part of each (`width` bytes from
+// byte `skip` of the block) packed back to back in a ring slot.
+struct LinkRun {
+    uint32_t region;
+    uint64_t offset;        // of the first block in the region
+    uint32_t blocks;
+    uint64_t slot_offset;   // where the first block's part sits in the ring slot
+};
+
+// The blocks that go through one ring slot: items [first, first + n) of the
+// host-class work list and runs [run0, run0 + runs).
+struct Batch {
+    uint32_t ring;
+    uint32_t first, n;
+    size_t run0, runs;
+};
+
+struct HostBlock {
+    uint32_t region;
+    uint64_t offset;
+    uint32_t slot;
+};
+
+// Pack a call's host-class blocks into ring slots.  Blocks are grouped by
+// region (stable, so a placed request's blocks in a region stay at
+// consecutive offsets) and cut into runs wherever the offsets stop being
+// consecutive or a slot fills up.  Each work item addresses its block's part
+// in the slot, less chunk0 chunks: the kernel adds (chunk0 + k) chunks.
+void plan_bounce(const Pool &p, std::vector<HostBlock> &blocks, uint64_t width, uint32_t chunk0,
+                 std::vector<CopyItem> &items, std::vector<LinkRun> &runs, std::vector<Batch> &batches)
+{
+    std::stable_sort(blocks.begin(), blocks.end(),
+                     [](const HostBlock &x, const HostBlock &y) { return x.region < y.region; });
+    const uint64_t per_slot = p.bounce_slot_bytes / width;   // >= 1: width <= block bytes <= slot bytes
+    const uint64_t rebase = static_cast<uint64_t>(chunk0) * p.chunk_bytes;
+    uint64_t used = per_slot;   // forces a first batch
+    for (const HostBlock &hb : blocks) {
+        if (used == per_slot) {
+            const uint32_t ring = static_cast<uint32_t>((p.bounce_next + batches.size()) % kBounceSlots);
+            batches.push_back(Batch{ring, static_cast<uint32_t>(items.size()), 0u, runs.size(), 0});
+            used = 0;
+        }
+        Batch &bt = batches.back();
+        LinkRun *last = bt.runs ? &runs.back() : nullptr;
+        if (last && last->region == hb.region && last->offset + last->blocks * p.block_bytes == hb.offset) {
+            ++last->blocks;
+        } else {
+            runs.push_back(LinkRun{hb.region, hb.offset, 1u, used * width});
+            ++bt.runs;
+        }
+        const uint64_t at = reinterpret_cast<uint64_t>(p.bounce) + bt.ring * p.bounce_slot_bytes + used * width;
+        items.push_back(CopyItem{at - rebase, hb.slot, 0u});   // unsigned wrap is exact
+        ++bt.n;
+        ++used;
+    }
 }
 
 }  // namespace
@@ -534,9 +651,12 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
 
     std::lock_guard<std::mutex> lock(p.mu);
     DeviceScope dev(p.device);
+    const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
+    const bool sdma = (p.launch[KVP_CLASS_HOST][op].flags & KVP_LAUNCH_SDMA) != 0;
 
     // GLT-resolved locations, grouped by region class (Sec. 4.3)
     std::vector<CopyItem> items[2];
+    std::vector<HostBlock> host_blocks;   // copy-engine transport: placed in ring slots below
     std::vector<RequestRec *> touched;
     std::vector<uint64_t> targets;   // store: (region, offset) keys; retrieve: destination slots
     // one hint per region: a request's blocks in a region share one range,
@@ -556,7 +676,10 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (std::find(touched.begin(), touched.end(), hint->owner) == touched.end()) touched.push_back(hint->owner);
         const Region &r = p.regions[e.region];
         const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
-        items[cls].push_back(CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
+        if (cls == KVP_CLASS_HOST && sdma)
+            host_blocks.push_back(HostBlock{e.region, e.offset, static_cast<uint32_t>(slot)});
+        else
+            items[cls].push_back(CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
     }
     // no two present entries may write the same place (a destination slot on
     // retrieve, a pool block on store): sorted keys, independent of num_slots
@@ -565,8 +688,13 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     if (dup != targets.end())
         fail(KVP_ERR_INVALID, gather ? "destination slot " + std::to_string(*dup) + " named twice"
                                      : std::string("two map entries name the same pool block"));
+    const uint64_t width = 2ull * (layer_end - layer_begin) * p.chunk_bytes;   // bytes moved per block
+    const uint64_t skip = 2ull * layer_begin * p.chunk_bytes;
+    std::vector<LinkRun> runs;
+    std::vector<Batch> batches;
+    if (!host_blocks.empty()) plan_bounce(p, host_blocks, width, 2 * layer_begin, items[KVP_CLASS_HOST], runs, batches);
+
     const size_t n_items = items[0].size() + items[1].size();
-    const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
     if (p.timing) {
         if (p.timed.size() >= kMaxTimedCalls) drain_timed(p, nullptr);   // bound the history
         TimedCall tc;
@@ -641,13 +769,80 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         }
     };
     const bool staging = !items[KVP_CLASS_STAGING].empty();
-    if (staging) {
-        check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
-        launch(KVP_CLASS_STAGING, p.s_stage);
-        check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
+    if (batches.empty()) {
+        if (staging) {
+            check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
+            launch(KVP_CLASS_STAGING, p.s_stage);
+            check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
+        }
+        if (!items[KVP_CLASS_HOST].empty()) launch(KVP_CLASS_HOST, s);
+        if (staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
+    } else {
+        // Copy-engine transport: the host-link copies take the internal
+        // stream (no stream beyond the kernel path's two) and every kernel
+        // runs on the caller's stream -- the staging class first, then one
+        // ring-slot kernel per batch.  A slot is refilled only after its
+        // previous contents were consumed (by any call, either op).
+        if (staging) launch(KVP_CLASS_STAGING, s);
+        const LaunchCfg &lc = p.launch[KVP_CLASS_STAGING][op];
+        const hipMemcpyKind kind = gather ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost;
+        hipStream_t sc = p.s_stage;
+        auto link_copies = [&](const Batch &bt) {
+            char *ring = p.bounce + static_cast<uint64_t>(bt.ring) * p.bounce_slot_bytes;
+            for (size_t i = bt.run0; i < bt.run0 + bt.runs; ++i) {
+                const LinkRun &run = runs[i];
+                char *host = static_cast<char *>(p.regions[run.region].host) + run.offset + skip;
+                char *dev = ring + run.slot_offset;
+                void *dst = gather ? static_cast<void *>(dev) : static_cast<void *>(host);
+                const void *src = gather ? static_cast<const void *>(host) : static_cast<const void *>(dev);
+                if (width == p.block_bytes)
+                    check_hip(hipMemcpyAsync(dst, src, run.blocks * width, kind, sc), "hipMemcpyAsync");
+                else
+                    check_hip(hipMemcpy2DAsync(dst, gather ? width : p.block_bytes, src, gather ? p.block_bytes : width,
+                                               width, run.blocks, kind, sc),
+                              "hipMemcpy2DAsync");
+            }
+        };
+        auto ring_kernel = [&](const Batch &bt) {
+            CopyArgs a = args[KVP_CLASS_HOST];
+            a.items = dev_list + bt.first;
+            a.n_items = bt.n;
+            check_hip(launch_chunk_copy(a, KVP_CLASS_STAGING, gather, lc.grid, lc.flags, s), "kernel launch");
+        };
+        if (gather) {
+            check_hip(hipStreamWaitEvent(sc, p.fork, 0), "hipStreamWaitEvent");
+            if (tc) check_hip(hipEventRecord(tc->t0[KVP_CLASS_HOST], sc), "hipEventRecord");
+            for (const Batch &bt : batches) {
+                if (p.bounce_free_rec[bt.ring])
+                    check_hip(hipStreamWaitEvent(sc, p.bounce_free[bt.ring], 0), "hipStreamWaitEvent");
+                link_copies(bt);
+                check_hip(hipEventRecord(p.bounce_filled[bt.ring], sc), "hipEventRecord");
+                check_hip(hipStreamWaitEvent(s, p.bounce_filled[bt.ring], 0), "hipStreamWaitEvent");
+                ring_kernel(bt);
+                check_hip(hipEventRecord(p.bounce_free[bt.ring], s), "hipEventRecord");
+                p.bounce_free_rec[bt.ring] = true;
+            }
+        } else {
+            if (tc) check_hip(hipEventRecord(tc->t0[KVP_CLASS_HOST], s), "hipEventRecord");
+            for (const Batch &bt : batches) {
+                if (p.bounce_free_rec[bt.ring])
+                    check_hip(hipStreamWaitEvent(s, p.bounce_free[bt.ring], 0), "hipStreamWaitEvent");
+                ring_kernel(bt);
+                check_hip(hipEventRecord(p.bounce_filled[bt.ring], s), "hipEventRecord");
+                check_hip(hipStreamWaitEvent(sc, p.bounce_filled[bt.ring], 0), "hipStreamWaitEvent");
+                link_copies(bt);
+                check_hip(hipEventRecord(p.bounce_free[bt.ring], sc), "hipEventRecord");
+                p.bounce_free_rec[bt.ring] = true;
+            }
+            check_hip(hipEventRecord(p.stage_done, sc), "hipEventRecord");
+            check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
+        }
+        p.bounce_next = static_cast<uint32_t>((p.bounce_next + batches.size()) % kBounceSlots);
+        if (tc) {
+            check_hip(hipEventRecord(tc->t1[KVP_CLASS_HOST], s), "hipEventRecord");
+            tc->ran[KVP_CLASS_HOST] = true;
+        }
     }
-    if (!items[KVP_CLASS_HOST].empty()) launch(KVP_CLASS_HOST, s);
-    if (staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     check_hip(hipEventRecord(slot.done, s), "hipEventRecord");
     for (RequestRec *rec : touched) {
         check_hip(hipEventRecord(rec->busy, s), "hipEventRecord");
@@ -671,8 +866,10 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
 {
     probe_bytes &= ~15ull;
     void *scratch = nullptr;
-    if (hipMalloc(&scratch, probe_bytes) != hipSuccess || !scratch)
+    if (hipMalloc(&scratch, probe_bytes) != hipSuccess || !scratch) {
+        clear_hip_error();
         fail(KVP_ERR_NOMEM, "probe scratch of " + std::to_string(probe_bytes) + " bytes");
+    }
     hipEvent_t e0 = nullptr, e1 = nullptr;
     try {
         check_hip(hipEventCreate(&e0), "hipEventCreate");
@@ -770,11 +967,34 @@ void pool_region_read(Pool &p, uint32_t region, uint64_t offset, uint64_t bytes,
 void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)
 {
     if (cls > 1 || op > 1) fail(KVP_ERR_INVALID, "class and op must be 0 or 1");
-    if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS | KVP_LAUNCH_SPLIT2 | KVP_LAUNCH_XCD))
+    if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS | KVP_LAUNCH_SPLIT2 | KVP_LAUNCH_XCD |
+                  KVP_LAUNCH_SDMA))
         fail(KVP_ERR_INVALID, "unknown flags");
     if (grid > (1u << 20)) fail(KVP_ERR_INVALID, "grid too large");
+    if ((flags & KVP_LAUNCH_SDMA) && cls != KVP_CLASS_HOST)
+        fail(KVP_ERR_INVALID, "the copy-engine transport is for the host class");
+    if ((flags & KVP_LAUNCH_SDMA) && p.placement_only)
+        fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
     std::lock_guard<std::mutex> lock(p.mu);
+    if (flags & KVP_LAUNCH_SDMA) {
+        DeviceScope dev(p.device);
+        ensure_bounce(p);
+    }
     p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op, p.spec), flags};  // flags taken as given
+}
+
+void pool_set_copy_ring(Pool &p, uint64_t slot_bytes)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
+    if (slot_bytes % kSector || slot_bytes < (64u << 10) || slot_bytes > (1ull << 36))
+        fail(KVP_ERR_INVALID, "slot_bytes must be a multiple of 4096 in [64 KiB, 64 GiB]");
+    std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+    release_bounce(p);
+    p.bounce_slot_request = slot_bytes;
+    if ((p.launch[KVP_CLASS_HOST][KVP_OP_RETRIEVE].flags | p.launch[KVP_CLASS_HOST][KVP_OP_STORE].flags) &
+        KVP_LAUNCH_SDMA)
+        ensure_bounce(p);
 }
 
 void pool_set_timing(Pool &p, int enable)

@@ -24,7 +24,7 @@ HOST_DEFAULT, HOST_COHERENT, HOST_NONCOHERENT = 0, 1, 2
 ABSENT = 0xFFFFFFFF
 CLASS_HOST, CLASS_STAGING = 0, 1
 OP_RETRIEVE, OP_STORE = 0, 1
-LAUNCH_NT_LOAD, LAUNCH_NT_STORE, LAUNCH_LDS, LAUNCH_SPLIT2, LAUNCH_XCD = 1, 2, 4, 8, 16
+LAUNCH_NT_LOAD, LAUNCH_NT_STORE, LAUNCH_LDS, LAUNCH_SPLIT2, LAUNCH_XCD, LAUNCH_SDMA = 1, 2, 4, 8, 16, 32
 MEASURE_SHARED_LINK = 1
 
 LOC_DTYPE = np.dtype([("region", "<u4"), ("gen", "<u4"), ("offset", "<u8")])
@@ -98,6 +98,7 @@ _SIGS = {
     "kv_pool_measure_bandwidth": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_set_bandwidths": (_i32, [_vp, _vp]),
     "kv_pool_set_launch": (_i32, [_vp, _u32, _u32, _u32, _u32]),
+    "kv_pool_set_copy_ring": (_i32, [_vp, _u64]),
     "kv_pool_set_timing": (_i32, [_vp, _i32]),
     "kv_pool_last_timing": (_i32, [_vp, _vp]),
     "kv_pool_timing_summary": (_i32, [_vp, _vp]),
@@ -291,6 +292,9 @@ class KVPool:
     # ---- launch configuration and timing
     def set_launch(self, cls: int, op: int, grid: int = 0, flags: int = 0) -> None:
         _check(_lib.kv_pool_set_launch(self._h, cls, op, grid, flags))
+
+    def set_copy_ring(self, slot_bytes: int) -> None:
+        _check(_lib.kv_pool_set_copy_ring(self._h, slot_bytes))
 
     def set_timing(self, enable: bool) -> None:
         _check(_lib.kv_pool_set_timing(self._h, 1 if enable else 0))

@@ -437,6 +437,8 @@ def test_allocation_failure_reports_nomem_and_cleans_up():
     with pytest.raises(K.KVPoolError) as ei:
         K.KVPool([K.Region("staging", 1 << 30), K.Region("staging", 1 << 46)], [1, 1], spec, 0)
     assert ei.value.name == "NOMEM"
+    # the failed allocation leaves no HIP error behind for the caller's next launch check
+    assert int(torch.full((16,), 3, device="cuda").sum()) == 48
     torch.cuda.synchronize()
     assert torch.cuda.mem_get_info()[0] >= free_before - (64 << 20)
     with K.KVPool([K.Region("staging", 1 << 30)], [1], spec, 0) as p:

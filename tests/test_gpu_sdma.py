@@ -1,0 +1,232 @@
+"""GPU parity of the copy-engine transport of the host class (KVP_LAUNCH_SDMA).
+
+The host-link bytes move by hipMemcpy through an HBM ring and the HBM kernel
+moves them between the ring and the engine cache; the result must be the
+oracle's, bit for bit, exactly as with the zero-copy kernel.  Cases cover
+both ops and layouts, layer ranges (2-D copies), runs broken by absent
+entries, the ring wrapping inside one call and across calls, and the mixing
+of the two transports on one pool.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from kvgen import workloads
+from paper_2606_14779_amd import kvpool as K
+from paper_2606_14779_amd.runner import SENTINEL
+
+from gpu_util import check_full, make_run, oracle_expectation, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _sdma(run, ops=(K.OP_RETRIEVE, K.OP_STORE)):
+    for op in ops:
+        run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+@pytest.mark.parametrize("layout", [0, 1])
+def test_sdma_store_and_retrieve(cfg, layout):
+    wl = workloads.make(cfg, max_blocks=61, layout=layout)
+    say("case sdma", wl.name, "layout", layout, "blocks", [q.n_present for q in wl.requests])
+    run = make_run(wl)
+    try:
+        _sdma(run)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def test_sdma_ring_wraps_inside_one_call():
+    """520 LLaMA blocks of 2 MiB on two host regions through 256 MiB slots:
+    five batches over the two slots in one call, twice."""
+    wl = workloads.make(1, max_blocks=520)
+    say("case sdma ring wrap")
+    run = make_run(wl)
+    try:
+        run.pool.set_copy_ring(256 << 20)
+        _sdma(run)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        run.fill_dst()                  # stream-ordered after the first retrieve
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_sdma_one_block_slots(layout):
+    """Slots raised to one block: every block is its own batch and the ring
+    wraps many times inside each call, both ops."""
+    wl = workloads.make(3, max_blocks=47, layout=layout)
+    say("case sdma one-block slots", layout)
+    run = make_run(wl)
+    try:
+        run.pool.set_copy_ring(64 << 10)
+        _sdma(run)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+        run.pool.set_copy_ring(8 << 20)       # four blocks a slot, reallocated while enabled
+        run.fill_dst()
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("store_sdma,retrieve_sdma", [(False, True), (True, False)])
+def test_sdma_mixed_with_kernel(store_sdma, retrieve_sdma):
+    wl = workloads.make(2, max_blocks=45)
+    say("case sdma mixed", store_sdma, retrieve_sdma)
+    run = make_run(wl)
+    try:
+        _sdma(run, ([K.OP_STORE] if store_sdma else []) + ([K.OP_RETRIEVE] if retrieve_sdma else []))
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_sdma_layer_ranges(layout):
+    """Per-layer retrieve and layer-group store move part of each block (2-D copies)."""
+    wl = workloads.make(2, max_blocks=37, layout=layout)
+    say("case sdma layers", layout)
+    run = make_run(wl)
+    try:
+        _sdma(run)
+        host = run.fill_source(keep_host=True)
+        run.fill_dst()
+        run.place_all()
+        q = wl.requests[0]
+        L = wl.shape.layers
+        s = torch.cuda.current_stream().cuda_stream
+        skp, svp = run.layer_ptrs(run.src)
+        for lo, hi in [(0, 5), (5, 6), (6, L)]:
+            run.pool.store_layers(run.maps[q.request_id], q.src_slots, wl.src_num_slots, lo, hi, skp, svp, s)
+        kp, vp = run.layer_ptrs(run.dst)
+        m = run.retrieve_maps[q.request_id]
+        for l in range(L):
+            run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, l, l + 1, kp, vp, s)
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+        run.fill_dst()
+        kp_part = [p if 3 <= l < 7 else 0 for l, p in enumerate(kp)]
+        vp_part = [p if 3 <= l < 7 else 0 for l, p in enumerate(vp)]
+        run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, 3, 7, kp_part, vp_part, s)
+        torch.cuda.synchronize()
+        _, _, expect = oracle_expectation(wl, run, host)
+        got = run.dst.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got[3:7], expect[3:7])
+        assert np.all(got[:3] == SENTINEL) and np.all(got[7:] == SENTINEL)
+    finally:
+        run.close()
+
+
+def test_sdma_runs_broken_by_absent_entries():
+    """Absent entries and a reordered map split a region's blocks into many runs."""
+    wl = workloads.make(2, max_blocks=60)
+    say("case sdma absent")
+    run = make_run(wl)
+    try:
+        _sdma(run)
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        m = run.retrieve_maps[q.request_id].copy()
+        table = q.dst_slots.copy()
+        rng = np.random.default_rng(5)
+        skip = np.sort(rng.choice(q.n_blocks, size=q.n_blocks // 4, replace=False))
+        m["region"][skip] = K.ABSENT
+        order = rng.permutation(q.n_blocks)          # entries in any order: same result
+        m, table = m[order], table[order]
+        table[np.isin(order, skip)] = -1             # never read for absent entries
+        kp, vp = run.layer_ptrs(run.dst)
+        run.pool.retrieve(m, table, wl.dst_num_slots, kp, vp, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        maps, regions, _ = oracle_expectation(wl, run, host)
+        sh = wl.shape
+        L = sh.layers
+        expect = np.full(tuple(run.dst.shape), SENTINEL, np.uint16)
+        om = maps[q.request_id]
+        full = np.zeros(q.n_blocks, dtype=oracle.LOC_DTYPE)
+        full[:q.n_present] = om
+        full["region"][q.n_present:] = oracle.ABSENT
+        full["region"][skip] = oracle.ABSENT
+        oracle.gather(full[order], np.where(table < 0, 0, table), regions, [expect[l, 0] for l in range(L)],
+                      [expect[l, 1] for l in range(L)], (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes),
+                      wl.layout)
+        got = run.dst.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, expect)
+    finally:
+        run.close()
+
+
+def test_sdma_ragged_chunk_and_timing():
+    shape = workloads.KVShape("ragged", 3, 3, 24)    # chunk 2304 B: not a multiple of 32
+    regions = [workloads.RegionSpec("host", 2, 0), workloads.RegionSpec("staging", 3),
+               workloads.RegionSpec("host", 1, 1)]
+    n = 29
+    rng = np.random.default_rng(n)
+    src = rng.permutation(n + 3)[:n].astype(np.int32)
+    dst = rng.permutation(n + 3)[:n].astype(np.int32)
+    req = workloads.RequestSpec(1, n, n, src, dst)
+    wl = workloads.Workload(0, "custom", 77, shape, 0, regions, [req], n + 3, n + 3)
+    workloads._size_regions(wl.regions, [n], shape.block_bytes)
+    say("case sdma ragged")
+    run = make_run(wl)
+    try:
+        _sdma(run)
+        run.pool.set_timing(True)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        t = run.pool.last_timing()
+        assert t["host_ms"] > 0 and t["staging_ms"] > 0
+        assert t["host_blocks"] + t["staging_blocks"] == n
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def test_sdma_flag_validation():
+    wl = workloads.make(2, max_blocks=8)
+    run = make_run(wl)
+    try:
+        for op in (K.OP_RETRIEVE, K.OP_STORE):
+            with pytest.raises(K.KVPoolError) as ei:
+                run.pool.set_launch(K.CLASS_STAGING, op, 0, K.LAUNCH_SDMA)
+            assert ei.value.name == "INVALID"
+        _sdma(run)
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, 0)    # back to the kernel; ring kept
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+    p = K.KVPool([K.Region("host", 1 << 20)], [1], K.KVSpec(1, 1, 8), device=-1)
+    with pytest.raises(K.KVPoolError) as ei:
+        p.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+    assert ei.value.name == "INVALID"
+    p.close()

@@ -143,6 +143,9 @@ def test_transfers_rejected_without_device():
     assert _err(p.set_launch, 2, 0, 0, 0) == "INVALID"
     assert _err(p.set_launch, 0, 0, 0, 64) == "INVALID"
     p.set_launch(0, 0, 64, K.LAUNCH_NT_LOAD)
+    assert _err(p.set_launch, K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA) == "INVALID"   # nothing to copy with
+    assert _err(p.set_launch, K.CLASS_STAGING, K.OP_STORE, 0, K.LAUNCH_SDMA) == "INVALID"  # host class only
+    assert _err(p.set_copy_ring, 1 << 20) == "INVALID"                                     # no device
     info = p.region_info(0)
     assert info["device_ptr"] is None and info["capacity_bytes"] == 1 << 20
     assert _err(p.region_info, 1) == "INVALID"
