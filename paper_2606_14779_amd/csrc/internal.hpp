@@ -150,6 +150,10 @@ struct Pool {
     hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's);
                                        // with KVP_LAUNCH_SDMA the host-link copies' stream instead
     hipEvent_t fork = nullptr, stage_done = nullptr;
+    // host link, per direction [op]: the last host-class kernel enqueued; the
+    // next one (any stream) waits for it, so calls take the link in turn
+    hipEvent_t link_done[2] = {nullptr, nullptr};
+    bool link_rec[2] = {false, false};
     std::vector<Slot> ring;
     uint32_t ring_next = 0;
     LaunchCfg launch[2][2];      // [class][op]

@@ -212,7 +212,7 @@ void release_gpu(Pool &p)
         if (kv.second->stored) (void)hipEventDestroy(kv.second->stored);
         if (kv.second->busy) (void)hipEventDestroy(kv.second->busy);
     }
-    hipEvent_t *evs[] = {&p.fork, &p.stage_done};
+    hipEvent_t *evs[] = {&p.fork, &p.stage_done, &p.link_done[0], &p.link_done[1]};
     for (auto e : evs)
         if (*e) (void)hipEventDestroy(*e), *e = nullptr;
     for (auto &tc : p.timed)
@@ -333,6 +333,7 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         check_hip(hipStreamCreateWithFlags(&p->s_stage, hipStreamNonBlocking), "hipStreamCreate");
         check_hip(hipEventCreateWithFlags(&p->fork, hipEventDisableTiming), "hipEventCreate");
         check_hip(hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming), "hipEventCreate");
+        for (auto &e : p->link_done) check_hip(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate");
         p->ring.resize(kRingSlots);
         for (auto &s : p->ring) check_hip(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreate");
         if (!bandwidths) {
@@ -775,7 +776,14 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             launch(KVP_CLASS_STAGING, p.s_stage);
             check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
         }
-        if (!items[KVP_CLASS_HOST].empty()) launch(KVP_CLASS_HOST, s);
+        if (!items[KVP_CLASS_HOST].empty()) {
+            // one host-class kernel on the link at a time, in enqueue order:
+            // two of them would only share its bandwidth and both end late
+            if (p.link_rec[op]) check_hip(hipStreamWaitEvent(s, p.link_done[op], 0), "hipStreamWaitEvent");
+            launch(KVP_CLASS_HOST, s);
+            check_hip(hipEventRecord(p.link_done[op], s), "hipEventRecord");
+            p.link_rec[op] = true;
+        }
         if (staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     } else {
         // Copy-engine transport: the host-link copies take the internal
