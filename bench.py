@@ -354,6 +354,8 @@ def main():
     ap.add_argument("--sdma", action="store_true",
                     help="host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
+    ap.add_argument("--flush", action="store_true",
+                    help="overwrite 1 GiB before each timed step; ms_per_step is then the median event span")
     ap.add_argument("--pipeline", action="store_true",
                     help="instead of the bench line, overlap per-layer retrieval with stand-in compute")
     ap.add_argument("--ablation", action="store_true",
@@ -427,11 +429,16 @@ def main():
     # timed region: K retrieves back to back; the library records HIP events
     # around each kernel on the stream it runs on, summarised afterwards
     log("warm-up done; timing %d steps" % args.steps)
+    # --flush: before each step, overwrite 1 GiB (more than the 256 MiB Infinity Cache plus the L2s)
+    # on the same stream, so every step starts cold; the per-step event span then excludes the flush
+    flush = torch.empty(1 << 29, dtype=torch.int16, device="cuda") if args.flush else None
     run.pool.set_timing(True)
     spans, enqueue_ms = [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        if flush is not None:
+            flush.fill_(i)
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.record(cur)
         tq = time.perf_counter()
@@ -445,6 +452,9 @@ def main():
     run.pool.set_timing(False)
     span_ms = [s.elapsed_time(e) for s, e in spans]
     ms_per_step = wall / args.steps * 1e3
+    if flush is not None:        # the wall clock includes the flushes: rate per retrieve from the spans
+        ms_per_step = statistics.median(span_ms)
+        del flush
     gbps = wl.retrieved_bytes / (ms_per_step / 1e3) / 1e9
     host_avg = summ["host_ms_sum"] / summ["host_calls"] if summ["host_calls"] else None
     stage_avg = summ["staging_ms_sum"] / summ["staging_calls"] if summ["staging_calls"] else None
@@ -594,6 +604,7 @@ def main():
         "store_ms": round(store_wall * 1e3, 1),
         "store_kernels_ms": store_t,
         "cpu_baseline": cpu,
+        "caches_flushed_per_step": bool(args.flush),
         "launch": {"host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                    "host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,
                    "host_flags": args.host_flags, "staging_flags": args.staging_flags,
