@@ -352,7 +352,7 @@ def main():
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
     ap.add_argument("--sdma", action="store_true",
-                    help="host class through the copy engines and an HBM ring instead of the zero-copy kernel")
+                    help="retrieve the host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 1 GiB before each timed step; ms_per_step is then the median event span")
@@ -391,11 +391,10 @@ def main():
     t_create = time.perf_counter() - t
     if args.host_grid or args.host_flags:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
-    if args.sdma:
+    if args.sdma:        # retrieve only: the runtime copies device-to-host with a kernel of its own
         if args.copy_ring_mib:
             run.pool.set_copy_ring(args.copy_ring_mib << 20)
-        for op in (K.OP_RETRIEVE, K.OP_STORE):
-            run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     if args.staging_grid or args.staging_flags:
         run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
     log("pool created in %.1f s" % t_create)
