@@ -197,6 +197,47 @@ struct CopyArgs {
     uint32_t layout;           // 0 head-major, 1 token-major
 };
 
+// ---------------------------------------------------------------- copy-engine plan (bounce.cpp)
+
+struct HostBlock {         // one host-class block of a call
+    uint32_t region;
+    uint64_t offset;       // in the region
+    uint32_t slot;         // engine-cache slot
+};
+
+// One host-link copy: `blocks` blocks of one region at consecutive offsets,
+// the moved part of each (`width` bytes) packed back to back in a ring slot.
+struct LinkRun {
+    uint32_t region;
+    uint64_t offset;       // of the first block in the region
+    uint32_t blocks;
+    uint64_t slot_offset;  // where the first block's part sits in the ring slot
+};
+
+// The blocks that go through one ring slot: work items [first, first + n)
+// and runs [run0, run0 + runs).
+struct Batch {
+    uint32_t ring;
+    uint32_t first, n;
+    size_t run0, runs;
+};
+
+struct RingGeometry {
+    uint64_t base;         // device address of slot 0
+    uint64_t slot_bytes;   // >= block_bytes
+    uint32_t slots;
+    uint32_t next;         // ring slot of the first batch
+    uint64_t block_bytes;
+    uint64_t chunk_bytes;
+};
+
+// Pack a call's host-class blocks into ring slots: grouped by region
+// (stable), cut into runs where offsets stop being consecutive or a slot
+// fills.  Appends one work item per block, addressing the block's part in
+// its slot less chunk0 chunks (the kernel adds (chunk0 + k) chunks).
+void plan_bounce(const RingGeometry &g, std::vector<HostBlock> &blocks, uint64_t width, uint32_t chunk0,
+                 std::vector<CopyItem> &items, std::vector<LinkRun> &runs, std::vector<Batch> &batches);
+
 // cls: KVP_CLASS_HOST / KVP_CLASS_STAGING (selects the kernel entry point);
 // gather: pool -> cache (retrieve); !gather: cache -> pool (store)
 hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,

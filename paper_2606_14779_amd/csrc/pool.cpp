@@ -570,68 +570,6 @@ Slot &acquire_slot(Pool &p, size_t bytes)
 
 }  // namespace
 
-namespace {
-
-// One host-link copy of the copy-engine transport: `blocks` blocks of one
-// region at consecutive offsets, the moved part of each (`width` bytes from
-// byte `skip` of the block) packed back to back in a ring slot.
-struct LinkRun {
-    uint32_t region;
-    uint64_t offset;        // of the first block in the region
-    uint32_t blocks;
-    uint64_t slot_offset;   // where the first block's part sits in the ring slot
-};
-
-// The blocks that go through one ring slot: items [first, first + n) of the
-// host-class work list and runs [run0, run0 + runs).
-struct Batch {
-    uint32_t ring;
-    uint32_t first, n;
-    size_t run0, runs;
-};
-
-struct HostBlock {
-    uint32_t region;
-    uint64_t offset;
-    uint32_t slot;
-};
-
-// Pack a call's host-class blocks into ring slots.  Blocks are grouped by
-// region (stable, so a placed request's blocks in a region stay at
-// consecutive offsets) and cut into runs wherever the offsets stop being
-// consecutive or a slot fills up.  Each work item addresses its block's part
-// in the slot, less chunk0 chunks: the kernel adds (chunk0 + k) chunks.
-void plan_bounce(const Pool &p, std::vector<HostBlock> &blocks, uint64_t width, uint32_t chunk0,
-                 std::vector<CopyItem> &items, std::vector<LinkRun> &runs, std::vector<Batch> &batches)
-{
-    std::stable_sort(blocks.begin(), blocks.end(),
-                     [](const HostBlock &x, const HostBlock &y) { return x.region < y.region; });
-    const uint64_t per_slot = p.bounce_slot_bytes / width;   // >= 1: width <= block bytes <= slot bytes
-    const uint64_t rebase = static_cast<uint64_t>(chunk0) * p.chunk_bytes;
-    uint64_t used = per_slot;   // forces a first batch
-    for (const HostBlock &hb : blocks) {
-        if (used == per_slot) {
-            const uint32_t ring = static_cast<uint32_t>((p.bounce_next + batches.size()) % kBounceSlots);
-            batches.push_back(Batch{ring, static_cast<uint32_t>(items.size()), 0u, runs.size(), 0});
-            used = 0;
-        }
-        Batch &bt = batches.back();
-        LinkRun *last = bt.runs ? &runs.back() : nullptr;
-        if (last && last->region == hb.region && last->offset + last->blocks * p.block_bytes == hb.offset) {
-            ++last->blocks;
-        } else {
-            runs.push_back(LinkRun{hb.region, hb.offset, 1u, used * width});
-            ++bt.runs;
-        }
-        const uint64_t at = reinterpret_cast<uint64_t>(p.bounce) + bt.ring * p.bounce_slot_bytes + used * width;
-        items.push_back(CopyItem{at - rebase, hb.slot, 0u});   // unsigned wrap is exact
-        ++bt.n;
-        ++used;
-    }
-}
-
-}  // namespace
-
 void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t *table, uint32_t num_slots,
                    uint32_t layer_begin, uint32_t layer_end, void *const *k_layers, void *const *v_layers,
                    void *stream_ptr, bool gather)
@@ -693,7 +631,11 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     const uint64_t skip = 2ull * layer_begin * p.chunk_bytes;
     std::vector<LinkRun> runs;
     std::vector<Batch> batches;
-    if (!host_blocks.empty()) plan_bounce(p, host_blocks, width, 2 * layer_begin, items[KVP_CLASS_HOST], runs, batches);
+    if (!host_blocks.empty()) {
+        const RingGeometry g{reinterpret_cast<uint64_t>(p.bounce), p.bounce_slot_bytes, kBounceSlots, p.bounce_next,
+                             p.block_bytes, p.chunk_bytes};
+        plan_bounce(g, host_blocks, width, 2 * layer_begin, items[KVP_CLASS_HOST], runs, batches);
+    }
 
     const size_t n_items = items[0].size() + items[1].size();
     if (p.timing) {

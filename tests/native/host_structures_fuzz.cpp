@@ -6,9 +6,14 @@
 //                    backward-shift deletions
 //   target_counts    sum and per-region bounds of Eq. 2
 //   stripe           every region receives exactly its count
+//   plan_bounce      the copy-engine plan: every block exactly once, runs of
+//                    consecutive offsets in one region, every byte a copy or
+//                    the kernel touches inside its ring slot, and the
+//                    kernel's addresses equal to the copies' addresses
 //
-// Only placement.cpp and glt.cpp are linked; the two error helpers they call
-// are defined here.  Exit status 0 means every check held.
+// Only placement.cpp, glt.cpp and bounce.cpp are linked; the two error
+// helpers they call are defined here.  Exit status 0 means every check held.
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <map>
@@ -140,12 +145,83 @@ static void counts_and_stripe(std::mt19937_64 &rng)
     CHECK(threw);
 }
 
+static void bounce_plan(std::mt19937_64 &rng)
+{
+    for (int t = 0; t < 3000; ++t) {
+        const uint64_t chunk = 16 * (1 + rng() % 64);
+        const uint32_t L = 1 + rng() % 6;
+        const uint64_t block = 2 * L * chunk;
+        kvp::RingGeometry g{0x100000000ull + 4096 * (rng() % 1000), block * (1 + rng() % 9) + 16 * (rng() % 4), 
+                            static_cast<uint32_t>(1 + rng() % 4), 0, block, chunk};
+        g.next = static_cast<uint32_t>(rng() % g.slots);
+        const uint32_t l0 = rng() % L, l1 = l0 + 1 + rng() % (L - l0);
+        const uint64_t width = 2ull * (l1 - l0) * chunk;
+        // a few regions, each with one range of blocks, some entries dropped, in shuffled order
+        const uint32_t N = 1 + rng() % 5;
+        std::vector<kvp::HostBlock> in;
+        uint32_t slot = 0;
+        for (uint32_t r = 0; r < N; ++r) {
+            const uint64_t base = block * (rng() % 50);
+            const uint32_t cnt = rng() % 40;
+            for (uint32_t k = 0; k < cnt; ++k)
+                if (rng() % 5) in.push_back(kvp::HostBlock{r, base + k * block, slot++});
+        }
+        std::shuffle(in.begin(), in.end(), rng);
+        std::vector<kvp::HostBlock> blocks = in;
+        std::vector<kvp::CopyItem> items;
+        std::vector<kvp::LinkRun> runs;
+        std::vector<kvp::Batch> batches;
+        kvp::plan_bounce(g, blocks, width, 2 * l0, items, runs, batches);
+        CHECK(items.size() == in.size());
+        std::map<uint32_t, std::pair<uint32_t, uint64_t>> seen;   // slot -> (region, offset)
+        size_t next_item = 0, next_run = 0;
+        for (size_t b = 0; b < batches.size(); ++b) {
+            const kvp::Batch &bt = batches[b];
+            CHECK(bt.ring == (g.next + b) % g.slots);
+            CHECK(bt.first == next_item && bt.n > 0 && bt.run0 == next_run && bt.runs > 0);
+            CHECK(bt.n <= g.slot_bytes / width);
+            const uint64_t slot_base = g.base + bt.ring * g.slot_bytes;
+            uint64_t packed = 0;
+            size_t it = bt.first;
+            for (size_t q = bt.run0; q < bt.run0 + bt.runs; ++q) {
+                const kvp::LinkRun &run = runs[q];
+                CHECK(run.slot_offset == packed && run.blocks > 0);
+                CHECK(run.slot_offset + run.blocks * width <= g.slot_bytes);
+                if (q > bt.run0) {      // a new run only where the previous one cannot continue
+                    const kvp::LinkRun &prev = runs[q - 1];
+                    CHECK(prev.region != run.region || prev.offset + prev.blocks * block != run.offset);
+                }
+                for (uint32_t k = 0; k < run.blocks; ++k, ++it) {
+                    const kvp::CopyItem &ci = items[it];
+                    // the kernel reads / writes [pool + chunk0*C, + width): the copy's bytes
+                    CHECK(ci.pool + 2ull * l0 * chunk == slot_base + run.slot_offset + k * width);
+                    CHECK(seen.count(ci.slot) == 0);
+                    seen[ci.slot] = {run.region, run.offset + k * block};
+                }
+                packed += run.blocks * width;
+            }
+            CHECK(packed == bt.n * width && it == bt.first + bt.n);
+            next_item += bt.n;
+            next_run += bt.runs;
+        }
+        CHECK(next_item == items.size() && next_run == runs.size());
+        CHECK(seen.size() == in.size());
+        for (const kvp::HostBlock &hb : in) {
+            auto f = seen.find(hb.slot);
+            CHECK(f != seen.end() && f->second.first == hb.region && f->second.second == hb.offset);
+        }
+        // regions appear in order, each region's blocks in their input order
+        for (size_t q = 1; q < runs.size(); ++q) CHECK(runs[q - 1].region <= runs[q].region);
+    }
+}
+
 int main()
 {
     std::mt19937_64 rng(12345);
     for (int i = 0; i < 40; ++i) allocator_against_model(rng);
     glt_against_map(rng);
     counts_and_stripe(rng);
+    bounce_plan(rng);
     std::puts("host structures: all checks passed");
     return 0;
 }

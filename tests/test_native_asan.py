@@ -19,7 +19,8 @@ def test_host_structures_under_asan_ubsan(tmp_path):
            "-D__HIP_PLATFORM_AMD__", "-isystem", os.path.join(ROCM, "include"),
            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(ROOT, "tests", "native", "host_structures_fuzz.cpp"),
-           os.path.join(CSRC, "placement.cpp"), os.path.join(CSRC, "glt.cpp"), "-o", exe]
+           os.path.join(CSRC, "placement.cpp"), os.path.join(CSRC, "glt.cpp"), os.path.join(CSRC, "bounce.cpp"),
+           "-o", exe]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
