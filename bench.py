@@ -354,6 +354,7 @@ def main():
     ap.add_argument("--sdma", action="store_true",
                     help="retrieve the host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
+    ap.add_argument("--no-copy-engine", action="store_true", help="skip the copy-engine retrieve figure")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 1 GiB before each timed step; ms_per_step is then the median event span")
     ap.add_argument("--pipeline", action="store_true",
@@ -525,6 +526,24 @@ def main():
                      "ms_per_layer_max": round(max(per_layer), 3)}
         log("layerwise done: %.3f ms" % statistics.median(tot))
 
+    # the same request through the copy-engine transport (hipMemcpy into an HBM ring, ring kernel on the
+    # caller's stream): the option that leaves every CU to compute running beside a retrieve.  Last
+    # use of the pool's launch settings, so they need no restoring.
+    copy_engine = None
+    if host_blocks and not args.sdma and not args.no_copy_engine:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+        for _ in range(args.warmup):
+            run.retrieve_all()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            run.retrieve_all()
+        torch.cuda.synchronize()
+        ce_ms = (time.perf_counter() - t) / args.steps * 1e3
+        copy_engine = {"ms_per_step": round(ce_ms, 3), "gbps": round(wl.retrieved_bytes / ce_ms / 1e6, 2),
+                       "ring": "2 x 1 GiB HBM"}
+        log("copy-engine retrieve timed: %.3f ms" % ce_ms)
+
     pr = None if args.no_probes else probes(torch, K, run, int(args.probe_gib * 2**30) // 4096 * 4096)
     log("probes done")
     cpu = None if args.no_cpu_baseline else cpu_baseline(run, wl)
@@ -599,6 +618,7 @@ def main():
         "store": store,
         "roofline_store": store_roof,
         "layerwise": layerwise,
+        "copy_engine_retrieve": copy_engine,
         "place_ms": round(t_place * 1e3, 3),
         "store_ms": round(store_wall * 1e3, 1),
         "store_kernels_ms": store_t,

@@ -238,8 +238,10 @@ struct RingGeometry {
 void plan_bounce(const RingGeometry &g, std::vector<HostBlock> &blocks, uint64_t width, uint32_t chunk0,
                  std::vector<CopyItem> &items, std::vector<LinkRun> &runs, std::vector<Batch> &batches);
 
-// cls: KVP_CLASS_HOST / KVP_CLASS_STAGING (selects the kernel entry point);
+// cls: KVP_CLASS_HOST / KVP_CLASS_STAGING / kClassRing (selects the kernel
+// entry point: zero-copy host region, HBM staging region, copy-engine ring);
 // gather: pool -> cache (retrieve); !gather: cache -> pool (store)
+constexpr uint32_t kClassRing = 2;
 hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
                              hipStream_t s);
 hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid,

@@ -250,8 +250,9 @@ __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
     }
 }
 
-// One entry point per region class, so that traces and counters tell the
-// zero-copy (host link) kernel from the HBM staging kernel.
+// One entry point per kind of source, so that traces and counters tell the
+// zero-copy (host link) kernel, the HBM staging kernel and the kernel that
+// empties / fills a copy-engine ring slot apart.  The body is the same.
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __global__ __launch_bounds__(kThreads) void host_region_copy(CopyArgs a)
 {
@@ -260,6 +261,12 @@ __global__ __launch_bounds__(kThreads) void host_region_copy(CopyArgs a)
 
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __global__ __launch_bounds__(kThreads) void staging_region_copy(CopyArgs a)
+{
+    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
+}
+
+template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+__global__ __launch_bounds__(kThreads) void ring_slot_copy(CopyArgs a)
 {
     chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
 }
@@ -280,49 +287,51 @@ __global__ __launch_bounds__(kThreads) void probe_copy_kernel(const v4u *__restr
 
 // ---------------------------------------------------------------- host-side dispatch
 
-template <bool HOST, bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+template <uint32_t CLS, bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 static void launch_one(const CopyArgs &a, dim3 g, size_t lds, hipStream_t s)
 {
-    if constexpr (HOST)
+    if constexpr (CLS == KVP_CLASS_HOST)
         hipLaunchKernelGGL((host_region_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
-    else
+    else if constexpr (CLS == KVP_CLASS_STAGING)
         hipLaunchKernelGGL((staging_region_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
+    else
+        hipLaunchKernelGGL((ring_slot_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
 }
 
-template <bool HOST, bool GATHER, int FORM, int UNROLL>
+template <uint32_t CLS, bool GATHER, int FORM, int UNROLL>
 static hipError_t launch_form(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
 {
     const bool ntl = flags & KVP_LAUNCH_NT_LOAD, nts = flags & KVP_LAUNCH_NT_STORE;
     const dim3 g(grid);
     if (ntl && nts)
-        launch_one<HOST, GATHER, FORM, UNROLL, true, true>(a, g, lds, s);
+        launch_one<CLS, GATHER, FORM, UNROLL, true, true>(a, g, lds, s);
     else if (ntl)
-        launch_one<HOST, GATHER, FORM, UNROLL, true, false>(a, g, lds, s);
+        launch_one<CLS, GATHER, FORM, UNROLL, true, false>(a, g, lds, s);
     else if (nts)
-        launch_one<HOST, GATHER, FORM, UNROLL, false, true>(a, g, lds, s);
+        launch_one<CLS, GATHER, FORM, UNROLL, false, true>(a, g, lds, s);
     else
-        launch_one<HOST, GATHER, FORM, UNROLL, false, false>(a, g, lds, s);
+        launch_one<CLS, GATHER, FORM, UNROLL, false, false>(a, g, lds, s);
     return hipGetLastError();
 }
 
-template <bool HOST, bool GATHER, int FORM>
+template <uint32_t CLS, bool GATHER, int FORM>
 static hipError_t launch_unroll(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
 {
     // enough 16-byte loads in flight per lane to cover the whole unit, up to 8
     const uint64_t per_lane = (a.chunk_bytes / a.parts / 16 + kThreads - 1) / kThreads;
-    if (per_lane >= 8) return launch_form<HOST, GATHER, FORM, 8>(a, grid, flags, lds, s);
-    if (per_lane >= 4) return launch_form<HOST, GATHER, FORM, 4>(a, grid, flags, lds, s);
-    if (per_lane >= 2) return launch_form<HOST, GATHER, FORM, 2>(a, grid, flags, lds, s);
-    return launch_form<HOST, GATHER, FORM, 1>(a, grid, flags, lds, s);
+    if (per_lane >= 8) return launch_form<CLS, GATHER, FORM, 8>(a, grid, flags, lds, s);
+    if (per_lane >= 4) return launch_form<CLS, GATHER, FORM, 4>(a, grid, flags, lds, s);
+    if (per_lane >= 2) return launch_form<CLS, GATHER, FORM, 2>(a, grid, flags, lds, s);
+    return launch_form<CLS, GATHER, FORM, 1>(a, grid, flags, lds, s);
 }
 
-template <bool HOST, bool GATHER>
+template <uint32_t CLS, bool GATHER>
 static hipError_t launch_dir(const CopyArgs &a, uint32_t grid, uint32_t flags, hipStream_t s)
 {
-    if (a.layout == 0) return launch_unroll<HOST, GATHER, kPlain>(a, grid, flags, 0, s);
+    if (a.layout == 0) return launch_unroll<CLS, GATHER, kPlain>(a, grid, flags, 0, s);
     if ((flags & KVP_LAUNCH_LDS) && a.chunk_bytes <= kMaxLdsChunk)
-        return launch_unroll<HOST, GATHER, kConvertLds>(a, grid, flags, a.chunk_bytes, s);
-    return launch_unroll<HOST, GATHER, kConvert>(a, grid, flags, 0, s);
+        return launch_unroll<CLS, GATHER, kConvertLds>(a, grid, flags, a.chunk_bytes, s);
+    return launch_unroll<CLS, GATHER, kConvert>(a, grid, flags, 0, s);
 }
 
 hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
@@ -338,8 +347,12 @@ hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, ui
     // the XCD renumbering is a permutation of [0, grid) only for multiples of 8
     a.xcd_remap = (flags & KVP_LAUNCH_XCD) && grid % kXcds == 0 ? 1u : 0u;
     if (cls == KVP_CLASS_HOST)
-        return gather ? launch_dir<true, true>(a, grid, flags, s) : launch_dir<true, false>(a, grid, flags, s);
-    return gather ? launch_dir<false, true>(a, grid, flags, s) : launch_dir<false, false>(a, grid, flags, s);
+        return gather ? launch_dir<KVP_CLASS_HOST, true>(a, grid, flags, s)
+                      : launch_dir<KVP_CLASS_HOST, false>(a, grid, flags, s);
+    if (cls == KVP_CLASS_STAGING)
+        return gather ? launch_dir<KVP_CLASS_STAGING, true>(a, grid, flags, s)
+                      : launch_dir<KVP_CLASS_STAGING, false>(a, grid, flags, s);
+    return gather ? launch_dir<kClassRing, true>(a, grid, flags, s) : launch_dir<kClassRing, false>(a, grid, flags, s);
 }
 
 hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid, uint32_t flags,

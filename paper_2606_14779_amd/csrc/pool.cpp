@@ -757,7 +757,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             CopyArgs a = args[KVP_CLASS_HOST];
             a.items = dev_list + bt.first;
             a.n_items = bt.n;
-            check_hip(launch_chunk_copy(a, KVP_CLASS_STAGING, gather, lc.grid, lc.flags, s), "kernel launch");
+            check_hip(launch_chunk_copy(a, kClassRing, gather, lc.grid, lc.flags, s), "kernel launch");
         };
         if (gather) {
             check_hip(hipStreamWaitEvent(sc, p.fork, 0), "hipStreamWaitEvent");
