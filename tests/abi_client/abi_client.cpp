@@ -1,7 +1,9 @@
 // A plain C++ client of libkvpool.so: no Python, no PyTorch.  Creates a pool
 // of one host and one HBM staging region, places a request, stores a source
 // cache filled with a per-element tag, retrieves it into a destination cache
-// under a permuted block table, and checks every element on the host.
+// under a permuted block table, and checks every element on the host.  Then
+// it retrieves again through the copy-engine transport with one-block ring
+// slots, in two layer ranges, and checks again.
 // Built by the package build step; run by tests/test_abi_client.py (GPU).
 #include <hip/hip_runtime.h>
 
@@ -76,16 +78,29 @@ int main()
     std::vector<char> used(slots, 0);
     for (uint32_t b = 0; b < n; ++b) used[dst_table[b]] = 1;
     uint64_t bad = 0;
-    for (uint32_t i = 0; i < 2 * L; ++i) {
-        HIPTRY(hipMemcpy(got.data(), dst[i], layer_bytes, hipMemcpyDeviceToHost));
-        for (uint64_t e = 0; e < want.size(); ++e) want[e] = uint16_t(e * 2654435761u + i * 40503u);
-        for (uint32_t b = 0; b < n; ++b)
-            bad += std::memcmp(&got[dst_table[b] * chunk_elems], &want[src_table[b] * chunk_elems],
-                               chunk_elems * 2) != 0;
-        for (uint32_t sl = 0; sl < slots; ++sl)
-            if (!used[sl])
-                for (uint64_t e = 0; e < chunk_elems; ++e) bad += got[sl * chunk_elems + e] != 0xA5A5;
-    }
+    auto check = [&]() -> int {
+        for (uint32_t i = 0; i < 2 * L; ++i) {
+            HIPTRY(hipMemcpy(got.data(), dst[i], layer_bytes, hipMemcpyDeviceToHost));
+            for (uint64_t e = 0; e < want.size(); ++e) want[e] = uint16_t(e * 2654435761u + i * 40503u);
+            for (uint32_t b = 0; b < n; ++b)
+                bad += std::memcmp(&got[dst_table[b] * chunk_elems], &want[src_table[b] * chunk_elems],
+                                   chunk_elems * 2) != 0;
+            for (uint32_t sl = 0; sl < slots; ++sl)
+                if (!used[sl])
+                    for (uint64_t e = 0; e < chunk_elems; ++e) bad += got[sl * chunk_elems + e] != 0xA5A5;
+        }
+        return 0;
+    };
+    if (check()) return 1;
+
+    // the same request through the copy engines: ring slots of one block, two layer ranges
+    for (uint32_t i = 0; i < 2 * L; ++i) HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
+    TRY(kv_pool_set_copy_ring(pool, 64 << 10));
+    TRY(kv_pool_set_launch(pool, KVP_CLASS_HOST, KVP_OP_RETRIEVE, 0, KVP_LAUNCH_SDMA));
+    TRY(kv_pool_retrieve_layers(pool, map.data(), n, dst_table.data(), slots, 0, 1, k_dst.data(), v_dst.data(), stream));
+    TRY(kv_pool_retrieve_layers(pool, map.data(), n, dst_table.data(), slots, 1, L, k_dst.data(), v_dst.data(), stream));
+    HIPTRY(hipStreamSynchronize(stream));
+    if (check()) return 1;
     TRY(kv_pool_release(pool, 42));
     kv_pool_destroy(pool);
     HIPTRY(hipStreamDestroy(stream));
@@ -95,6 +110,6 @@ int main()
         std::fprintf(stderr, "abi client: %llu mismatching chunks or elements\n", (unsigned long long)bad);
         return 1;
     }
-    std::printf("abi client: %u blocks stored and retrieved exactly\n", n);
+    std::printf("abi client: %u blocks stored and retrieved exactly (zero-copy kernel, then copy engines)\n", n);
     return 0;
 }
