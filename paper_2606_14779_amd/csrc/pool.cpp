@@ -592,6 +592,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     DeviceScope dev(p.device);
     const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
     const bool sdma = (p.launch[KVP_CLASS_HOST][op].flags & KVP_LAUNCH_SDMA) != 0;
+    if (sdma && !p.bounce)   // only after a kv_pool_set_copy_ring that could not allocate
+        fail(KVP_ERR_NOMEM, "copy-engine ring not allocated: set a smaller ring or clear KVP_LAUNCH_SDMA");
 
     // GLT-resolved locations, grouped by region class (Sec. 4.3)
     std::vector<CopyItem> items[2];
