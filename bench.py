@@ -278,6 +278,8 @@ def pipeline(args):
         if args.copy_ring_mib:
             run.pool.set_copy_ring(args.copy_ring_mib << 20)
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+    if args.staging_grid or args.staging_flags:   # also the ring kernel's shape with --sdma
+        run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
     run.setup()
     q = wl.requests[0]
     kp, vp = run.layer_ptrs(run.dst)
@@ -332,6 +334,7 @@ def pipeline(args):
     print(json.dumps({"metric": "blocked I/O time with layerwise pipelining (stand-in compute)",
                       "workload": wl.name, "layers": sh.layers, "retrieve_only_ms": round(retrieve_only, 2),
                       "host_transport": "copy engines" if args.sdma else "zero-copy kernel",
+                      "staging_launch": {"grid": args.staging_grid or None, "flags": args.staging_flags},
                       "gemm_8192_ms": round(one, 3), "rows": rows}), flush=True)
     run.close()
 
