@@ -339,6 +339,55 @@ def pipeline(args):
     run.close()
 
 
+def latency(args):
+    """Call-to-complete time of small retrieves: the first n blocks of the request (striped over all
+    regions) for n = 1 ... 1024, one call at a time with a host synchronisation after each.  This is
+    the fixed cost per call that a fetch of a few blocks sees."""
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    wl = workloads.make(args.config)
+    run = WorkloadRun(wl, device=0)
+    if args.sdma:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+    run.setup()
+    q = wl.requests[0]
+    kp, vp = run.layer_ptrs(run.dst)
+    m = run.retrieve_maps[q.request_id]
+    cur = torch.cuda.current_stream()
+    bb = wl.shape.block_bytes
+    rows = []
+    for n in (1, 4, 16, 64, 256, 1024):
+        sub, table = m[:n].copy(), q.dst_slots[:n].copy()
+        for _ in range(3):
+            run.pool.retrieve(sub, table, wl.dst_num_slots, kp, vp, cur.cuda_stream)
+        torch.cuda.synchronize()
+        wall, span, enq = [], [], []
+        for _ in range(20):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t = time.perf_counter()
+            s.record(cur)
+            run.pool.retrieve(sub, table, wl.dst_num_slots, kp, vp, cur.cuda_stream)
+            te = time.perf_counter()
+            e.record(cur)
+            e.synchronize()
+            wall.append((time.perf_counter() - t) * 1e6)
+            enq.append((te - t) * 1e6)
+            span.append(s.elapsed_time(e) * 1e3)
+        w = statistics.median(wall)
+        rows.append({"blocks": n, "bytes": n * bb, "call_to_complete_us": round(w, 1),
+                     "enqueue_us": round(statistics.median(enq), 1),
+                     "span_us": round(statistics.median(span), 1), "gbps": round(n * bb / w / 1e3, 2)})
+        log(json.dumps(rows[-1]))
+    print(json.dumps({"metric": "retrieve latency by request size (first n blocks, call to complete)",
+                      "workload": wl.name, "host_transport": "copy engines" if args.sdma else "zero-copy kernel",
+                      "rows": rows}), flush=True)
+    run.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -358,6 +407,8 @@ def main():
                     help="retrieve the host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
     ap.add_argument("--no-copy-engine", action="store_true", help="skip the copy-engine retrieve figure")
+    ap.add_argument("--latency", action="store_true",
+                    help="instead of the bench line, time single retrieves of the first 1 ... 1024 blocks")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 1 GiB before each timed step; ms_per_step is then the median event span")
     ap.add_argument("--pipeline", action="store_true",
@@ -372,6 +423,9 @@ def main():
         return
     if args.gpus == 1 and args.pipeline:
         pipeline(args)
+        return
+    if args.gpus == 1 and args.latency:
+        latency(args)
         return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "

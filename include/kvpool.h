@@ -169,7 +169,9 @@ int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
  * Retrieve (Sec. 4.3, "KV Retrieval"): group the present entries by region
  * type, then read the host regions (zero-copy kernel, on `stream`) and the
  * staging regions (HBM gather kernel, on the pool's internal stream forked
- * from `stream` and joined back into it) in parallel; every chunk lands in slot
+ * from `stream` and joined back into it) in parallel -- a call with under
+ * 32 MiB of staging-region bytes runs its HBM kernel on `stream` ahead of the
+ * host-region kernel instead, since forking costs more; every chunk lands in slot
  * dst_block_table[b] of layer l's K or V buffer in the engine layout.
  * Absent entries are skipped and every slot not named by a present entry is
  * left untouched.

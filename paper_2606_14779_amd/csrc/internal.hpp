@@ -154,6 +154,7 @@ struct Pool {
     // next one (any stream) waits for it, so calls take the link in turn
     hipEvent_t link_done[2] = {nullptr, nullptr};
     bool link_rec[2] = {false, false};
+    hipStream_t link_stream[2] = {nullptr, nullptr};   // stream of that kernel (same stream: no wait)
     std::vector<Slot> ring;
     uint32_t ring_next = 0;
     LaunchCfg launch[2][2];      // [class][op]

@@ -45,6 +45,11 @@ constexpr uint64_t kSector = 4096;
 constexpr uint32_t kRingSlots = 32;
 constexpr size_t kSlotMin = 64 * 1024;
 constexpr uint64_t kCreateProbeBytes = 256ull << 20;   // per-region read probe when no bandwidths are given
+// Staging-class bytes below which the HBM kernel runs on the caller's stream
+// ahead of the host-class kernel instead of being forked: forking costs about
+// 25 us of host time per call, more than such a kernel takes (32 MiB read and
+// written at ~2.5 TB/s copied: ~13 us).
+constexpr uint64_t kForkMinBytes = 32ull << 20;
 
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -676,8 +681,10 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (!gather && rec->busy_rec) check_hip(hipStreamWaitEvent(s, rec->busy, 0), "hipStreamWaitEvent");
     }
     check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
-    check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
     slot.pending = true;  // from here on the slot is in use even if a launch fails
+    // the internal stream takes work only for enough staging bytes or for ring batches
+    const bool fork_staging = batches.empty() && items[KVP_CLASS_STAGING].size() * width >= kForkMinBytes;
+    if (fork_staging || !batches.empty()) check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
 
     const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
     // Staging class forked onto the internal stream first, then the host
@@ -715,20 +722,24 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     };
     const bool staging = !items[KVP_CLASS_STAGING].empty();
     if (batches.empty()) {
-        if (staging) {
+        if (fork_staging) {
             check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
             launch(KVP_CLASS_STAGING, p.s_stage);
             check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
+        } else if (staging) {
+            launch(KVP_CLASS_STAGING, s);   // small: in order on the caller's stream
         }
         if (!items[KVP_CLASS_HOST].empty()) {
             // one host-class kernel on the link at a time, in enqueue order:
             // two of them would only share its bandwidth and both end late
-            if (p.link_rec[op]) check_hip(hipStreamWaitEvent(s, p.link_done[op], 0), "hipStreamWaitEvent");
+            if (p.link_rec[op] && p.link_stream[op] != s)
+                check_hip(hipStreamWaitEvent(s, p.link_done[op], 0), "hipStreamWaitEvent");
             launch(KVP_CLASS_HOST, s);
             check_hip(hipEventRecord(p.link_done[op], s), "hipEventRecord");
             p.link_rec[op] = true;
+            p.link_stream[op] = s;
         }
-        if (staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
+        if (fork_staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     } else {
         // Copy-engine transport: the host-link copies take the internal
         // stream (no stream beyond the kernel path's two) and every kernel

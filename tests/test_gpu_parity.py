@@ -381,13 +381,19 @@ def test_measured_bandwidths_drive_placement():
         assert np.array_equal(p.place(1, 300), ora.place(1, 300))
 
 
-def test_concurrent_retrieves_from_threads():
-    """store/retrieve may be called from several threads on different streams."""
+@pytest.mark.parametrize("sdma", [False, True])
+def test_concurrent_retrieves_from_threads(sdma):
+    """store/retrieve may be called from several threads on different streams
+    (with the copy-engine option, all of them share the pool's ring)."""
     import threading
     wl = workloads.make(5, max_blocks=80)
-    say("case threads")
+    say("case threads", "copy engines" if sdma else "kernel")
     run = make_run(wl)
     try:
+        if sdma:
+            run.pool.set_copy_ring(32 << 20)          # a few 1.5 MiB blocks a slot: many slot reuses
+            for op in (K.OP_RETRIEVE, K.OP_STORE):
+                run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
         host = run.setup(keep_host=True)
         streams = [torch.cuda.Stream() for _ in wl.requests]
         cur = torch.cuda.current_stream()
