@@ -351,7 +351,8 @@ typedef struct {
 /* Enable (1) or disable (0) HIP-event timing of the kernels store/retrieve
  * launch; either way the recorded history is cleared.  Timing events are
  * recorded on the stream each kernel runs on (the caller's stream for the
- * host class, the pool's internal stream for the staging class; with
+ * host class, the pool's internal stream for the staging class unless the
+ * call's staging bytes are few enough to run it on the caller's; with
  * KVP_LAUNCH_SDMA both classes time on the caller's stream, except a
  * retrieve's host-class start, recorded before its first copy).
  * Errors: INVALID. */
