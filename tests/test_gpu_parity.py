@@ -256,6 +256,51 @@ def test_store_then_retrieve_across_streams():
         run.close()
 
 
+@pytest.mark.parametrize("sdma", [False, True])
+def test_store_waits_for_retrieve_on_other_stream(sdma):
+    """Write after read across streams: a store of new values into a request's
+    blocks, enqueued on another stream right after a retrieve of the old ones,
+    must wait for it; a retrieve after that store sees the new values."""
+    wl = workloads.make(1, max_blocks=100)                 # 200 MiB over the host link: ~4 ms each way
+    say("case store-after-retrieve", "copy engines" if sdma else "kernel")
+    run = make_run(wl)
+    try:
+        if sdma:
+            run.pool.set_copy_ring(64 << 20)
+            for op in (K.OP_RETRIEVE, K.OP_STORE):
+                run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
+        run.fill_source()
+        run.place_all()
+        q = wl.requests[0]
+        n = q.n_present
+        kp_src, vp_src = run.layer_ptrs(run.src)
+        kp_dst, vp_dst = run.layer_ptrs(run.dst)
+        src_slots = torch.from_numpy(q.src_slots.astype(np.int64)).cuda()
+        v1 = run.src[:, :, src_slots].clone()
+        v2 = v1 ^ 0x5A5A                                      # different values, same shape
+        a, b, c = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+        torch.cuda.synchronize()
+        m = run.maps[q.request_id]
+        d1 = np.arange(n, dtype=np.int32)                     # two disjoint destination ranges
+        d2 = np.arange(n, 2 * n, dtype=np.int32)
+        dst = torch.full((wl.shape.layers, 2, 2 * n) + tuple(run.dst.shape[3:]), 0, dtype=torch.int16,
+                         device="cuda")
+        kp2 = [dst[l, 0].data_ptr() for l in range(wl.shape.layers)]
+        vp2 = [dst[l, 1].data_ptr() for l in range(wl.shape.layers)]
+        run.pool.store(m, q.src_slots, wl.src_num_slots, kp_src, vp_src, a.cuda_stream)
+        run.pool.retrieve(m, d1, 2 * n, kp2, vp2, b.cuda_stream)
+        with torch.cuda.stream(c):                            # new source values, then the store on c
+            c.wait_stream(a)                                  # (the source buffer itself is the caller's)
+            run.src[:, :, src_slots] = v2
+        run.pool.store(m, q.src_slots, wl.src_num_slots, kp_src, vp_src, c.cuda_stream)
+        run.pool.retrieve(m, d2, 2 * n, kp2, vp2, a.cuda_stream)
+        torch.cuda.synchronize()
+        assert torch.equal(dst[:, :, :n], v1), "the retrieve saw values stored after it"
+        assert torch.equal(dst[:, :, n:], v2), "the later retrieve missed the later store"
+    finally:
+        run.close()
+
+
 def test_timing_reports_both_classes():
     wl = workloads.make(2, max_blocks=64)
     run = make_run(wl)
