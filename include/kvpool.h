@@ -296,6 +296,9 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
 #define KVP_LAUNCH_XCD      16u  /* renumber workgroups so that each of the 8 XCDs takes
                                     contiguous units (grids that are multiples of 8) */
 #define KVP_LAUNCH_SDMA     32u  /* host class only: copy-engine transport (below) */
+#define KVP_LAUNCH_CHUNK_MAJOR 64u /* order units chunk by chunk over all blocks (the units in
+                                    flight then write neighbouring slots of one layer buffer)
+                                    instead of block by block */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host

@@ -191,6 +191,7 @@ struct CopyArgs {
     uint32_t chunk0;           // first chunk: 2 * first layer
     uint32_t parts;            // units per chunk (1, or 2 with KVP_LAUNCH_SPLIT2 on plain chunks)
     uint32_t xcd_remap;        // 1: renumber workgroups so each XCD takes contiguous units
+    uint32_t chunk_major;      // 1: units ordered chunk, item, part (else item, chunk, part)
     uint64_t chunk_bytes;      // C, multiple of 16
     uint32_t heads;            // token-major conversion: H
     uint32_t tokens;           //   bs

@@ -201,17 +201,29 @@ struct Unit {
 };
 
 // Unit u of a launch: item u / (chunks * parts), then chunk, then part of
-// the chunk (parts > 1 only for plain chunks).
+// the chunk (parts > 1 only for plain chunks); or, chunk-major, chunk
+// u / (items * parts), then item, then part, so that the units in flight
+// write neighbouring slots of one per-layer buffer.
 __device__ __forceinline__ Unit unit_at(const CopyArgs &a, uint32_t u)
 {
     citem_t *items = (citem_t *)a.items;
     cptr_t *table = (cptr_t *)a.cache;
-    const uint32_t per_item = a.chunks * a.parts;
-    const uint32_t item = u / per_item;
-    const uint32_t r = u - item * per_item;
-    const uint32_t k = r / a.parts;
+    uint32_t item, k, p;
+    if (a.chunk_major) {
+        const uint32_t per_chunk = a.n_items * a.parts;
+        k = u / per_chunk;
+        const uint32_t r = u - k * per_chunk;
+        item = r / a.parts;
+        p = r - item * a.parts;
+    } else {
+        const uint32_t per_item = a.chunks * a.parts;
+        item = u / per_item;
+        const uint32_t r = u - item * per_item;
+        k = r / a.parts;
+        p = r - k * a.parts;
+    }
     const uint32_t c = a.chunk0 + k;
-    const uint64_t part = static_cast<uint64_t>(r - k * a.parts) * (a.chunk_bytes / a.parts);
+    const uint64_t part = static_cast<uint64_t>(p) * (a.chunk_bytes / a.parts);
     const uint64_t pool = items[item].pool;
     const uint64_t slot = items[item].slot;
     return Unit{pool + static_cast<uint64_t>(c) * a.chunk_bytes + part, table[c] + slot * a.chunk_bytes + part};
@@ -346,6 +358,7 @@ hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, ui
     if (grid == 0) grid = 1;
     // the XCD renumbering is a permutation of [0, grid) only for multiples of 8
     a.xcd_remap = (flags & KVP_LAUNCH_XCD) && grid % kXcds == 0 ? 1u : 0u;
+    a.chunk_major = (flags & KVP_LAUNCH_CHUNK_MAJOR) ? 1u : 0u;
     if (cls == KVP_CLASS_HOST)
         return gather ? launch_dir<KVP_CLASS_HOST, true>(a, grid, flags, s)
                       : launch_dir<KVP_CLASS_HOST, false>(a, grid, flags, s);

@@ -42,6 +42,9 @@ def _case(seed):
     grid = [int(rng.choice([1, 3, 12, 64, 8192])) for _ in range(4)]
     flags = [int(rng.choice([0, K.LAUNCH_NT_LOAD, K.LAUNCH_NT_STORE, K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE]))
              | (K.LAUNCH_LDS if layout == 1 and rng.random() < 0.5 else 0) for _ in range(4)]
+    # unit order drawn from a generator of its own, so the draws above stay as they were
+    order = np.random.default_rng(seed + 7919)
+    flags = [f | (K.LAUNCH_CHUNK_MAJOR if order.random() < 0.4 else 0) for f in flags]
     return rng, layout, (L, H, bs, D), kinds, weights, n, grid, flags
 
 

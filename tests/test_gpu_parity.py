@@ -48,7 +48,9 @@ def test_parity_scaled_workloads(cfg, layout):
 @pytest.mark.parametrize("grid,flags", [(1, 0), (7, K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE),
                                         (4096, K.LAUNCH_NT_LOAD), (300, K.LAUNCH_NT_STORE),
                                         (64, K.LAUNCH_XCD), (96, K.LAUNCH_XCD | K.LAUNCH_SPLIT2),
-                                        (12, K.LAUNCH_XCD), (65536, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD)])
+                                        (12, K.LAUNCH_XCD), (65536, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD),
+                                        (7, K.LAUNCH_CHUNK_MAJOR), (65536, K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_SPLIT2),
+                                        (96, K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_XCD | K.LAUNCH_SPLIT2)])
 def test_parity_launch_shapes(grid, flags):
     wl = workloads.make(2, max_blocks=45)
     say("case launch", grid, flags)
@@ -65,7 +67,8 @@ def test_parity_launch_shapes(grid, flags):
         run.close()
 
 
-@pytest.mark.parametrize("flags", [0, K.LAUNCH_LDS, K.LAUNCH_LDS | K.LAUNCH_NT_LOAD])
+@pytest.mark.parametrize("flags", [0, K.LAUNCH_LDS, K.LAUNCH_LDS | K.LAUNCH_NT_LOAD,
+                                   K.LAUNCH_LDS | K.LAUNCH_CHUNK_MAJOR, K.LAUNCH_CHUNK_MAJOR])
 def test_parity_token_major_lds(flags):
     wl = workloads.make(4, max_blocks=33, layout=1)
     say("case token-major", flags)
