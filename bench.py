@@ -388,6 +388,75 @@ def latency(args):
     run.close()
 
 
+def duplex(args):
+    """The host link is full duplex: store (offload) one 128K LLaMA-shaped request while another is
+    retrieved, on two streams, against each alone.  Two requests are placed in one pool with the
+    128K workload's regions and weights (4:4:1:1:1:1), each with its own source and destination slots."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    base = workloads.make(3)
+    sh = base.shape
+    n = base.requests[0].n_present
+    regions = [dataclasses.replace(r) for r in base.regions]
+    workloads._size_regions(regions, [n, n], sh.block_bytes)
+    reqs = [workloads.RequestSpec(i + 1, n, n, np.arange(i * n, (i + 1) * n, dtype=np.int32),
+                                  np.arange(i * n, (i + 1) * n, dtype=np.int32)) for i in range(2)]
+    wl = workloads.Workload(3, base.name + "-x2", base.seed, sh, 0, regions, reqs, 2 * n, 2 * n)
+    run = WorkloadRun(wl, device=0)
+    if args.host_grid or args.host_flags:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
+    if args.store_grid:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, args.store_grid, K.LAUNCH_NT_STORE)
+    if args.sdma:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+    run.setup()
+    kp_s, vp_s = run.layer_ptrs(run.src)
+    kp_d, vp_d = run.layer_ptrs(run.dst)
+    q1, q2 = wl.requests
+    a, b = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def store(st):
+        run.pool.store(run.maps[q1.request_id], q1.src_slots, wl.src_num_slots, kp_s, vp_s, st.cuda_stream)
+
+    def retrieve(st):
+        run.pool.retrieve_request(q2.request_id, q2.dst_slots, wl.dst_num_slots, kp_d, vp_d, st.cuda_stream)
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / reps * 1e3
+
+    reps = max(3, args.steps // 2)
+    st_ms = timed(lambda: store(a), reps)
+    rt_ms = timed(lambda: retrieve(b), reps)
+    both_ms = timed(lambda: (store(a), retrieve(b)), reps)
+    host_bytes = sum(int(np.isin(run.maps[q.request_id]["region"],
+                                 [i for i, r in enumerate(wl.regions) if r.kind == "host"]).sum())
+                     for q in (q1,)) * sh.block_bytes
+    out = {"metric": "store and retrieve of two 128K-token requests at once (host link full duplex)",
+           "workload": wl.name, "request_bytes": wl.requests[0].n_present * sh.block_bytes,
+           "host_link_bytes_each_way": host_bytes,
+           "store_alone_ms": round(st_ms, 2), "retrieve_alone_ms": round(rt_ms, 2),
+           "both_ms": round(both_ms, 2), "serial_ms": round(st_ms + rt_ms, 2),
+           "link_gbps_both_directions": round(2 * host_bytes / both_ms / 1e6, 2),
+           "launch": {"retrieve": "copy engines" if args.sdma else {"grid": args.host_grid or 12},
+                      "store_grid": args.store_grid or 12}}
+    print(json.dumps(out), flush=True)
+    run.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -400,6 +469,7 @@ def main():
     ap.add_argument("--host-grid", type=int, default=0)
     ap.add_argument("--staging-grid", type=int, default=0)
     ap.add_argument("--host-flags", type=int, default=0)
+    ap.add_argument("--store-grid", type=int, default=0, help="host-class store workgroups (0: library default)")
     ap.add_argument("--staging-flags", type=int, default=0)
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
@@ -407,6 +477,8 @@ def main():
                     help="retrieve the host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
     ap.add_argument("--no-copy-engine", action="store_true", help="skip the copy-engine retrieve figure")
+    ap.add_argument("--duplex", action="store_true",
+                    help="instead of the bench line, store one request while retrieving another")
     ap.add_argument("--latency", action="store_true",
                     help="instead of the bench line, time single retrieves of the first 1 ... 1024 blocks")
     ap.add_argument("--flush", action="store_true",
@@ -426,6 +498,9 @@ def main():
         return
     if args.gpus == 1 and args.latency:
         latency(args)
+        return
+    if args.gpus == 1 and args.duplex:
+        duplex(args)
         return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "
