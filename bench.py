@@ -204,8 +204,9 @@ def ablation(args):
     """Retrieval of the same request through differently organised pools (the
     paper's ablation of its orchestrator, Sec. 5.3, restated for this path):
     everything on one host region; striped over the two host regions only;
-    the configured 4:4:1:1:1:1 striping; and weights measured by the pool
-    organizer (per-region read probes, host regions sharing one link)."""
+    all six regions with equal weights; the configured 4:4:1:1:1:1 striping;
+    and weights measured by the pool organizer (per-region read probes, host
+    regions sharing one link)."""
     import copy
 
     import torch
@@ -250,6 +251,8 @@ def ablation(args):
     res = []
     res.append(variant("single host region", [R("host", 1, 0)])[0])
     res.append(variant("two host regions 1:1", [R("host", 1, 0), R("host", 1, 1)])[0])
+    res.append(variant("same regions, equal weights (striping without Eq. 1)",
+                       [R(r.kind, 1, r.numa) for r in base.regions])[0])
     conf, measured = variant("configured 4:4:1:1:1:1", copy.deepcopy(base.regions))
     res.append(conf)
     mregions = [R(r.kind, int(w), r.numa) for r, w in zip(base.regions, measured)]
