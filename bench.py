@@ -480,6 +480,8 @@ def main():
                     help="retrieve the host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
     ap.add_argument("--no-copy-engine", action="store_true", help="skip the copy-engine retrieve figure")
+    ap.add_argument("--batch", action="store_true",
+                    help="retrieve all requests of the workload in one call (concatenated maps) per step")
     ap.add_argument("--duplex", action="store_true",
                     help="instead of the bench line, store one request while retrieving another")
     ap.add_argument("--latency", action="store_true",
@@ -557,8 +559,9 @@ def main():
 
     cur = torch.cuda.current_stream()
     run.pool.set_timing(False)
+    step = run.retrieve_batch if args.batch else run.retrieve_all
     for _ in range(args.warmup):
-        run.retrieve_all()
+        step()
     torch.cuda.synchronize()
 
     # timed region: K retrieves back to back; the library records HIP events
@@ -577,7 +580,7 @@ def main():
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s.record(cur)
         tq = time.perf_counter()
-        run.retrieve_all()
+        step()
         enqueue_ms.append((time.perf_counter() - tq) * 1e3)
         e.record(cur)
         spans.append((s, e))
@@ -759,6 +762,7 @@ def main():
         "store_kernels_ms": store_t,
         "cpu_baseline": cpu,
         "caches_flushed_per_step": bool(args.flush),
+        "requests_per_call": len(wl.requests) if args.batch else 1,
         "launch": {"host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                    "host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,
                    "host_flags": args.host_flags, "staging_flags": args.staging_flags,

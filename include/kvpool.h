@@ -174,7 +174,8 @@ int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
  * host-region kernel instead, since forking costs more; every chunk lands in slot
  * dst_block_table[b] of layer l's K or V buffer in the engine layout.
  * Absent entries are skipped and every slot not named by a present entry is
- * left untouched.
+ * left untouched.  Entries may belong to several requests: a batch retrieved
+ * by one call shares one work list and one kernel per region class.
  *   map[n_blocks], dst_block_table[n_blocks]   host arrays; destination slots
  *                        of present entries must be distinct and lie in
  *                        [0, dst_num_slots).

@@ -102,6 +102,18 @@ class WorkloadRun:
             self.pool.retrieve(self.retrieve_maps[q.request_id], q.dst_slots, self.wl.dst_num_slots, kp, vp,
                                s.cuda_stream)
 
+    def retrieve_batch(self, stream=None):
+        """Every request in one kv_pool_retrieve call: the maps (absent tails included) and the
+        destination tables concatenated."""
+        kp, vp = self.layer_ptrs(self.dst)
+        s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
+        if not hasattr(self, "_batch"):
+            m = np.concatenate([self.retrieve_maps[q.request_id] for q in self.wl.requests])
+            t = np.concatenate([q.dst_slots for q in self.wl.requests]).astype(np.int32)
+            self._batch = (m, t)
+        m, t = self._batch
+        self.pool.retrieve(m, t, self.wl.dst_num_slots, kp, vp, s.cuda_stream)
+
     def retrieve_all(self):
         """One retrieve per request; request i on stream i % n_streams (forked from the current stream)."""
         torch = self.torch

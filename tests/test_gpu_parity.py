@@ -260,6 +260,23 @@ def test_store_then_retrieve_across_streams():
 
 
 @pytest.mark.parametrize("sdma", [False, True])
+def test_batch_of_requests_in_one_call(sdma):
+    """The four requests of workload 5 (absent tails included) retrieved by one call."""
+    wl = workloads.make(5, max_blocks=70)
+    say("case batch in one call", "copy engines" if sdma else "kernel")
+    run = make_run(wl)
+    try:
+        if sdma:
+            run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+        host = run.setup(keep_host=True)
+        run.retrieve_batch()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("sdma", [False, True])
 def test_store_waits_for_retrieve_on_other_stream(sdma):
     """Write after read across streams: a store of new values into a request's
     blocks, enqueued on another stream right after a retrieve of the old ones,
