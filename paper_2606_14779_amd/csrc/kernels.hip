@@ -15,9 +15,17 @@
 // so neighbouring workgroups read neighbouring pieces of the same pool block
 // (the pool side streams through memory in address order).  There is no data
 // reuse; an optional renumbering that gives each of the 8 XCDs contiguous
-// units (KVP_LAUNCH_XCD) measured no better than the round-robin default.
+// units (KVP_LAUNCH_XCD) measured no better than the round-robin default, and
+// so did the optional chunk-major order (KVP_LAUNCH_CHUNK_MAJOR), in which the
+// units in flight write neighbouring slots of one per-layer engine buffer.
 // The work list and the engine pointer table are read with scalar loads, and
 // the next unit's entries are fetched while the current unit is copied.
+//
+// Three entry points share the body, so that traces and counters tell them
+// apart: host_region_copy (zero-copy reads or writes of pinned host regions
+// over the host link), staging_region_copy (HBM staging regions) and
+// ring_slot_copy (a copy-engine ring slot in HBM, whose host-link leg is a
+// hipMemcpy).
 //
 // Three copy forms:
 //   - head-major pool chunks: the chunk is [H][bs][D] on both sides; a plain
