@@ -46,6 +46,7 @@ class WorkloadRun:
         self._ptrs = {}           # id(cache) -> (K pointers, V pointers), computed once
         self.maps = {}            # request_id -> placed map (present prefix)
         self.retrieve_maps = {}   # request_id -> map of the whole context (absent tail)
+        self._batch = None        # concatenated maps and tables of all requests (retrieve_batch)
         # one caller stream per concurrent request; a single-stream workload uses the current stream
         self.streams = [torch.cuda.Stream(device=dev) for _ in range(wl.n_streams)] if wl.n_streams > 1 else []
 
@@ -77,6 +78,7 @@ class WorkloadRun:
         self.dst.fill_(np.int16(np.uint16(value).view(np.int16)).item())
 
     def place_all(self):
+        self._batch = None
         for q in self.wl.requests:
             m = self.pool.place(q.request_id, q.n_present)
             self.maps[q.request_id] = m
@@ -107,7 +109,7 @@ class WorkloadRun:
         destination tables concatenated."""
         kp, vp = self.layer_ptrs(self.dst)
         s = stream if stream is not None else self.torch.cuda.current_stream(self.device)
-        if not hasattr(self, "_batch"):
+        if self._batch is None:
             m = np.concatenate([self.retrieve_maps[q.request_id] for q in self.wl.requests])
             t = np.concatenate([q.dst_slots for q in self.wl.requests]).astype(np.int32)
             self._batch = (m, t)
