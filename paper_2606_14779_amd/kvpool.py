@@ -178,7 +178,30 @@ def probe_memcpy(dst: int, src: int, nbytes: int, stream: int = 0):
 
 
 class KVPool:
-    """A pool of regions with bandwidth weights (kv_pool_create ... kv_pool_destroy)."""
+    """A pool of regions with bandwidth weights (kv_pool_create ... kv_pool_destroy).
+
+    Every method is one entry point of include/kvpool.h, which documents its
+    arguments and errors; failures raise KVPoolError with the library's code
+    and message.  A minimal round trip::
+
+        import torch
+        from paper_2606_14779_amd import kvpool as K
+        spec = K.KVSpec(num_layers=32, num_kv_heads=8, head_dim=128)          # 2 MiB blocks
+        pool = K.KVPool([K.Region("host", 8 << 30), K.Region("staging", 2 << 30)], [4, 1], spec, device=0)
+        cache = torch.empty(32, 2, 1024, 8, 16, 128, dtype=torch.bfloat16, device="cuda")
+        k = [cache[l, 0].data_ptr() for l in range(32)]
+        v = [cache[l, 1].data_ptr() for l in range(32)]
+        m = pool.place(7, 100)                                  # Eq. 2 counts, striped map
+        s = torch.cuda.current_stream().cuda_stream
+        pool.store(m, list(range(100)), 1024, k, v, s)          # offload slots 0..99
+        pool.retrieve_request(7, list(range(200, 300)), 1024, k, v, s)   # back into slots 200..299
+        pool.release(7)
+        pool.close()
+
+    Options: set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA) moves the
+    host-link bytes by the copy engines; retrieve_layers / store_layers move a
+    layer range; a map may concatenate several requests (one call per batch).
+    """
 
     def __init__(self, regions, bandwidths, spec: KVSpec, device: int = 0):
         n = len(regions)
