@@ -188,13 +188,15 @@ class KVPool:
         from paper_2606_14779_amd import kvpool as K
         spec = K.KVSpec(num_layers=32, num_kv_heads=8, head_dim=128)          # 2 MiB blocks
         pool = K.KVPool([K.Region("host", 8 << 30), K.Region("staging", 2 << 30)], [4, 1], spec, device=0)
-        cache = torch.empty(32, 2, 1024, 8, 16, 128, dtype=torch.bfloat16, device="cuda")
+        cache = torch.randn(32, 2, 1024, 8, 16, 128, device="cuda").to(torch.bfloat16)
         k = [cache[l, 0].data_ptr() for l in range(32)]
         v = [cache[l, 1].data_ptr() for l in range(32)]
         m = pool.place(7, 100)                                  # Eq. 2 counts, striped map
         s = torch.cuda.current_stream().cuda_stream
         pool.store(m, list(range(100)), 1024, k, v, s)          # offload slots 0..99
         pool.retrieve_request(7, list(range(200, 300)), 1024, k, v, s)   # back into slots 200..299
+        torch.cuda.synchronize()
+        assert torch.equal(cache[:, :, 200:300], cache[:, :, :100])
         pool.release(7)
         pool.close()
 

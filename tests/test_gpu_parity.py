@@ -514,3 +514,12 @@ def test_allocation_failure_reports_nomem_and_cleans_up():
     assert torch.cuda.mem_get_info()[0] >= free_before - (64 << 20)
     with K.KVPool([K.Region("staging", 1 << 30)], [1], spec, 0) as p:
         assert p.region_info(0)["device_ptr"]
+
+
+def test_binding_docstring_example_runs():
+    """The round trip shown in KVPool's docstring runs as printed and checks itself."""
+    import textwrap
+    doc = K.KVPool.__doc__
+    code = doc.split("::", 1)[1].split("\n\n    Options:", 1)[0]
+    exec(compile(textwrap.dedent(code), "KVPool docstring", "exec"), {})
+    torch.cuda.empty_cache()
