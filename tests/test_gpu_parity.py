@@ -523,3 +523,28 @@ def test_binding_docstring_example_runs():
     code = doc.split("::", 1)[1].split("\n\n    Options:", 1)[0]
     exec(compile(textwrap.dedent(code), "KVPool docstring", "exec"), {})
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("sdma", [False, True])
+def test_many_regions(sdma):
+    """40 regions of both types with random weights: per-region bookkeeping, runs and placement at width."""
+    rng = np.random.default_rng(40)
+    regions = [workloads.RegionSpec("host" if i % 2 == 0 else "staging", int(rng.integers(1, 9)),
+                                    0 if i % 2 == 0 else -1) for i in range(40)]
+    shape = workloads.KVShape("many", 4, 2, 64)
+    wl = _custom(shape, regions, 300)
+    say("case many regions", "copy engines" if sdma else "kernel")
+    run = make_run(wl)
+    try:
+        if sdma:
+            run.pool.set_copy_ring(1 << 20)                  # 32 blocks of 32 KiB a slot: many batches
+            for op in (K.OP_RETRIEVE, K.OP_STORE):
+                run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+        counts = np.bincount(run.maps[1]["region"].astype(np.int64), minlength=40)
+        assert (counts > 0).sum() >= 35                      # the stripe reaches nearly every region
+    finally:
+        run.close()
