@@ -480,6 +480,8 @@ def main():
                     help="retrieve the host class through the copy engines and an HBM ring instead of the zero-copy kernel")
     ap.add_argument("--copy-ring-mib", type=int, default=0, help="with --sdma: MiB per ring slot (0: library default)")
     ap.add_argument("--no-copy-engine", action="store_true", help="skip the copy-engine retrieve figure")
+    ap.add_argument("--context", type=int, default=None,
+                    help="workload 3 with this many tokens instead of 128K (e.g. 524288)")
     ap.add_argument("--batch", action="store_true",
                     help="retrieve all requests of the workload in one call (concatenated maps) per step")
     ap.add_argument("--duplex", action="store_true",
@@ -521,7 +523,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    wl = workloads.make(args.config, layout=args.layout)
+    wl = workloads.make(args.config, layout=args.layout, context_tokens=args.context)
     sh = wl.shape
     log("workload", wl.name, "retrieved bytes", wl.retrieved_bytes)
     t = time.perf_counter()

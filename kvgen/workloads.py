@@ -133,13 +133,17 @@ def _scaled(n_full: int, max_blocks):
     return n_full if max_blocks is None else max(1, min(n_full, max_blocks))
 
 
-def make(cfg: int, max_blocks: int | None = None, layout: int = 0, seed: int | None = None) -> Workload:
+def make(cfg: int, max_blocks: int | None = None, layout: int = 0, seed: int | None = None,
+         context_tokens: int | None = None) -> Workload:
     """Build workload ``cfg`` (1..5).
 
     ``max_blocks`` caps the blocks of each request (same shapes, regions,
     weights and table recipes) for parity cases the oracle finishes in
-    seconds; ``None`` gives the full size.
+    seconds; ``None`` gives the full size.  ``context_tokens`` (workload 3
+    only) replaces its 128K-token context, keeping every other recipe.
     """
+    if context_tokens is not None and cfg != 3:
+        raise ValueError("context_tokens applies to workload 3 only")
     seed = 1000 + cfg if seed is None else seed
     if cfg == 1:
         shape = LLAMA_8B
@@ -160,7 +164,8 @@ def make(cfg: int, max_blocks: int | None = None, layout: int = 0, seed: int | N
         wl = Workload(2, "llama3.1-8b-kv-64k-4region", seed, shape, layout, regions, [req], n, n)
     elif cfg == 3:
         shape = LLAMA_8B
-        n = _scaled(131072 // 16, max_blocks)
+        ctx = 131072 if context_tokens is None else int(context_tokens)
+        n = _scaled(ctx // 16, max_blocks)
         regions = [RegionSpec("host", 4, 0), RegionSpec("host", 4, 1)] + \
                   [RegionSpec("staging", 1) for _ in range(4)]
         n_occ = n // 4                      # 8192 blocks -> 10240 slots, 2048 occupied
@@ -169,8 +174,8 @@ def make(cfg: int, max_blocks: int | None = None, layout: int = 0, seed: int | N
         free = np.setdiff1d(np.arange(slots, dtype=np.int32), occ)   # ascending free slots
         src = _rng(seed, "src").permutation(n).astype(np.int32)
         req = RequestSpec(1, n, n, src, free[:n].astype(np.int32))
-        wl = Workload(3, "llama3.1-8b-kv-128k-6region", seed, shape, layout, regions, [req], n,
-                      slots, occupied_dst_slots=occ)
+        name = "llama3.1-8b-kv-128k-6region" if ctx == 131072 else "llama3.1-8b-kv-%dk-6region" % (ctx // 1024)
+        wl = Workload(3, name, seed, shape, layout, regions, [req], n, slots, occupied_dst_slots=occ)
     elif cfg == 4:
         shape = GPT_OSS_20B
         n = _scaled(131072 // 16, max_blocks)
