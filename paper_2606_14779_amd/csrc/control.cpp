@@ -1,0 +1,186 @@
+// Runtime control and introspection of a pool: measured region bandwidths
+// (Sec. 4.1.2, the pool organizer's input to Eq. 1), region information and
+// reads, launch settings of the two kernel classes, the copy-engine ring, and
+// the HIP-event timing of store / retrieve calls.
+
+#include <algorithm>
+#include <cstring>
+
+#include "internal.hpp"
+
+namespace kvp {
+
+// ---------------------------------------------------------------- measured bandwidths (Sec. 4.1.2)
+
+// Read rate of every region (bytes from the region into HBM per second, in
+// MB/s): the region-class kernel's launch shape streams min(probe_bytes,
+// capacity) bytes from the region into a scratch buffer; best of 3 after one
+// warm-up.  Caller holds the pool lock and the device scope.
+void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps)
+{
+    probe_bytes &= ~15ull;
+    void *scratch = nullptr;
+    if (hipMalloc(&scratch, probe_bytes) != hipSuccess || !scratch) {
+        clear_hip_error();
+        fail(KVP_ERR_NOMEM, "probe scratch of " + std::to_string(probe_bytes) + " bytes");
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    try {
+        check_hip(hipEventCreate(&e0), "hipEventCreate");
+        check_hip(hipEventCreate(&e1), "hipEventCreate");
+        uint32_t n_host = 0;
+        for (size_t r = 0; r < p.regions.size(); ++r) {
+            const Region &reg = p.regions[r];
+            const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
+            n_host += cls == KVP_CLASS_HOST;
+            hipStream_t st = p.s_stage;   // one probe at a time
+            const uint64_t n = std::min<uint64_t>(probe_bytes, reg.capacity) & ~15ull;
+            const LaunchCfg &lc = p.launch[cls][KVP_OP_RETRIEVE];
+            float best = 0.f;
+            for (int it = 0; it < 4; ++it) {
+                check_hip(hipEventRecord(e0, st), "hipEventRecord");
+                check_hip(launch_probe_copy(scratch, reg.dev, n, lc.grid, lc.flags & KVP_LAUNCH_NT_LOAD, st),
+                          "probe launch");
+                check_hip(hipEventRecord(e1, st), "hipEventRecord");
+                check_hip(hipEventSynchronize(e1), "hipEventSynchronize");
+                float ms = 0.f;
+                check_hip(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
+                if (it > 0 && (best == 0.f || ms < best)) best = ms;
+            }
+            const double rate = best > 0.f ? static_cast<double>(n) / (best * 1e3) : 1.0;   // MB/s
+            mbps[r] = std::max<uint64_t>(1, static_cast<uint64_t>(rate + 0.5));
+        }
+        // host regions reach the GPU over one shared link: split what one measured alone
+        if ((flags & KVP_MEASURE_SHARED_LINK) && n_host > 1)
+            for (size_t r = 0; r < p.regions.size(); ++r)
+                if (p.regions[r].desc.type == KVP_REGION_HOST) mbps[r] = std::max<uint64_t>(1, mbps[r] / n_host);
+    } catch (...) {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+        (void)hipFree(scratch);
+        throw;
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    (void)hipFree(scratch);
+}
+
+void pool_measure(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_out)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to measure");
+    if (!mbps_out) fail(KVP_ERR_INVALID, "null output");
+    if (flags & ~KVP_MEASURE_SHARED_LINK) fail(KVP_ERR_INVALID, "unknown flags");
+    if (probe_bytes < (1u << 16) || probe_bytes > (1ull << 36)) fail(KVP_ERR_INVALID, "probe_bytes outside [64 KiB, 64 GiB]");
+    std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+    measure_regions(p, probe_bytes, flags, mbps_out);
+}
+
+void pool_set_bandwidths(Pool &p, const uint64_t *bw)
+{
+    if (!bw) fail(KVP_ERR_INVALID, "null bandwidths");
+    for (size_t i = 0; i < p.regions.size(); ++i)
+        if (bw[i] == 0) fail(KVP_ERR_INVALID, "bandwidth of region " + std::to_string(i) + " is 0");
+    std::lock_guard<std::mutex> lock(p.mu);
+    for (size_t i = 0; i < p.regions.size(); ++i) {
+        p.bandwidth[i] = bw[i];
+        p.regions[i].bandwidth = bw[i];
+    }
+}
+
+// ---------------------------------------------------------------- introspection, launch config, timing
+
+void pool_region_info(const Pool &p, uint32_t region, kvp_region_info *out)
+{
+    if (!out) fail(KVP_ERR_INVALID, "null output");
+    if (region >= p.regions.size()) fail(KVP_ERR_INVALID, "region index out of range");
+    const Region &r = p.regions[region];
+    *out = kvp_region_info{r.desc.type, r.desc.numa_node, r.numa_actual, r.flags_used, r.capacity,
+                           r.bandwidth, r.host, r.dev};
+}
+
+void pool_region_read(Pool &p, uint32_t region, uint64_t offset, uint64_t bytes, void *dst)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory");
+    if (region >= p.regions.size()) fail(KVP_ERR_INVALID, "region index out of range");
+    const Region &r = p.regions[region];
+    if (!dst && bytes) fail(KVP_ERR_INVALID, "null destination");
+    if (offset > r.capacity || r.capacity - offset < bytes) fail(KVP_ERR_INVALID, "range outside region");
+    if (!bytes) return;
+    if (r.host) {
+        std::memcpy(dst, static_cast<const char *>(r.host) + offset, bytes);
+    } else {
+        DeviceScope dev(p.device);
+        check_hip(hipMemcpy(dst, static_cast<const char *>(r.dev) + offset, bytes, hipMemcpyDeviceToHost),
+                  "hipMemcpy");
+    }
+}
+
+void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags)
+{
+    if (cls > 1 || op > 1) fail(KVP_ERR_INVALID, "class and op must be 0 or 1");
+    if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS | KVP_LAUNCH_SPLIT2 | KVP_LAUNCH_XCD |
+                  KVP_LAUNCH_SDMA | KVP_LAUNCH_CHUNK_MAJOR))
+        fail(KVP_ERR_INVALID, "unknown flags");
+    if (grid > (1u << 20)) fail(KVP_ERR_INVALID, "grid too large");
+    if ((flags & KVP_LAUNCH_SDMA) && cls != KVP_CLASS_HOST)
+        fail(KVP_ERR_INVALID, "the copy-engine transport is for the host class");
+    if ((flags & KVP_LAUNCH_SDMA) && p.placement_only)
+        fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (flags & KVP_LAUNCH_SDMA) {
+        DeviceScope dev(p.device);
+        ensure_bounce(p);
+    }
+    p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op, p.spec), flags};  // flags taken as given
+}
+
+void pool_set_copy_ring(Pool &p, uint64_t slot_bytes)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
+    if (slot_bytes % kSector || slot_bytes < (64u << 10) || slot_bytes > (1ull << 36))
+        fail(KVP_ERR_INVALID, "slot_bytes must be a multiple of 4096 in [64 KiB, 64 GiB]");
+    std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+    release_bounce(p);
+    p.bounce_slot_request = slot_bytes;
+    if ((p.launch[KVP_CLASS_HOST][KVP_OP_RETRIEVE].flags | p.launch[KVP_CLASS_HOST][KVP_OP_STORE].flags) &
+        KVP_LAUNCH_SDMA)
+        ensure_bounce(p);
+}
+
+void pool_set_timing(Pool &p, int enable)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
+    std::lock_guard<std::mutex> lock(p.mu);
+    DeviceScope dev(p.device);
+    drain_timed(p, nullptr);
+    p.timing = enable != 0;
+}
+
+void pool_last_timing(Pool &p, kvp_timing *out)
+{
+    if (!out) fail(KVP_ERR_INVALID, "null output");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (!p.timing || p.timed.empty()) fail(KVP_ERR_INVALID, "no timed call");
+    DeviceScope dev(p.device);
+    const TimedCall &tc = p.timed.back();
+    float ms[2] = {-1.f, -1.f};
+    for (int c = 0; c < 2; ++c) {
+        if (!tc.ran[c]) continue;
+        check_hip(hipEventSynchronize(tc.t1[c]), "hipEventSynchronize");
+        check_hip(hipEventElapsedTime(&ms[c], tc.t0[c], tc.t1[c]), "hipEventElapsedTime");
+    }
+    *out = kvp_timing{ms[0], ms[1], tc.blocks[0], tc.blocks[1]};
+}
+
+void pool_timing_summary(Pool &p, kvp_timing_summary *out)
+{
+    if (!out) fail(KVP_ERR_INVALID, "null output");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (!p.timing) fail(KVP_ERR_INVALID, "timing is off");
+    DeviceScope dev(p.device);
+    drain_timed(p, out);
+}
+
+}  // namespace kvp

@@ -26,6 +26,30 @@ struct Error {
 void check_hip(hipError_t e, const char *what);   // on failure: clears the last error, throws HIP
 void clear_hip_error();                            // take a failed call's code off the thread
 
+constexpr uint64_t kSector = 4096;   // allocation granule of every region (the LBA-range rule's sector)
+
+inline uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// Make `dev` the calling thread's device for the scope, then restore.
+class DeviceScope {
+public:
+    explicit DeviceScope(int dev)
+    {
+        if (dev < 0) return;
+        check_hip(hipGetDevice(&old_), "hipGetDevice");
+        if (old_ != dev) check_hip(hipSetDevice(dev), "hipSetDevice");
+        else old_ = -1;
+    }
+    ~DeviceScope()
+    {
+        if (old_ >= 0) (void)hipSetDevice(old_);
+    }
+
+private:
+    int old_ = -1;
+};
+
+
 // ---------------------------------------------------------------- placement (Sec. 4.1.2-4.1.3)
 
 // Eq. (2) target counts with the remainder rule.  Throws INVALID on bad input.
@@ -174,6 +198,14 @@ struct Pool {
     std::vector<TimedCall> timed;      // calls recorded since timing was enabled or last summarised
     std::vector<hipEvent_t> spare;     // timing events ready for reuse
 };
+
+// ---------------------------------------------------------------- helpers shared by the pool sources
+
+void free_slot(Slot &s);                                    // pool.cpp: one work-list buffer
+void release_bounce(Pool &p);                               // pool.cpp: copy-engine ring, after its work
+void ensure_bounce(Pool &p);                                // pool.cpp: copy-engine ring on first use
+void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps);   // control.cpp
+void drain_timed(Pool &p, kvp_timing_summary *sum);        // transfer.cpp: wait, summarise, recycle
 
 // ---------------------------------------------------------------- kernels (kernels.hip)
 
