@@ -289,15 +289,26 @@ def pipeline(args):
     m = run.retrieve_maps[q.request_id]
     io = torch.cuda.Stream()
     comp = torch.cuda.Stream()
-    a = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
-    b = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda").contiguous()
+    if args.stand_in == "gemm":          # compute-bound layer stand-in: bf16 8192^3 GEMM
+        a = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+        b = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda").contiguous()
+
+        def work():
+            torch.mm(a, b)
+    else:                                # HBM-bound stand-in (a decode step reading its KV): 1 GiB copy
+        a = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1)
+
+        def work():
+            b.copy_(a)
 
     def gemm_ms(reps):
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         s.record()
         for _ in range(reps):
-            torch.mm(a, b)
+            work()
         e.record()
         e.synchronize()
         return s.elapsed_time(e)
@@ -319,7 +330,7 @@ def pipeline(args):
                     if with_io:
                         comp.wait_event(evs[l])
                     for _ in range(reps):
-                        torch.mm(a, b)
+                        work()
         torch.cuda.synchronize()
         return (time.perf_counter() - t) * 1e3
 
@@ -338,7 +349,8 @@ def pipeline(args):
                       "workload": wl.name, "layers": sh.layers, "retrieve_only_ms": round(retrieve_only, 2),
                       "host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                       "staging_launch": {"grid": args.staging_grid or None, "flags": args.staging_flags},
-                      "gemm_8192_ms": round(one, 3), "rows": rows}), flush=True)
+                      "stand_in": "bf16 GEMM 8192^3" if args.stand_in == "gemm" else "1 GiB HBM copy",
+                      "stand_in_ms": round(one, 3), "rows": rows}), flush=True)
     run.close()
 
 
@@ -490,6 +502,8 @@ def main():
                     help="instead of the bench line, time single retrieves of the first 1 ... 1024 blocks")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 1 GiB before each timed step; ms_per_step is then the median event span")
+    ap.add_argument("--stand-in", choices=["gemm", "copy"], default="gemm",
+                    help="with --pipeline: the per-layer compute stand-in (compute-bound GEMM or HBM-bound copy)")
     ap.add_argument("--pipeline", action="store_true",
                     help="instead of the bench line, overlap per-layer retrieval with stand-in compute")
     ap.add_argument("--ablation", action="store_true",

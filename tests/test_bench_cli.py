@@ -27,7 +27,8 @@ def test_help_lists_every_mode():
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup", "--config", "--layout", "--sdma", "--copy-ring-mib", "--flush",
                  "--pipeline", "--latency", "--duplex", "--ablation", "--layerwise", "--no-cpu-baseline",
-                 "--no-probes", "--no-copy-engine", "--host-grid", "--staging-grid", "--store-grid"):
+                 "--no-probes", "--no-copy-engine", "--host-grid", "--staging-grid", "--store-grid", "--stand-in",
+                 "--batch", "--context"):
         assert flag in r.stdout, flag
 
 
