@@ -283,6 +283,8 @@ def pipeline(args):
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     if args.staging_grid or args.staging_flags:   # also the ring kernel's shape with --sdma
         run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
+    if (args.host_grid or args.host_flags) and not args.sdma:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
     run.setup()
     q = wl.requests[0]
     kp, vp = run.layer_ptrs(run.dst)
@@ -349,6 +351,7 @@ def pipeline(args):
                       "workload": wl.name, "layers": sh.layers, "retrieve_only_ms": round(retrieve_only, 2),
                       "host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                       "staging_launch": {"grid": args.staging_grid or None, "flags": args.staging_flags},
+                      "host_launch": {"grid": args.host_grid or None, "flags": args.host_flags},
                       "stand_in": "bf16 GEMM 8192^3" if args.stand_in == "gemm" else "1 GiB HBM copy",
                       "stand_in_ms": round(one, 3), "rows": rows}), flush=True)
     run.close()
