@@ -73,6 +73,9 @@ def build(verbose: bool = False, extra: list[str] | None = None) -> str:
         if r.returncode != 0:
             raise RuntimeError("abi client build failed: %s\n%s%s" % (" ".join(cmd), r.stdout, r.stderr))
         os.replace(exe + ".tmp", exe)
+        # the same client over a host-sanitized build of the library (its own file: g++ only)
+        from . import build_asan
+        build_asan.build(os.path.join(BUILD, "kernels.hip.o"))
     if verbose:
         print("built", LIB)
     return LIB
