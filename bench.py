@@ -690,11 +690,11 @@ def main():
     if host_blocks and not args.sdma and not args.no_copy_engine:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
         for _ in range(args.warmup):
-            run.retrieve_all()
+            step()
         torch.cuda.synchronize()
         t = time.perf_counter()
         for _ in range(args.steps):
-            run.retrieve_all()
+            step()
         torch.cuda.synchronize()
         ce_ms = (time.perf_counter() - t) / args.steps * 1e3
         copy_engine = {"ms_per_step": round(ce_ms, 3), "gbps": round(wl.retrieved_bytes / ce_ms / 1e6, 2),
