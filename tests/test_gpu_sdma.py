@@ -230,3 +230,45 @@ def test_sdma_flag_validation():
         p.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     assert ei.value.name == "INVALID"
     p.close()
+
+
+def test_copy_ring_allocation_failure_is_reported_and_recoverable():
+    """With HBM filled from the host, resizing the ring fails with NOMEM; the transport then refuses
+    transfers with NOMEM (and no HIP error is left behind); clearing the flag brings back the kernel
+    path, and a later resize with memory free brings back the copy engines."""
+    wl = workloads.make(2, max_blocks=20)
+    run = make_run(wl)
+    filler = None
+    try:
+        host = run.setup(keep_host=True)
+        _sdma(run, [K.OP_RETRIEVE])
+        free, _ = torch.cuda.mem_get_info()
+        filler = torch.empty(max(0, free - (512 << 20)), dtype=torch.uint8, device="cuda")   # leave 512 MiB
+        with pytest.raises(K.KVPoolError) as ei:
+            # the resize frees the 2 x 1 GiB ring first: 2.5 GiB are then free, and 2 x 4 GiB cannot fit
+            run.pool.set_copy_ring(4 << 30)
+        assert ei.value.name == "NOMEM"
+        assert int(torch.full((8,), 2, device="cuda").sum()) == 16    # no HIP error left for the caller
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        with pytest.raises(K.KVPoolError) as ei:
+            run.pool.retrieve(run.retrieve_maps[q.request_id], q.dst_slots, wl.dst_num_slots, kp, vp,
+                              torch.cuda.current_stream().cuda_stream)
+        assert ei.value.name == "NOMEM"
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, 0)   # the zero-copy kernel needs no ring
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+        del filler
+        filler = None
+        torch.cuda.empty_cache()
+        run.pool.set_copy_ring(64 << 20)
+        _sdma(run, [K.OP_RETRIEVE])
+        run.fill_dst()
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        filler = None
+        run.close()
+        torch.cuda.empty_cache()
