@@ -360,7 +360,9 @@ def pipeline(args):
 def latency(args):
     """Call-to-complete time of small retrieves: the first n blocks of the request (striped over all
     regions) for n = 1 ... 1024, one call at a time with a host synchronisation after each.  This is
-    the fixed cost per call that a fetch of a few blocks sees."""
+    the fixed cost per call that a fetch of a few blocks sees.  Calls with a small work list run as one
+    launch with the list in the kernel arguments; --upload times them the way larger calls run (work
+    list uploaded, one launch per region class)."""
     import torch
 
     from kvgen import workloads
@@ -371,6 +373,8 @@ def latency(args):
     run = WorkloadRun(wl, device=0)
     if args.sdma:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+    if args.upload:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, (K.LAUNCH_SDMA if args.sdma else 0) | K.LAUNCH_UPLOAD)
     run.setup()
     q = wl.requests[0]
     kp, vp = run.layer_ptrs(run.dst)
@@ -378,7 +382,7 @@ def latency(args):
     cur = torch.cuda.current_stream()
     bb = wl.shape.block_bytes
     rows = []
-    for n in (1, 4, 16, 64, 256, 1024):
+    for n in (1, 4, 16, 32, 64, 256, 1024):
         sub, table = m[:n].copy(), q.dst_slots[:n].copy()
         for _ in range(3):
             run.pool.retrieve(sub, table, wl.dst_num_slots, kp, vp, cur.cuda_stream)
@@ -402,7 +406,7 @@ def latency(args):
         log(json.dumps(rows[-1]))
     print(json.dumps({"metric": "retrieve latency by request size (first n blocks, call to complete)",
                       "workload": wl.name, "host_transport": "copy engines" if args.sdma else "zero-copy kernel",
-                      "rows": rows}), flush=True)
+                      "small_call_launch": not args.upload, "rows": rows}), flush=True)
     run.close()
 
 
@@ -503,6 +507,8 @@ def main():
                     help="instead of the bench line, store one request while retrieving another")
     ap.add_argument("--latency", action="store_true",
                     help="instead of the bench line, time single retrieves of the first 1 ... 1024 blocks")
+    ap.add_argument("--upload", action="store_true",
+                    help="with --latency: no small-call launch (upload the work list, one launch per class)")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 1 GiB before each timed step; ms_per_step is then the median event span")
     ap.add_argument("--stand-in", choices=["gemm", "copy"], default="gemm",

@@ -300,6 +300,7 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
 #define KVP_LAUNCH_CHUNK_MAJOR 64u /* order units chunk by chunk over all blocks (the units in
                                     flight then write neighbouring slots of one layer buffer)
                                     instead of block by block */
+#define KVP_LAUNCH_UPLOAD  128u  /* on either class of an op: no small-call launch (below) */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
@@ -327,6 +328,19 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
  * does not fit) and kept until kv_pool_destroy; the grid and other flags of
  * the host class are unused while it is set.  Results are identical to the
  * kernel's.
+ *
+ * Small calls: when a store or retrieve moves no bytes through the
+ * copy-engine ring, has under 32 MiB of staging-class bytes, is not timed,
+ * and its work list -- 2 * (layers moved) engine pointers plus two 8-byte
+ * words per present block -- fits in 384 words (3 KiB), that list travels
+ * in the kernel arguments and both classes run in ONE launch: workgroups up
+ * to each class's grid (capped at its units), the copy form of the host
+ * class's flags (of the staging class's when no host-class block is moved),
+ * without KVP_LAUNCH_XCD and KVP_LAUNCH_CHUNK_MAJOR.  This saves the
+ * work-list upload and the wait between two launches (tens of microseconds
+ * on MI355X); for a full 32-layer range it covers up to 160 blocks.
+ * KVP_LAUNCH_UPLOAD on either class of the op turns it off (one launch per
+ * class after an upload, as for larger calls).  Results are identical.
  * Errors: INVALID (unknown flags; KVP_LAUNCH_SDMA on the staging class or on
  * a placement-only pool), NOMEM, HIP. */
 int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid, uint32_t flags);
@@ -353,7 +367,9 @@ typedef struct {
 } kvp_timing;
 
 /* Enable (1) or disable (0) HIP-event timing of the kernels store/retrieve
- * launch; either way the recorded history is cleared.  Timing events are
+ * launch; either way the recorded history is cleared.  Timed calls take one
+ * launch per class (never the small-call launch), so each class has a
+ * duration of its own.  Timing events are
  * recorded on the stream each kernel runs on (the caller's stream for the
  * host class, the pool's internal stream for the staging class unless the
  * call's staging bytes are few enough to run it on the caller's; with

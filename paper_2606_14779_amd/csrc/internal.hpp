@@ -217,7 +217,8 @@ struct CopyItem {          // 16 bytes, one block of work
 
 struct CopyArgs {
     const CopyItem *items;     // device
-    const uint64_t *cache;     // device, [2L]: base of layer l's K (2l) / V (2l+1)
+    const uint64_t *cache;     // device, [chunks]: engine buffer of moved chunk k, i.e. the K (even
+                               // chunk0 + k) or V (odd) buffer of layer (chunk0 + k) / 2
     uint32_t n_items;
     uint32_t chunks;           // chunks per item moved by this launch: 2 * (layers in range)
     uint32_t chunk0;           // first chunk: 2 * first layer
@@ -229,6 +230,19 @@ struct CopyArgs {
     uint32_t tokens;           //   bs
     uint32_t row_vec;          //   D*elem_bytes/16
     uint32_t layout;           // 0 head-major, 1 token-major
+};
+
+// A call whose work list is small enough travels in the kernel arguments,
+// and both classes run in one launch: workgroups [0, grid_host) take the
+// host-class items [0, n_host), the others the staging-class items.  There is
+// then no work-list upload and no second launch to wait for.
+constexpr uint32_t kInlineWords = 384;   // 3 KiB: [chunks cache pointers][items, two words each]
+
+struct SmallCallArgs {
+    CopyArgs a;                // geometry; a.items and a.cache unused, a.n_items = all items
+    uint32_t n_host;           // items [0, n_host) are host-class, the rest staging-class
+    uint32_t grid_host;        // workgroups taking the host-class items (the rest: staging)
+    uint64_t words[kInlineWords];
 };
 
 // ---------------------------------------------------------------- copy-engine plan (bounce.cpp)
@@ -278,6 +292,11 @@ void plan_bounce(const RingGeometry &g, std::vector<HostBlock> &blocks, uint64_t
 constexpr uint32_t kClassRing = 2;
 hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
                              hipStream_t s);
+// One launch of both classes for a call whose table and items are already in
+// f.words (f.a.chunks pointers, then f.a.n_items items); the copy form comes
+// from `flags`, the workgroups of each class from its grid, capped at its units.
+hipError_t launch_small_call(SmallCallArgs &f, bool gather, uint32_t grid_host, uint32_t grid_staging,
+                             uint32_t flags, hipStream_t s);
 hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid,
                              uint32_t flags, hipStream_t s);
 uint32_t default_grid(uint32_t cls, uint32_t op, const kvp_kv_spec &spec);

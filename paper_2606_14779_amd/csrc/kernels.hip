@@ -21,11 +21,12 @@
 // The work list and the engine pointer table are read with scalar loads, and
 // the next unit's entries are fetched while the current unit is copied.
 //
-// Three entry points share the body, so that traces and counters tell them
+// Four entry points share the body, so that traces and counters tell them
 // apart: host_region_copy (zero-copy reads or writes of pinned host regions
-// over the host link), staging_region_copy (HBM staging regions) and
+// over the host link), staging_region_copy (HBM staging regions),
 // ring_slot_copy (a copy-engine ring slot in HBM, whose host-link leg is a
-// hipMemcpy).
+// hipMemcpy), and small_call_copy (both region classes of a call whose work
+// list fits in the kernel arguments, in one launch with no upload).
 //
 // Three copy forms:
 //   - head-major pool chunks: the chunk is [H][bs][D] on both sides; a plain
@@ -211,11 +212,10 @@ struct Unit {
 // Unit u of a launch: item u / (chunks * parts), then chunk, then part of
 // the chunk (parts > 1 only for plain chunks); or, chunk-major, chunk
 // u / (items * parts), then item, then part, so that the units in flight
-// write neighbouring slots of one per-layer buffer.
-__device__ __forceinline__ Unit unit_at(const CopyArgs &a, uint32_t u)
+// write neighbouring slots of one per-layer buffer.  table[k] is the engine
+// buffer of moved chunk k; the pool block holds chunk chunk0 + k.
+__device__ __forceinline__ Unit unit_at(const CopyArgs &a, citem_t *items, cptr_t *table, uint32_t u)
 {
-    citem_t *items = (citem_t *)a.items;
-    cptr_t *table = (cptr_t *)a.cache;
     uint32_t item, k, p;
     if (a.chunk_major) {
         const uint32_t per_chunk = a.n_items * a.parts;
@@ -234,28 +234,25 @@ __device__ __forceinline__ Unit unit_at(const CopyArgs &a, uint32_t u)
     const uint64_t part = static_cast<uint64_t>(p) * (a.chunk_bytes / a.parts);
     const uint64_t pool = items[item].pool;
     const uint64_t slot = items[item].slot;
-    return Unit{pool + static_cast<uint64_t>(c) * a.chunk_bytes + part, table[c] + slot * a.chunk_bytes + part};
+    return Unit{pool + static_cast<uint64_t>(c) * a.chunk_bytes + part, table[k] + slot * a.chunk_bytes + part};
 }
 
+// Workgroup g of the G that share the launch's a.n_items items takes units
+// g, g + G, g + 2G, ...
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
-__device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
+__device__ __forceinline__ void chunk_copy_body(const CopyArgs &a, citem_t *items, cptr_t *table, uint32_t g,
+                                                uint32_t G)
 {
     extern __shared__ v4u lds[];
     const uint32_t units = a.n_items * a.chunks * a.parts;
     const uint32_t nvec = static_cast<uint32_t>((a.chunk_bytes / a.parts) >> 4);
-    uint32_t u = blockIdx.x;
-    if (a.xcd_remap) {
-        // workgroups are dealt to the 8 XCDs round-robin; renumber them so that
-        // each XCD takes one contiguous run of units per pass over the grid
-        const uint32_t per = gridDim.x / kXcds;          // grid is a multiple of 8 here
-        u = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-    }
+    uint32_t u = g;
     if (u >= units) return;
-    Unit cur = unit_at(a, u);
+    Unit cur = unit_at(a, items, table, u);
     for (;;) {
-        const uint32_t nu = u + gridDim.x;
+        const uint32_t nu = u + G;
         const bool more = nu < units;
-        const Unit next = more ? unit_at(a, nu) : cur;   // fetched while this chunk is copied
+        const Unit next = more ? unit_at(a, items, table, nu) : cur;   // fetched while this chunk is copied
         const v4u *src = reinterpret_cast<const v4u *>(GATHER ? cur.pool : cur.cache);
         v4u *dst = reinterpret_cast<v4u *>(GATHER ? cur.cache : cur.pool);
         if constexpr (FORM == kPlain)
@@ -270,25 +267,56 @@ __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a)
     }
 }
 
+// A launch of one class: the work list and table in device memory, every
+// workgroup on its items.
+template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+__device__ __forceinline__ void class_body(const CopyArgs &a)
+{
+    uint32_t g = blockIdx.x;
+    if (a.xcd_remap) {
+        // workgroups are dealt to the 8 XCDs round-robin; renumber them so that
+        // each XCD takes one contiguous run of units per pass over the grid
+        const uint32_t per = gridDim.x / kXcds;          // grid is a multiple of 8 here
+        g = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+    }
+    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a, (citem_t *)a.items, (cptr_t *)a.cache, g, gridDim.x);
+}
+
 // One entry point per kind of source, so that traces and counters tell the
 // zero-copy (host link) kernel, the HBM staging kernel and the kernel that
 // empties / fills a copy-engine ring slot apart.  The body is the same.
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __global__ __launch_bounds__(kThreads) void host_region_copy(CopyArgs a)
 {
-    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
+    class_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
 }
 
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __global__ __launch_bounds__(kThreads) void staging_region_copy(CopyArgs a)
 {
-    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
+    class_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
 }
 
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __global__ __launch_bounds__(kThreads) void ring_slot_copy(CopyArgs a)
 {
-    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
+    class_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
+}
+
+// Both classes of a small call in one launch, the table and the items read
+// from the kernel arguments (scalar loads, as from the work list).  The
+// class split is uniform per workgroup.
+template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+__global__ __launch_bounds__(kThreads) void small_call_copy(SmallCallArgs f)
+{
+    cptr_t *table = (cptr_t *)&f.words[0];
+    citem_t *items = (citem_t *)&f.words[f.a.chunks];
+    CopyArgs a = f.a;
+    const bool host = blockIdx.x < f.grid_host;
+    a.n_items = host ? f.n_host : f.a.n_items - f.n_host;
+    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a, host ? items : items + f.n_host, table,
+                                                    host ? blockIdx.x : blockIdx.x - f.grid_host,
+                                                    host ? f.grid_host : gridDim.x - f.grid_host);
 }
 
 // Contiguous streaming copy over tiles of 256*UNROLL vectors (bandwidth probe).
@@ -307,10 +335,17 @@ __global__ __launch_bounds__(kThreads) void probe_copy_kernel(const v4u *__restr
 
 // ---------------------------------------------------------------- host-side dispatch
 
-template <uint32_t CLS, bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
-static void launch_one(const CopyArgs &a, dim3 g, size_t lds, hipStream_t s)
+constexpr uint32_t kClassSmall = 3;   // dispatch only: small_call_copy
+
+__device__ __host__ inline const CopyArgs &geometry(const CopyArgs &a) { return a; }
+__device__ __host__ inline const CopyArgs &geometry(const SmallCallArgs &f) { return f.a; }
+
+template <uint32_t CLS, bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS, class A>
+static void launch_one(const A &a, dim3 g, size_t lds, hipStream_t s)
 {
-    if constexpr (CLS == KVP_CLASS_HOST)
+    if constexpr (CLS == kClassSmall)
+        hipLaunchKernelGGL((small_call_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
+    else if constexpr (CLS == KVP_CLASS_HOST)
         hipLaunchKernelGGL((host_region_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
     else if constexpr (CLS == KVP_CLASS_STAGING)
         hipLaunchKernelGGL((staging_region_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
@@ -318,8 +353,8 @@ static void launch_one(const CopyArgs &a, dim3 g, size_t lds, hipStream_t s)
         hipLaunchKernelGGL((ring_slot_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
 }
 
-template <uint32_t CLS, bool GATHER, int FORM, int UNROLL>
-static hipError_t launch_form(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
+template <uint32_t CLS, bool GATHER, int FORM, int UNROLL, class A>
+static hipError_t launch_form(const A &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
 {
     const bool ntl = flags & KVP_LAUNCH_NT_LOAD, nts = flags & KVP_LAUNCH_NT_STORE;
     const dim3 g(grid);
@@ -334,23 +369,25 @@ static hipError_t launch_form(const CopyArgs &a, uint32_t grid, uint32_t flags, 
     return hipGetLastError();
 }
 
-template <uint32_t CLS, bool GATHER, int FORM>
-static hipError_t launch_unroll(const CopyArgs &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
+template <uint32_t CLS, bool GATHER, int FORM, class A>
+static hipError_t launch_unroll(const A &a, uint32_t grid, uint32_t flags, size_t lds, hipStream_t s)
 {
     // enough 16-byte loads in flight per lane to cover the whole unit, up to 8
-    const uint64_t per_lane = (a.chunk_bytes / a.parts / 16 + kThreads - 1) / kThreads;
+    const CopyArgs &geo = geometry(a);
+    const uint64_t per_lane = (geo.chunk_bytes / geo.parts / 16 + kThreads - 1) / kThreads;
     if (per_lane >= 8) return launch_form<CLS, GATHER, FORM, 8>(a, grid, flags, lds, s);
     if (per_lane >= 4) return launch_form<CLS, GATHER, FORM, 4>(a, grid, flags, lds, s);
     if (per_lane >= 2) return launch_form<CLS, GATHER, FORM, 2>(a, grid, flags, lds, s);
     return launch_form<CLS, GATHER, FORM, 1>(a, grid, flags, lds, s);
 }
 
-template <uint32_t CLS, bool GATHER>
-static hipError_t launch_dir(const CopyArgs &a, uint32_t grid, uint32_t flags, hipStream_t s)
+template <uint32_t CLS, bool GATHER, class A>
+static hipError_t launch_dir(const A &a, uint32_t grid, uint32_t flags, hipStream_t s)
 {
-    if (a.layout == 0) return launch_unroll<CLS, GATHER, kPlain>(a, grid, flags, 0, s);
-    if ((flags & KVP_LAUNCH_LDS) && a.chunk_bytes <= kMaxLdsChunk)
-        return launch_unroll<CLS, GATHER, kConvertLds>(a, grid, flags, a.chunk_bytes, s);
+    const CopyArgs &geo = geometry(a);
+    if (geo.layout == 0) return launch_unroll<CLS, GATHER, kPlain>(a, grid, flags, 0, s);
+    if ((flags & KVP_LAUNCH_LDS) && geo.chunk_bytes <= kMaxLdsChunk)
+        return launch_unroll<CLS, GATHER, kConvertLds>(a, grid, flags, geo.chunk_bytes, s);
     return launch_unroll<CLS, GATHER, kConvert>(a, grid, flags, 0, s);
 }
 
@@ -374,6 +411,24 @@ hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, ui
         return gather ? launch_dir<KVP_CLASS_STAGING, true>(a, grid, flags, s)
                       : launch_dir<KVP_CLASS_STAGING, false>(a, grid, flags, s);
     return gather ? launch_dir<kClassRing, true>(a, grid, flags, s) : launch_dir<kClassRing, false>(a, grid, flags, s);
+}
+
+hipError_t launch_small_call(SmallCallArgs &f, bool gather, uint32_t grid_host, uint32_t grid_staging,
+                             uint32_t flags, hipStream_t s)
+{
+    CopyArgs &a = f.a;
+    if (a.n_items == 0) return hipSuccess;
+    a.parts = (a.layout == 0 && (flags & KVP_LAUNCH_SPLIT2) && a.chunk_bytes % 32 == 0) ? 2u : 1u;
+    a.xcd_remap = 0;
+    a.chunk_major = 0;
+    auto cap = [&](uint32_t grid, uint32_t n) {
+        const uint64_t units = static_cast<uint64_t>(n) * a.chunks * a.parts;
+        if (n == 0) return 0u;
+        return grid == 0 ? 1u : static_cast<uint32_t>(grid < units ? grid : units);
+    };
+    f.grid_host = cap(grid_host, f.n_host);
+    const uint32_t grid = f.grid_host + cap(grid_staging, a.n_items - f.n_host);
+    return gather ? launch_dir<kClassSmall, true>(f, grid, flags, s) : launch_dir<kClassSmall, false>(f, grid, flags, s);
 }
 
 hipError_t launch_probe_copy(void *dst, const void *src, uint64_t bytes, uint32_t grid, uint32_t flags,

@@ -210,20 +210,6 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     }
     if (n_items == 0) return;
 
-    // work list: [2L cache pointers][host items][staging items]
-    const size_t ptr_bytes = round_up(2ull * L * sizeof(uint64_t), 16);
-    const size_t bytes = ptr_bytes + n_items * sizeof(CopyItem);
-    Slot &slot = acquire_slot(p, bytes);
-    auto *ptrs = static_cast<uint64_t *>(slot.host);
-    for (uint32_t l = 0; l < L; ++l) {
-        const bool in = l >= layer_begin && l < layer_end;   // entries outside the range are never read
-        ptrs[2 * l] = in ? reinterpret_cast<uint64_t>(k_layers[l]) : 0;
-        ptrs[2 * l + 1] = in ? reinterpret_cast<uint64_t>(v_layers[l]) : 0;
-    }
-    auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(slot.host) + ptr_bytes);
-    std::copy(items[0].begin(), items[0].end(), list);
-    std::copy(items[1].begin(), items[1].end(), list + items[0].size());
-
     hipStream_t s = static_cast<hipStream_t>(stream_ptr);
     // ordering with earlier work on the same requests from any stream:
     // retrieve after store (read after write), store after store/retrieve
@@ -231,10 +217,80 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (gather && rec->stored_rec) check_hip(hipStreamWaitEvent(s, rec->stored, 0), "hipStreamWaitEvent");
         if (!gather && rec->busy_rec) check_hip(hipStreamWaitEvent(s, rec->busy, 0), "hipStreamWaitEvent");
     }
-    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
-    slot.pending = true;  // from here on the slot is in use even if a launch fails
+    auto mark_requests = [&] {
+        for (RequestRec *rec : touched) {
+            check_hip(hipEventRecord(rec->busy, s), "hipEventRecord");
+            rec->busy_rec = true;
+            if (!gather) {
+                check_hip(hipEventRecord(rec->stored, s), "hipEventRecord");
+                rec->stored_rec = true;
+            }
+        }
+    };
+    // one host-class kernel on the link at a time, in enqueue order: two of
+    // them would only share its bandwidth and both end late
+    auto take_link = [&] {
+        if (p.link_rec[op] && p.link_stream[op] != s)
+            check_hip(hipStreamWaitEvent(s, p.link_done[op], 0), "hipStreamWaitEvent");
+    };
+    auto hand_back_link = [&] {
+        check_hip(hipEventRecord(p.link_done[op], s), "hipEventRecord");
+        p.link_rec[op] = true;
+        p.link_stream[op] = s;
+    };
+
+    const uint32_t chunks = 2 * (layer_end - layer_begin);
+    CopyArgs geo = {};
+    geo.chunks = chunks;
+    geo.chunk0 = 2 * layer_begin;
+    geo.parts = 1;
+    geo.chunk_bytes = p.chunk_bytes;
+    geo.heads = p.spec.num_kv_heads;
+    geo.tokens = p.spec.block_size;
+    geo.row_vec = static_cast<uint32_t>(static_cast<uint64_t>(p.spec.head_dim) * p.spec.elem_bytes / 16);
+    geo.layout = p.spec.pool_layout;
+    auto fill_table = [&](uint64_t *t) {   // engine buffer of moved chunk k
+        for (uint32_t k = 0; k < chunks; ++k) {
+            const uint32_t l = layer_begin + k / 2;
+            t[k] = reinterpret_cast<uint64_t>(k % 2 ? v_layers[l] : k_layers[l]);
+        }
+    };
+
     // the internal stream takes work only for enough staging bytes or for ring batches
     const bool fork_staging = batches.empty() && items[KVP_CLASS_STAGING].size() * width >= kForkMinBytes;
+    const LaunchCfg &lh = p.launch[KVP_CLASS_HOST][op], &ls = p.launch[KVP_CLASS_STAGING][op];
+    const bool host = !items[KVP_CLASS_HOST].empty();
+    if (batches.empty() && !fork_staging && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
+        chunks + 2 * n_items <= kInlineWords) {
+        // Small call: table and items in the kernel arguments, both classes in
+        // one launch in the host class's copy form (the link-bound part; the
+        // form does not change what is written)
+        SmallCallArgs f = {};
+        f.a = geo;
+        f.a.n_items = static_cast<uint32_t>(n_items);
+        f.n_host = static_cast<uint32_t>(items[KVP_CLASS_HOST].size());
+        fill_table(f.words);
+        auto *list = reinterpret_cast<CopyItem *>(f.words + chunks);
+        std::copy(items[0].begin(), items[0].end(), list);
+        std::copy(items[1].begin(), items[1].end(), list + items[0].size());
+        if (host) take_link();
+        check_hip(launch_small_call(f, gather, lh.grid, ls.grid, host ? lh.flags : ls.flags, s), "kernel launch");
+        if (host) hand_back_link();
+        mark_requests();
+        return;
+    }
+
+    // work list: [chunks cache pointers][host items][staging items]
+    const size_t ptr_bytes = round_up(static_cast<size_t>(chunks) * sizeof(uint64_t), 16);
+    const size_t bytes = ptr_bytes + n_items * sizeof(CopyItem);
+    Slot &slot = acquire_slot(p, bytes);
+    fill_table(static_cast<uint64_t *>(slot.host));
+    auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(slot.host) + ptr_bytes);
+    std::copy(items[0].begin(), items[0].end(), list);
+    std::copy(items[1].begin(), items[1].end(), list + items[0].size());
+
+    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
+    slot.pending = true;  // from here on the slot is in use even if a launch fails
     if (fork_staging || !batches.empty()) check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
 
     const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
@@ -244,21 +300,11 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     // hardware queues a process gets, so caller streams (e.g. compute
     // overlapping a layerwise retrieve) are not serialised behind it.
     size_t first = 0;
-    CopyArgs args[2] = {};
+    CopyArgs args[2] = {geo, geo};
     for (uint32_t c = 0; c < 2; ++c) {
-        CopyArgs &a = args[c];
-        a.items = dev_list + first;
-        a.cache = static_cast<const uint64_t *>(slot.dev);
-        a.n_items = static_cast<uint32_t>(items[c].size());
-        a.chunks = 2 * (layer_end - layer_begin);
-        a.chunk0 = 2 * layer_begin;
-        a.parts = 1;
-        a.xcd_remap = 0;
-        a.chunk_bytes = p.chunk_bytes;
-        a.heads = p.spec.num_kv_heads;
-        a.tokens = p.spec.block_size;
-        a.row_vec = static_cast<uint32_t>(static_cast<uint64_t>(p.spec.head_dim) * p.spec.elem_bytes / 16);
-        a.layout = p.spec.pool_layout;
+        args[c].items = dev_list + first;
+        args[c].cache = static_cast<const uint64_t *>(slot.dev);
+        args[c].n_items = static_cast<uint32_t>(items[c].size());
         first += items[c].size();
     }
     TimedCall *tc = p.timing ? &p.timed.back() : nullptr;
@@ -280,15 +326,10 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         } else if (staging) {
             launch(KVP_CLASS_STAGING, s);   // small: in order on the caller's stream
         }
-        if (!items[KVP_CLASS_HOST].empty()) {
-            // one host-class kernel on the link at a time, in enqueue order:
-            // two of them would only share its bandwidth and both end late
-            if (p.link_rec[op] && p.link_stream[op] != s)
-                check_hip(hipStreamWaitEvent(s, p.link_done[op], 0), "hipStreamWaitEvent");
+        if (host) {
+            take_link();
             launch(KVP_CLASS_HOST, s);
-            check_hip(hipEventRecord(p.link_done[op], s), "hipEventRecord");
-            p.link_rec[op] = true;
-            p.link_stream[op] = s;
+            hand_back_link();
         }
         if (fork_staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     } else {
@@ -358,14 +399,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         }
     }
     check_hip(hipEventRecord(slot.done, s), "hipEventRecord");
-    for (RequestRec *rec : touched) {
-        check_hip(hipEventRecord(rec->busy, s), "hipEventRecord");
-        rec->busy_rec = true;
-        if (!gather) {
-            check_hip(hipEventRecord(rec->stored, s), "hipEventRecord");
-            rec->stored_rec = true;
-        }
-    }
+    mark_requests();
 }
 
 }  // namespace kvp
