@@ -473,7 +473,8 @@ def duplex(args):
            "store_alone_ms": round(st_ms, 2), "retrieve_alone_ms": round(rt_ms, 2),
            "both_ms": round(both_ms, 2), "serial_ms": round(st_ms + rt_ms, 2),
            "link_gbps_both_directions": round(2 * host_bytes / both_ms / 1e6, 2),
-           "launch": {"retrieve": "copy engines" if args.sdma else {"grid": args.host_grid or 12},
+           "launch": {"retrieve": "copy engines" if args.sdma else
+                      {"grid": args.host_grid or "library default: 12, 48 while a store is in flight"},
                       "store_grid": args.store_grid or 12}}
     print(json.dumps(out), flush=True)
     run.close()

@@ -307,7 +307,13 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
  * class 12 workgroups (16 for the token-major store); staging class 65536
  * with KVP_LAUNCH_SPLIT2 for the pool_layout 0 retrieve, else 8192;
  * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
- * pool_layout 1 except the host-class store.
+ * pool_layout 1 except the host-class store.  With the default host-class
+ * retrieve grid, a retrieve enqueued while a host-class store kernel of this
+ * pool has not finished takes 48 workgroups: with traffic both ways the
+ * link's reads need more in flight (measured on MI355X, a 128K-token
+ * LLaMA-shaped store and retrieve at once: 264.6 instead of 320 ms), while
+ * alone, or beside HBM-bound kernels, 12 do as well or better.  An explicit
+ * grid is always used as given.
  *
  * KVP_LAUNCH_SDMA (host class, either op) replaces the zero-copy kernel by
  * the GPU's copy engines: a call's host-class blocks, grouped per region into

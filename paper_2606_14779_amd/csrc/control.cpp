@@ -132,7 +132,7 @@ void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t
         DeviceScope dev(p.device);
         ensure_bounce(p);
     }
-    p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op, p.spec), flags};  // flags taken as given
+    p.launch[cls][op] = LaunchCfg{grid ? grid : default_grid(cls, op, p.spec), flags, grid == 0};   // flags as given
 }
 
 void pool_set_copy_ring(Pool &p, uint64_t slot_bytes)

@@ -138,6 +138,7 @@ struct Region {
 struct LaunchCfg {
     uint32_t grid;
     uint32_t flags;
+    bool default_grid;   // the library chose the grid (it may then adapt it per call)
 };
 
 struct Slot {                    // one work-list buffer of the upload ring

@@ -291,7 +291,8 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         r.alloc = RangeAllocator(r.capacity);
     }
     for (uint32_t c = 0; c < 2; ++c)
-        for (uint32_t o = 0; o < 2; ++o) p->launch[c][o] = LaunchCfg{default_grid(c, o, p->spec), default_flags(c, o, p->spec)};
+        for (uint32_t o = 0; o < 2; ++o)
+            p->launch[c][o] = LaunchCfg{default_grid(c, o, p->spec), default_flags(c, o, p->spec), true};
 
     p->device = hip_device;
     p->placement_only = hip_device < 0;

@@ -28,6 +28,12 @@ constexpr size_t kSlotMin = 64 * 1024;   // smallest work-list buffer
 // 25 us of host time per call, more than such a kernel takes (32 MiB read and
 // written at ~2.5 TB/s copied: ~13 us).
 constexpr uint64_t kForkMinBytes = 32ull << 20;
+// Host-class retrieve workgroups while a host-class store of this pool is in
+// flight.  Under two-way traffic the reads need more in flight: a 128K-token
+// LLaMA-shaped store and retrieve at once took 264.6 ms with 48 against
+// 320 ms with the 12 that a lone retrieve wants (which, beside HBM-bound
+// work, loses with more).
+constexpr uint32_t kDuplexReadGrid = 48;
 
 // The live allocation holding the block at map entry e, or an error.
 const Allocation *resolve(const Pool &p, const kvp_loc &e, uint32_t b, const Allocation *hint)
@@ -258,8 +264,20 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
 
     // the internal stream takes work only for enough staging bytes or for ring batches
     const bool fork_staging = batches.empty() && items[KVP_CLASS_STAGING].size() * width >= kForkMinBytes;
-    const LaunchCfg &lh = p.launch[KVP_CLASS_HOST][op], &ls = p.launch[KVP_CLASS_STAGING][op];
+    const LaunchCfg &ls = p.launch[KVP_CLASS_STAGING][op];
+    LaunchCfg lh = p.launch[KVP_CLASS_HOST][op];
     const bool host = !items[KVP_CLASS_HOST].empty();
+    if (gather && host && lh.default_grid && p.link_rec[KVP_OP_STORE] && lh.grid < kDuplexReadGrid &&
+        hipPeekAtLastError() == hipSuccess) {   // never clear an error the caller has yet to read
+        // a store's host-class kernel not yet finished: the link carries traffic both ways
+        const hipError_t q = hipEventQuery(p.link_done[KVP_OP_STORE]);
+        if (q == hipErrorNotReady) {
+            (void)hipGetLastError();   // "not ready" is the answer, not an error to leave behind
+            lh.grid = kDuplexReadGrid;
+        } else {
+            check_hip(q, "hipEventQuery");
+        }
+    }
     if (batches.empty() && !fork_staging && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
         chunks + 2 * n_items <= kInlineWords) {
         // Small call: table and items in the kernel arguments, both classes in
@@ -309,7 +327,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     }
     TimedCall *tc = p.timing ? &p.timed.back() : nullptr;
     auto launch = [&](uint32_t c, hipStream_t st) {
-        const LaunchCfg &lc = p.launch[c][op];
+        const LaunchCfg &lc = c == KVP_CLASS_HOST ? lh : p.launch[c][op];
         if (tc) check_hip(hipEventRecord(tc->t0[c], st), "hipEventRecord");
         check_hip(launch_chunk_copy(args[c], c, gather, lc.grid, lc.flags, st), "kernel launch");
         if (tc) {

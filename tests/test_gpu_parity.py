@@ -548,3 +548,51 @@ def test_many_regions(sdma):
         assert (counts > 0).sum() >= 35                      # the stripe reaches nearly every region
     finally:
         run.close()
+
+
+def _hip_last_error():
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipPeekAtLastError.restype = ctypes.c_int
+    return hip.hipPeekAtLastError()
+
+
+@pytest.mark.parametrize("n", [24, 160])
+@pytest.mark.parametrize("grid", [0, 12])
+def test_retrieve_while_store_in_flight(n, grid):
+    """A retrieve enqueued while a host-class store is running (the library then widens a default
+    read grid; an explicit one is kept), then a retrieve of the request being stored, which must
+    wait for that store.  Both against the oracle; no HIP error is left for the caller."""
+    import dataclasses
+    base = workloads.make(2, max_blocks=n)
+    regions = [dataclasses.replace(r) for r in base.regions]
+    workloads._size_regions(regions, [n, n], base.shape.block_bytes)
+    reqs = [workloads.RequestSpec(i + 1, n, n, np.arange(i * n, (i + 1) * n, dtype=np.int32)[::-1].copy(),
+                                  np.random.default_rng(i).permutation(2 * n)[:n].astype(np.int32))
+            for i in range(2)]
+    reqs[1] = dataclasses.replace(reqs[1], dst_slots=np.setdiff1d(np.arange(2 * n), reqs[0].dst_slots)[:n]
+                                  .astype(np.int32))
+    wl = workloads.Workload(2, base.name + "-x2", base.seed, base.shape, 0, regions, reqs, 2 * n, 2 * n)
+    say("case duplex", n, grid)
+    run = make_run(wl)
+    try:
+        if grid:
+            run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, grid, 0)
+        host = run.setup(keep_host=True)
+        q1, q2 = wl.requests
+        kp_s, vp_s = run.layer_ptrs(run.src)
+        kp_d, vp_d = run.layer_ptrs(run.dst)
+        cur = torch.cuda.current_stream()
+        a, b = torch.cuda.Stream(), torch.cuda.Stream()
+        a.wait_stream(cur)
+        b.wait_stream(cur)
+        run.pool.store(run.maps[q1.request_id], q1.src_slots, wl.src_num_slots, kp_s, vp_s, a.cuda_stream)
+        run.pool.retrieve_request(q2.request_id, q2.dst_slots, wl.dst_num_slots, kp_d, vp_d, b.cuda_stream)
+        run.pool.retrieve_request(q1.request_id, q1.dst_slots, wl.dst_num_slots, kp_d, vp_d, b.cuda_stream)
+        assert _hip_last_error() == 0
+        cur.wait_stream(a)
+        cur.wait_stream(b)
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
