@@ -45,10 +45,15 @@ def _case(seed):
     # unit order drawn from a generator of its own, so the draws above stay as they were
     order = np.random.default_rng(seed + 7919)
     flags = [f | (K.LAUNCH_CHUNK_MAJOR if order.random() < 0.4 else 0) for f in flags]
+    # every case here fits the small-call launch; about half are sent through the upload path
+    # instead (the flag on the host class of both ops), again from a generator of its own
+    if np.random.default_rng(seed + 104729).random() < 0.5:
+        flags[0] |= K.LAUNCH_UPLOAD
+        flags[1] |= K.LAUNCH_UPLOAD
     return rng, layout, (L, H, bs, D), kinds, weights, n, grid, flags
 
 
-@pytest.mark.parametrize("seed", list(range(24)))
+@pytest.mark.parametrize("seed", list(range(40)))
 def test_random_case(seed):
     rng, layout, (L, H, bs, D), kinds, weights, n, grid, flags = _case(seed)
     say("fuzz", seed, dict(layout=layout, L=L, H=H, bs=bs, D=D, kinds=kinds, w=weights, n=n, grid=grid, flags=flags))
