@@ -3,7 +3,8 @@
 Requests are placed, stored, retrieved and released in random order, on
 three streams with no host synchronisation between the operations of a
 round; released ranges are placed again; the host-class transport is
-switched between the zero-copy kernel and the copy engines along the way.
+switched between the zero-copy kernel and the copy engines along the way,
+and small calls between their one-launch form and the upload path.
 Checked against what placement and the round trip fix:
 
 - every map equals the oracle's, the oracle pool carrying the same place /
@@ -48,6 +49,7 @@ def _need_gpu():
 @pytest.mark.parametrize("layout", [0, 1])
 def test_random_lifecycle(layout):
     rng = np.random.default_rng(SEED + layout)
+    path_rng = np.random.default_rng(SEED + 17 + layout)   # upload bit: apart, so rng's sequence is unchanged
     shape = workloads.KVShape("lifecycle", L, H, D)
     bb = shape.block_bytes
     weights = [3, 1, 2, 2]
@@ -151,7 +153,8 @@ def test_random_lifecycle(layout):
                     sdma[o] = not sdma[o]
                     # back to the library's defaults for the zero-copy kernel
                     default = K.LAUNCH_NT_STORE if o == K.OP_STORE else (K.LAUNCH_LDS if layout == 1 else 0)
-                    pool.set_launch(K.CLASS_HOST, o, 0, K.LAUNCH_SDMA if sdma[o] else default)
+                    upload = K.LAUNCH_UPLOAD if path_rng.random() < 0.5 else 0
+                    pool.set_launch(K.CLASS_HOST, o, 0, (K.LAUNCH_SDMA if sdma[o] else default) | upload)
                     counts["toggle"] += 1
             torch.cuda.synchronize()
             got = dst.cpu().numpy().view(np.uint16)
