@@ -16,6 +16,8 @@
 
 #include <algorithm>
 
+#include <unordered_map>
+
 #include "internal.hpp"
 
 namespace kvp {
@@ -161,7 +163,28 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::vector<CopyItem> items[2];
     std::vector<HostBlock> host_blocks;   // copy-engine transport: placed in ring slots below
     std::vector<RequestRec *> touched;
-    std::vector<uint64_t> targets;   // store: (region, offset) keys; retrieve: destination slots
+    // No two present entries may write the same place: a destination slot on
+    // retrieve, a pool block on store.  One pass over bitmaps -- of the
+    // destination slots, or of the blocks of each allocation a store touches
+    // (the block index within its allocation is exact after resolve) -- with
+    // sorted slots only for a retrieve into far more slots than it moves.
+    std::vector<uint64_t> seen;
+    const bool slot_bits = gather && num_slots <= std::max<uint64_t>(64ull * n_blocks, 1ull << 16);
+    if (slot_bits) seen.assign((num_slots + 63) / 64, 0);
+    std::vector<uint32_t> wide_slots;
+    std::unordered_map<const Allocation *, uint64_t> alloc_word;   // store: first bitmap word of an allocation
+    std::vector<uint64_t> region_word(p.regions.size(), 0);        // store: that of each region's hint
+    bool dup = false;
+    uint64_t dup_slot = 0;
+    auto mark = [&](uint64_t bit) {
+        uint64_t &w = seen[bit >> 6];
+        const uint64_t m = 1ull << (bit & 63);
+        if ((w & m) && !dup) {
+            dup = true;
+            dup_slot = bit;
+        }
+        w |= m;
+    };
     // one hint per region: a request's blocks in a region share one range,
     // while consecutive blocks of a striped map alternate between regions
     std::vector<const Allocation *> hints(p.regions.size(), nullptr);
@@ -169,13 +192,27 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         const kvp_loc &e = map[b];
         if (e.region == KVP_ABSENT) continue;
         const Allocation *hint = resolve(p, e, b, e.region < hints.size() ? hints[e.region] : nullptr);
+        const bool new_hint = hint != hints[e.region];
         hints[e.region] = hint;
         const int32_t slot = table[b];
         if (slot < 0 || static_cast<uint32_t>(slot) >= num_slots)
             fail(KVP_ERR_INVALID, "block table entry " + std::to_string(b) + " = " + std::to_string(slot) +
                                       " outside [0, " + std::to_string(num_slots) + ")");
-        targets.push_back(gather ? static_cast<uint64_t>(slot)
-                                 : (static_cast<uint64_t>(e.region) << 48) | (e.offset >> 4));
+        if (slot_bits) {
+            mark(static_cast<uint64_t>(slot));
+        } else if (gather) {
+            wide_slots.push_back(static_cast<uint32_t>(slot));
+        } else {
+            if (new_hint) {
+                auto it = alloc_word.find(hint);
+                if (it == alloc_word.end()) {
+                    it = alloc_word.emplace(hint, seen.size()).first;
+                    seen.resize(seen.size() + (hint->blocks + 63) / 64, 0);
+                }
+                region_word[e.region] = it->second;
+            }
+            mark(region_word[e.region] * 64 + (e.offset - hint->base) / p.block_bytes);
+        }
         if (std::find(touched.begin(), touched.end(), hint->owner) == touched.end()) touched.push_back(hint->owner);
         const Region &r = p.regions[e.region];
         const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
@@ -184,12 +221,16 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         else
             items[cls].push_back(CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
     }
-    // no two present entries may write the same place (a destination slot on
-    // retrieve, a pool block on store): sorted keys, independent of num_slots
-    std::sort(targets.begin(), targets.end());
-    auto dup = std::adjacent_find(targets.begin(), targets.end());
-    if (dup != targets.end())
-        fail(KVP_ERR_INVALID, gather ? "destination slot " + std::to_string(*dup) + " named twice"
+    if (!wide_slots.empty()) {
+        std::sort(wide_slots.begin(), wide_slots.end());
+        auto d = std::adjacent_find(wide_slots.begin(), wide_slots.end());
+        if (d != wide_slots.end()) {
+            dup = true;
+            dup_slot = *d;
+        }
+    }
+    if (dup)
+        fail(KVP_ERR_INVALID, gather ? "destination slot " + std::to_string(dup_slot) + " named twice"
                                      : std::string("two map entries name the same pool block"));
     const uint64_t width = 2ull * (layer_end - layer_begin) * p.chunk_bytes;   // bytes moved per block
     const uint64_t skip = 2ull * layer_begin * p.chunk_bytes;

@@ -190,6 +190,10 @@ def test_errors_leave_destination_untouched():
         dup = q.dst_slots.copy()
         dup[4] = dup[5]
         assert code(run.pool.retrieve, m, dup, wl.dst_num_slots, kp, vp, 0) == "INVALID"
+        assert code(run.pool.retrieve, m, dup, 1 << 24, kp, vp, 0) == "INVALID"   # far more slots than blocks
+        dup = q.dst_slots.copy()
+        dup[-1] = dup[0]
+        assert code(run.pool.retrieve, m, dup, wl.dst_num_slots, kp, vp, 0) == "INVALID"
         mm = m.copy()
         mm["region"][2] = 17
         assert code(run.pool.retrieve, mm, q.dst_slots, wl.dst_num_slots, kp, vp, 0) == "INVALID"
@@ -204,6 +208,9 @@ def test_errors_leave_destination_untouched():
         assert code(run.pool.retrieve, m, q.dst_slots, wl.dst_num_slots, kp2, vp, 0) == "INVALID"
         same = m.copy()
         same[1] = same[0]
+        assert code(run.pool.store, same, q.src_slots, wl.src_num_slots, *run.layer_ptrs(run.src), 0) == "INVALID"
+        same = m.copy()
+        same[9] = same[0]                                     # other regions' entries in between
         assert code(run.pool.store, same, q.src_slots, wl.src_num_slots, *run.layer_ptrs(run.src), 0) == "INVALID"
         torch.cuda.synchronize()
         got = run.dst.cpu().numpy().view(np.uint16)
@@ -592,6 +599,28 @@ def test_retrieve_while_store_in_flight(n, grid):
         assert _hip_last_error() == 0
         cur.wait_stream(a)
         cur.wait_stream(b)
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+def test_store_batch_and_retrieve_into_very_many_slots():
+    """The four requests of workload 5 stored again in ONE call (several allocations per region in
+    one map), then retrieved with a destination slot count far above the blocks moved (the
+    duplicate check then sorts instead of using a bitmap); against the oracle."""
+    wl = workloads.make(5, max_blocks=40)
+    say("case store batch")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        maps = np.concatenate([run.maps[q.request_id] for q in wl.requests])
+        src = np.concatenate([q.src_slots for q in wl.requests]).astype(np.int32)
+        run.pool.store(maps, src, wl.src_num_slots, *run.layer_ptrs(run.src), torch.cuda.current_stream().cuda_stream)
+        kp, vp = run.layer_ptrs(run.dst)
+        for q in wl.requests:
+            run.pool.retrieve(run.retrieve_maps[q.request_id], q.dst_slots, 1 << 24, kp, vp,
+                              torch.cuda.current_stream().cuda_stream)
         torch.cuda.synchronize()
         check_full(wl, run, host)
     finally:
