@@ -10,10 +10,11 @@
 // 1 KiB of contiguous memory, which the memory system merges into full
 // 128-byte lines.
 //
-// The grid is persistent: workgroup g takes units g, g+G, g+2G, ...  Unit u
-// is part u % parts of chunk (u / parts) % (2L) of work item u / (2L*parts),
-// so neighbouring workgroups read neighbouring pieces of the same pool block
-// (the pool side streams through memory in address order).  There is no data
+// The grid is persistent: workgroup g takes units g, g+G, g+2G, ...  With K
+// moved chunks per block (2L for all layers, fewer for a layer range), unit
+// u is part u % parts of moved chunk (u / parts) % K of work item
+// u / (K*parts), so neighbouring workgroups read neighbouring pieces of the
+// same pool block (the pool side streams through memory in address order).  There is no data
 // reuse; an optional renumbering that gives each of the 8 XCDs contiguous
 // units (KVP_LAUNCH_XCD) measured no better than the round-robin default, and
 // so did the optional chunk-major order (KVP_LAUNCH_CHUNK_MAJOR), in which the

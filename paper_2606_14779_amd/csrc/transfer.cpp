@@ -9,10 +9,12 @@
 // kernel runs on the caller's stream, and the two are joined again on the
 // caller's stream, so the caller sees one stream-ordered operation.  The store
 // (Alg. 1, offload) is the same path in the other direction.  The per-call
-// work list (one 16-byte item per block plus the 2L engine-buffer pointers) is
-// written to a pinned buffer and uploaded with one asynchronous copy; buffers
-// come from a ring guarded by events, so a call only blocks when the ring
-// wraps onto work that is still running.
+// work list (the engine-buffer pointers of the moved chunks, then one 16-byte
+// item per block) travels in the kernel arguments of a single launch when it
+// is small enough; otherwise it is written to a pinned buffer and uploaded
+// with one asynchronous copy.  Those buffers come from a ring guarded by
+// events, so a call only blocks when the ring wraps onto work that is still
+// running.
 
 #include <algorithm>
 
@@ -405,10 +407,10 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             char *ring = p.bounce + static_cast<uint64_t>(bt.ring) * p.bounce_slot_bytes;
             for (size_t i = bt.run0; i < bt.run0 + bt.runs; ++i) {
                 const LinkRun &run = runs[i];
-                char *host = static_cast<char *>(p.regions[run.region].host) + run.offset + skip;
+                char *hmem = static_cast<char *>(p.regions[run.region].host) + run.offset + skip;
                 char *dev = ring + run.slot_offset;
-                void *dst = gather ? static_cast<void *>(dev) : static_cast<void *>(host);
-                const void *src = gather ? static_cast<const void *>(host) : static_cast<const void *>(dev);
+                void *dst = gather ? static_cast<void *>(dev) : static_cast<void *>(hmem);
+                const void *src = gather ? static_cast<const void *>(hmem) : static_cast<const void *>(dev);
                 if (width == p.block_bytes)
                     check_hip(hipMemcpyAsync(dst, src, run.blocks * width, kind, sc), "hipMemcpyAsync");
                 else
