@@ -493,6 +493,7 @@ def main():
     ap.add_argument("--staging-grid", type=int, default=0)
     ap.add_argument("--host-flags", type=int, default=0)
     ap.add_argument("--store-grid", type=int, default=0, help="host-class store workgroups (0: library default)")
+    ap.add_argument("--store-flags", type=int, default=-1, help="host-class store flags (-1: library default)")
     ap.add_argument("--staging-flags", type=int, default=0)
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
@@ -561,6 +562,9 @@ def main():
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     if args.staging_grid or args.staging_flags:
         run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
+    if args.store_grid or args.store_flags >= 0:     # the host-class store the line also times
+        run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, args.store_grid,
+                            K.LAUNCH_NT_STORE if args.store_flags < 0 else args.store_flags)
     log("pool created in %.1f s" % t_create)
     t = time.perf_counter()
     run.fill_source()
@@ -792,6 +796,8 @@ def main():
         "launch": {"host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                    "host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,
                    "host_flags": args.host_flags, "staging_flags": args.staging_flags,
+                   "store_grid": args.store_grid or None,
+                   "store_flags": None if args.store_flags < 0 else args.store_flags,
                    "coherence": args.coherence},
     }
     print(json.dumps(out), flush=True)

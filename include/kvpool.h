@@ -304,7 +304,7 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
- * class 12 workgroups (16 for the token-major store); staging class 65536
+ * class 12 workgroups (token-major pool: 16, 20 for the store); staging class 65536
  * with KVP_LAUNCH_SPLIT2 for the pool_layout 0 retrieve, else 8192;
  * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
  * pool_layout 1 except the host-class store.  With the default host-class

@@ -231,13 +231,17 @@ uint32_t default_grid(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
     // Host class: the link needs only about its bandwidth-delay product in
     // flight; 12 workgroups x 32 KiB keep a PCIe 5.0 x16 link at its measured
     // peak, while more of them only queue reads in the shared memory path and
-    // slow the HBM kernel running beside them.  The token-major store (host
-    // writes in runs of whole chunks, reads from HBM by rows) wants 16.
+    // slow the HBM kernel running beside them.  A token-major pool wants
+    // more: its LDS-staged retrieve has no link reads in flight while a
+    // workgroup writes its chunk out (128K LLaMA-shaped retrieve: 200.5-200.7
+    // ms at 16, 201.7 at 12, 206 at 20, 216 at 24), and its store writes the
+    // host side in runs of whole chunks while reading HBM by rows (205.3 ms
+    // at 20 or 24, 207.4-208.7 at 16, 211.2 at 12).
     // Staging class: many workgroups so the HBM kernel keeps its share of
     // the memory queues while the host kernel runs -- 65536 half-chunk units
     // in flight for the plain retrieve (2.4 ms beside the host kernel, 2.22 ms
     // alone), 8192 otherwise.
-    if (cls == KVP_CLASS_HOST) return (op == KVP_OP_STORE && spec.pool_layout == 1) ? 16u : 12u;
+    if (cls == KVP_CLASS_HOST) return spec.pool_layout == 1 ? (op == KVP_OP_STORE ? 20u : 16u) : 12u;
     return (op == KVP_OP_RETRIEVE && spec.pool_layout == 0) ? 65536u : 8192u;
 }
 
