@@ -138,3 +138,25 @@ def test_back_to_back_small_calls_on_two_streams():
         check_full(wl, run, host)
     finally:
         run.close()
+
+
+def test_thousands_of_queued_small_calls():
+    """2000 one-block retrieves enqueued on one stream with no synchronisation: each launch holds
+    its own 3 KiB argument block until it runs; the result is the same as one call."""
+    wl = workloads.make(2, max_blocks=37)
+    say("case small-call queue")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        m = run.retrieve_maps[q.request_id]
+        s = torch.cuda.current_stream().cuda_stream
+        one = [(m[b:b + 1].copy(), q.dst_slots[b:b + 1].copy()) for b in range(q.n_present)]
+        for i in range(2000):
+            mb, tb = one[i % q.n_present]
+            run.pool.retrieve(mb, tb, wl.dst_num_slots, kp, vp, s)
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
