@@ -326,10 +326,11 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
  * staging-class blocks are then moved too.  The copy engines hold no compute
  * units while the bytes cross the link, so kernels running beside a retrieve
  * keep the whole GPU; the price is one HBM write and read of the host bytes.
- * It pays for the retrieve only: device-to-host copies are run by the HIP
- * runtime's own copy kernel (measured: 256 workgroups, 53.8 GB/s on MI355X),
- * slower than the zero-copy store kernel (12 workgroups, 56 GB/s) and holding
- * more compute units; the store op accepts the flag, with identical results.
+ * For the store, whether the device-to-host copies stay on the copy engines
+ * is the HIP runtime's choice: ROCm 7.2's runtime keeps them there, while the
+ * 7.0 runtime that PyTorch 2.10 ships runs them as a copy kernel of its own
+ * on 256 workgroups (as fast as the 12-workgroup store kernel, but holding
+ * more compute units); the no-CU copy kind does not change that.
  * The ring is allocated when the flag is first set (NOMEM if it
  * does not fit) and kept until kv_pool_destroy; the grid and other flags of
  * the host class are unused while it is set.  Results are identical to the

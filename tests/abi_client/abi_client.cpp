@@ -108,6 +108,18 @@ int main()
     TRY(kv_pool_retrieve_layers(pool, map.data(), n, dst_table.data(), slots, 1, L, k_dst.data(), v_dst.data(), stream));
     HIPTRY(hipStreamSynchronize(stream));
     if (check()) return 1;
+    // store through the copy engines too (ring to host region), after clearing the host region's copy,
+    // then retrieve by the kernel path: the pool bytes the engines wrote reach the cache unchanged
+    TRY(kv_pool_set_launch(pool, KVP_CLASS_HOST, KVP_OP_STORE, 0, KVP_LAUNCH_SDMA));
+    kvp_region_info info;
+    TRY(kv_pool_region_info(pool, 0, &info));
+    std::memset(info.host_ptr, 0, info.capacity_bytes);
+    TRY(kv_pool_store(pool, map.data(), n, src_table.data(), slots, k_src.data(), v_src.data(), stream));
+    for (uint32_t i = 0; i < 2 * L; ++i) HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
+    TRY(kv_pool_set_launch(pool, KVP_CLASS_HOST, KVP_OP_RETRIEVE, 0, KVP_LAUNCH_UPLOAD));
+    TRY(kv_pool_retrieve(pool, map.data(), n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
+    HIPTRY(hipStreamSynchronize(stream));
+    if (check()) return 1;
     TRY(kv_pool_release(pool, 42));
     kv_pool_destroy(pool);
     HIPTRY(hipStreamDestroy(stream));
@@ -117,7 +129,7 @@ int main()
         std::fprintf(stderr, "abi client: %llu mismatching chunks or elements\n", (unsigned long long)bad);
         return 1;
     }
-    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, copy engines)\n",
+    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, copy engines both ways)\n",
                 n);
     return 0;
 }
