@@ -74,7 +74,12 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, u
         if (!out) kvp::fail(KVP_ERR_INVALID, "out is null");
         *out = nullptr;
         kvp::Pool *p = kvp::pool_create(regions, bandwidths, n_regions, spec, hip_device);
-        *out = new kvp_pool{p};
+        try {
+            *out = new kvp_pool{p};
+        } catch (...) {
+            kvp::pool_destroy(p);
+            throw;
+        }
     });
 }
 
