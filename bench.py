@@ -193,7 +193,9 @@ def cpu_baseline(run, wl, budget_s=10.0, max_blocks=1024):
             break
     gbps_t = tpass * n * sh.block_bytes / elt / 1e9
     return {"value": round(gbps, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "threads": {"cores": T, "value": round(gbps_t, 3), "passes": tpass},
+            "threads": {"cores": T, "value": round(gbps_t, 3), "passes": tpass,
+                        "note": "host-to-host copies: the oracle's destination is host memory, so no host link "
+                                "is crossed; not a rate into HBM"},
             "sample": "first %d of %d blocks (%.2f GiB; %d host-region, %d staging blocks mirrored to host), "
                       "destination slots renumbered, %d passes in %.1f s" % (
                           n, q.n_present, n * sh.block_bytes / 2**30, n - len(mirrors), len(mirrors), passes, el),
