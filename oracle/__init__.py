@@ -61,6 +61,8 @@ def _load():
             lib.oracle_pool_free.argtypes = [vp]
             lib.oracle_place.restype = i32
             lib.oracle_place.argtypes = [vp, u64, u32, vp]
+            lib.oracle_extend.restype = i32
+            lib.oracle_extend.argtypes = [vp, u64, u32, vp]
             lib.oracle_lookup.restype = i32
             lib.oracle_lookup.argtypes = [vp, u64, u32, vp]
             lib.oracle_release.restype = i32
@@ -118,6 +120,19 @@ class Pool:
         out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
         rc = _load().oracle_place(self._p, request, n_blocks, out.ctypes.data)
         return rc, out[:n_blocks]
+
+    def extend(self, request: int, n_new: int) -> np.ndarray:
+        """The next offload set of a placed request: entries of its blocks n_old .. n_old+n_new-1."""
+        out = np.zeros(n_new, dtype=LOC_DTYPE)
+        rc = _load().oracle_extend(self._p, request, n_new, out.ctypes.data)
+        if rc:
+            raise PlacementError(rc)
+        return out
+
+    def try_extend(self, request: int, n_new: int):
+        out = np.zeros(max(n_new, 1), dtype=LOC_DTYPE)
+        rc = _load().oracle_extend(self._p, request, n_new, out.ctypes.data)
+        return rc, out[:n_new]
 
     def lookup(self, request: int, n_blocks: int) -> np.ndarray:
         out = np.zeros(n_blocks, dtype=LOC_DTYPE)

@@ -15,7 +15,10 @@
  *   oracle_place     Algorithm 1 (partition part) + one contiguous range
  *                    per (request, device) as in Sec. 4.2 + GLT record
  *                    (Table "Fields of the GLT").
- *   oracle_release   return a request's ranges.
+ *   oracle_extend    the next offload set of a placed request (the KV
+ *                    caches of a later decoding step, Sec. 4.1.3): the same
+ *                    steps on the new blocks alone, their own ranges.
+ *   oracle_release   return all of a request's ranges.
  *   oracle_store     offload copy, Algorithm 1 (store part, MemStore).
  *   oracle_gather    retrieval copy, Sec. 4.3 "KV Retrieval".
  *
@@ -31,6 +34,9 @@
  *  R4 bandwidths are positive integers; p_i = b_i / sum b is never rounded:
  *     floor(p_i * n) is computed as floor(b_i * n / W) exactly.
  *  R5 placement unit: one block (block_size tokens, all layers, K and V).
+ *  R6 offload set: the blocks of one place or extend call.  Counts, the
+ *     interleave and the ranges of R7 are taken per set, so an extension
+ *     never moves earlier blocks; all sets of a request share its gen.
  *  R7 location: a byte offset inside the device, both for host memory and
  *     for the SSD stand-in; each (request, device) gets one contiguous range
  *     of ceil(c_i * block_bytes / 4096) sectors of 4096 bytes, taken first fit
@@ -116,8 +122,9 @@ typedef struct {
     uint32_t n_blocks;
     uint32_t gen;
     oracle_loc *map;
-    uint64_t *base; /* per device, range start (if len > 0) */
-    uint64_t *len;  /* per device, range length in bytes (0 = none) */
+    uint32_t n_sets; /* offload sets placed (place, then each extend) */
+    uint64_t *base;  /* [set][device]: range start (if len > 0) */
+    uint64_t *len;   /* [set][device]: range length in bytes (0 = none) */
 } orecord;
 
 typedef struct {
@@ -224,33 +231,34 @@ static void give_back(ofreelist *f, uint64_t start, uint64_t len)
 }
 
 /*
- * Place the n_blocks blocks of one request.  Return codes: 0 ok, -1 bad
- * input or request already placed, -3 some device has no contiguous range
- * large enough (nothing changes in that case).
+ * One offload set of n blocks (Algorithm 1 on the set): Eq. 2 counts, one
+ * contiguous sector-rounded range per device with a share (Sec. 4.2, first
+ * fit), then the blocks in index order to the device with room and the
+ * largest deficit (R3).  Fills out[0..n) with gen and base/len[0..N).
+ * Returns 0, -1 (bad input) or -3 (some device has no range large enough;
+ * nothing changes).
  */
-int oracle_place(opool *p, uint64_t request, uint32_t n_blocks, oracle_loc *out)
+static int place_set(opool *p, uint32_t n, uint32_t gen, oracle_loc *out, uint64_t *base, uint64_t *len)
 {
-    if (!p || n_blocks == 0 || find_record(p, request) >= 0) return -1;
     const uint32_t N = p->n_dev;
     uint64_t *count = (uint64_t *)calloc(N, sizeof(uint64_t));
     uint64_t *given = (uint64_t *)calloc(N, sizeof(uint64_t));
-    uint64_t *base = (uint64_t *)calloc(N, sizeof(uint64_t));
-    uint64_t *len = (uint64_t *)calloc(N, sizeof(uint64_t));
     int *slot = (int *)malloc(N * sizeof(int));
-    if (!count || !given || !base || !len || !slot || oracle_counts(p->bandwidth, N, n_blocks, count)) {
-        free(count); free(given); free(base); free(len); free(slot);
+    if (!count || !given || !slot || oracle_counts(p->bandwidth, N, n, count)) {
+        free(count); free(given); free(slot);
         return -1;
     }
 
     /* Sec. 4.2: one contiguous range of ceil(c_i * KV_size / sector) sectors
      * per device.  Check every device first so that a failure changes nothing. */
     for (uint32_t i = 0; i < N; ++i) {
+        base[i] = 0;
         len[i] = (count[i] * p->block_bytes + ORACLE_SECTOR - 1) / ORACLE_SECTOR * ORACLE_SECTOR;
         slot[i] = -1;
         if (len[i] == 0) continue;
         slot[i] = first_fit(&p->free[i], len[i]);
         if (slot[i] < 0) {
-            free(count); free(given); free(base); free(len); free(slot);
+            free(count); free(given); free(slot);
             return -3;
         }
     }
@@ -265,13 +273,12 @@ int oracle_place(opool *p, uint64_t request, uint32_t n_blocks, oracle_loc *out)
 
     /* Algorithm 1, partition part: blocks in index order, each to the device
      * with room and the largest deficit (R3). */
-    const uint32_t gen = p->next_gen++;
-    for (uint32_t j = 0; j < n_blocks; ++j) {
+    for (uint32_t j = 0; j < n; ++j) {
         uint32_t best = N;
         __int128 best_score = 0;
         for (uint32_t i = 0; i < N; ++i) {
             if (given[i] >= count[i]) continue;
-            __int128 score = (__int128)(j + 1) * (__int128)count[i] - (__int128)n_blocks * (__int128)given[i];
+            __int128 score = (__int128)(j + 1) * (__int128)count[i] - (__int128)n * (__int128)given[i];
             if (best == N || score > best_score) {
                 best = i;
                 best_score = score;
@@ -282,6 +289,33 @@ int oracle_place(opool *p, uint64_t request, uint32_t n_blocks, oracle_loc *out)
         out[j].offset = base[best] + given[best] * p->block_bytes;
         given[best] += 1;
     }
+    free(count);
+    free(given);
+    free(slot);
+    return 0;
+}
+
+/*
+ * Place the n_blocks blocks of one request.  Return codes: 0 ok, -1 bad
+ * input or request already placed, -3 some device has no contiguous range
+ * large enough (nothing changes in that case).
+ */
+int oracle_place(opool *p, uint64_t request, uint32_t n_blocks, oracle_loc *out)
+{
+    if (!p || n_blocks == 0 || find_record(p, request) >= 0) return -1;
+    const uint32_t N = p->n_dev;
+    uint64_t *base = (uint64_t *)calloc(N, sizeof(uint64_t));
+    uint64_t *len = (uint64_t *)calloc(N, sizeof(uint64_t));
+    if (!base || !len) {
+        free(base); free(len);
+        return -1;
+    }
+    const int rc = place_set(p, n_blocks, p->next_gen, out, base, len);
+    if (rc) {
+        free(base); free(len);
+        return rc;
+    }
+    const uint32_t gen = p->next_gen++;
 
     /* UpdateGLT: keep the record */
     if (p->n_rec == p->cap_rec) {
@@ -297,11 +331,40 @@ int oracle_place(opool *p, uint64_t request, uint32_t n_blocks, oracle_loc *out)
     r->gen = gen;
     r->map = (oracle_loc *)malloc(n_blocks * sizeof(oracle_loc));
     memcpy(r->map, out, n_blocks * sizeof(oracle_loc));
+    r->n_sets = 1;
     r->base = base;
     r->len = len;
-    free(count);
-    free(given);
-    free(slot);
+    return 0;
+}
+
+/*
+ * The next offload set of a placed request: blocks n_old .. n_old+n_new-1,
+ * placed as one set on their own (R6) with the request's gen.  out[0..n_new)
+ * receives their entries.  Return codes: 0 ok, -1 bad input, -4 request not
+ * placed, -3 no range large enough (nothing changes).
+ */
+int oracle_extend(opool *p, uint64_t request, uint32_t n_new, oracle_loc *out)
+{
+    if (!p || n_new == 0) return -1;
+    const int k = find_record(p, request);
+    if (k < 0) return -4;
+    orecord *r = &p->rec[k];
+    if ((uint64_t)r->n_blocks + n_new > 0xFFFFFFFFull) return -1;
+    const uint32_t N = p->n_dev;
+    uint64_t *base = (uint64_t *)realloc(r->base, (size_t)(r->n_sets + 1) * N * sizeof(uint64_t));
+    if (!base) return -1;
+    r->base = base;
+    uint64_t *len = (uint64_t *)realloc(r->len, (size_t)(r->n_sets + 1) * N * sizeof(uint64_t));
+    if (!len) return -1;
+    r->len = len;
+    oracle_loc *map = (oracle_loc *)realloc(r->map, (size_t)(r->n_blocks + n_new) * sizeof(oracle_loc));
+    if (!map) return -1;
+    r->map = map;
+    const int rc = place_set(p, n_new, r->gen, out, r->base + (size_t)r->n_sets * N, r->len + (size_t)r->n_sets * N);
+    if (rc) return rc;
+    memcpy(r->map + r->n_blocks, out, n_new * sizeof(oracle_loc));
+    r->n_blocks += n_new;
+    r->n_sets += 1;
     return 0;
 }
 
@@ -321,8 +384,11 @@ int oracle_release(opool *p, uint64_t request)
     int k = find_record(p, request);
     if (k < 0) return -4;
     orecord *r = &p->rec[k];
-    for (uint32_t i = 0; i < p->n_dev; ++i)
-        if (r->len[i]) give_back(&p->free[i], r->base[i], r->len[i]);
+    for (uint32_t set = 0; set < r->n_sets; ++set)
+        for (uint32_t i = 0; i < p->n_dev; ++i) {
+            const size_t at = (size_t)set * p->n_dev + i;
+            if (r->len[at]) give_back(&p->free[i], r->base[at], r->len[at]);
+        }
     free(r->map);
     free(r->base);
     free(r->len);
