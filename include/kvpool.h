@@ -140,6 +140,24 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths,
 int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
 
 /*
+ * Extend a placed request by its next n_new blocks (Sec. 4.1.3: the KV
+ * caches offloaded at each decoding step form an offload set of their own,
+ * and Algorithm 1 runs on that set).  Blocks n_old .. n_old+n_new-1 are
+ * placed exactly as kv_pool_place places a request of n_new blocks on the
+ * pool as it stands -- Eq. 2 counts of the set, the same block order, one
+ * new contiguous range per region with a share -- while earlier blocks keep
+ * their places.  Every entry carries the request's gen, so earlier maps stay
+ * valid; kv_pool_lookup, kv_pool_retrieve_request and kv_pool_release then
+ * cover all n_old + n_new blocks.  Small sets follow Eq. 2 literally: a
+ * one-block set goes to the region with the largest p_i (lowest index on
+ * ties).
+ *   map_out[n_new]    caller-owned, receives the new blocks' entries.
+ * Atomic: on KVP_ERR_NOSPACE nothing changes.  Errors: INVALID (n_new == 0,
+ * more than 2^32-1 blocks in all), NOTFOUND, NOSPACE.
+ */
+int kv_pool_extend(kvp_pool *pool, uint64_t request_id, uint32_t n_new, kvp_loc *map_out);
+
+/*
  * GLT read (Sec. 4.3, the lookup that starts a retrieval): the map of a placed
  * request.  n_blocks must equal the placed count.  Errors: NOTFOUND, INVALID.
  */

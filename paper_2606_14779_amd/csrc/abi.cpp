@@ -11,6 +11,7 @@ namespace kvp {
 Pool *pool_create(const kvp_region_desc *, const uint64_t *, uint32_t, const kvp_kv_spec *, int);
 void pool_destroy(Pool *);
 void pool_place(Pool &, uint64_t, uint32_t, kvp_loc *);
+void pool_extend(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_lookup(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_lookup_vector(Pool &, uint64_t, uint32_t, std::vector<kvp_loc> &);
 void pool_release(Pool &, uint64_t);
@@ -86,6 +87,11 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, u
 int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out)
 {
     return guarded([&] { kvp::pool_place(impl(pool), request_id, n_blocks, map_out); });
+}
+
+int kv_pool_extend(kvp_pool *pool, uint64_t request_id, uint32_t n_new, kvp_loc *map_out)
+{
+    return guarded([&] { kvp::pool_extend(impl(pool), request_id, n_new, map_out); });
 }
 
 int kv_pool_lookup(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out)

@@ -7,6 +7,7 @@
 #include <map>
 #include <memory>
 #include <mutex>
+#include <deque>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -114,9 +115,9 @@ struct Allocation {       // one contiguous range of one request in one region
 
 struct RequestRec {
     uint64_t id;
-    uint32_t n_blocks;
+    uint32_t n_blocks;              // over all offload sets (place, then each extend)
     uint32_t gen;
-    std::vector<Allocation> ranges;
+    std::deque<Allocation> ranges;  // one per (offload set, region); stable addresses
     hipEvent_t stored = nullptr;   // recorded after each store touching the request
     hipEvent_t busy = nullptr;     // recorded after each store / retrieve touching it
     bool stored_rec = false;

@@ -342,25 +342,63 @@ void pool_destroy(Pool *p)
 
 // ---------------------------------------------------------------- place / lookup / release
 
+namespace {
+
+// One offload set (Alg. 1 on the blocks of one place or extend call; the
+// KV caches of one decoding step in Sec. 4.1.3): Eq. 2 counts for the set,
+// and per region with a share one contiguous, sector-rounded range (Sec. 4.2),
+// found first fit.  reserve() finds them all and changes nothing, so a
+// failure leaves the pool as it was; commit() takes them.
+struct SetPlan {
+    std::vector<uint64_t> counts, base, len;
+};
+
+SetPlan reserve_set(Pool &p, uint32_t n)
+{
+    const uint32_t N = static_cast<uint32_t>(p.regions.size());
+    SetPlan s{std::vector<uint64_t>(N), std::vector<uint64_t>(N, 0), std::vector<uint64_t>(N, 0)};
+    target_counts(p.bandwidth.data(), N, n, s.counts.data());
+    for (uint32_t i = 0; i < N; ++i) {
+        s.len[i] = round_up(s.counts[i] * p.block_bytes, kSector);
+        if (s.len[i] && !p.regions[i].alloc.first_fit(s.len[i], &s.base[i]))
+            fail(KVP_ERR_NOSPACE, "region " + std::to_string(i) + " has no free range of " + std::to_string(s.len[i]) +
+                                      " bytes");
+    }
+    return s;
+}
+
+// Take the planned ranges for blocks first .. first+n-1 of rec, stripe the
+// blocks over them (R3) and record their GLT entries.
+void commit_set(Pool &p, RequestRec &rec, const SetPlan &s, uint32_t first, uint32_t n, kvp_loc *out)
+{
+    const uint32_t N = static_cast<uint32_t>(p.regions.size());
+    for (uint32_t i = 0; i < N; ++i) {
+        if (!s.len[i]) continue;
+        p.regions[i].alloc.take(s.base[i], s.len[i]);
+        rec.ranges.push_back(Allocation{&rec, i, rec.gen, s.base[i], s.counts[i], s.len[i]});
+        p.regions[i].live[s.base[i]] = &rec.ranges.back();
+    }
+    std::vector<uint32_t> region_of;
+    stripe(s.counts, n, region_of);
+    std::vector<uint64_t> next(N, 0);
+    for (uint32_t j = 0; j < n; ++j) {
+        const uint32_t r = region_of[j];
+        const uint64_t off = s.base[r] + next[r]++ * p.block_bytes;
+        out[j] = kvp_loc{r, rec.gen, off};
+        p.glt.insert(GltEntry{rec.id, first + j, r, p.regions[r].desc.type, rec.gen, off});
+    }
+    rec.n_blocks = first + n;
+}
+
+}  // namespace
+
 void pool_place(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
 {
     if (n_blocks == 0) fail(KVP_ERR_INVALID, "n_blocks must be positive");
     if (!out) fail(KVP_ERR_INVALID, "map_out is null");
     std::lock_guard<std::mutex> lock(p.mu);
     if (p.requests.count(request)) fail(KVP_ERR_INVALID, "request " + std::to_string(request) + " is already placed");
-    const uint32_t N = static_cast<uint32_t>(p.regions.size());
-    std::vector<uint64_t> counts(N);
-    target_counts(p.bandwidth.data(), N, n_blocks, counts.data());
-
-    // one contiguous, sector-rounded range per region with a nonzero share;
-    // find them all before taking any, so a failure changes nothing
-    std::vector<uint64_t> base(N, 0), len(N, 0);
-    for (uint32_t i = 0; i < N; ++i) {
-        len[i] = round_up(counts[i] * p.block_bytes, kSector);
-        if (len[i] && !p.regions[i].alloc.first_fit(len[i], &base[i]))
-            fail(KVP_ERR_NOSPACE, "region " + std::to_string(i) + " has no free range of " + std::to_string(len[i]) +
-                                      " bytes");
-    }
+    const SetPlan plan = reserve_set(p, n_blocks);
 
     auto rec = std::make_unique<RequestRec>();
     if (!p.placement_only) {
@@ -373,26 +411,22 @@ void pool_place(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
         }
     }
     rec->id = request;
-    rec->n_blocks = n_blocks;
     rec->gen = p.next_gen++;
-    rec->ranges.reserve(N);
-    for (uint32_t i = 0; i < N; ++i) {
-        if (!len[i]) continue;
-        p.regions[i].alloc.take(base[i], len[i]);
-        rec->ranges.push_back(Allocation{rec.get(), i, rec->gen, base[i], counts[i], len[i]});
-    }
-    for (auto &a : rec->ranges) p.regions[a.region].live[a.base] = &a;
-
-    std::vector<uint32_t> region_of;
-    stripe(counts, n_blocks, region_of);
-    std::vector<uint64_t> next(N, 0);
-    for (uint32_t j = 0; j < n_blocks; ++j) {
-        const uint32_t r = region_of[j];
-        const uint64_t off = base[r] + next[r]++ * p.block_bytes;
-        out[j] = kvp_loc{r, rec->gen, off};
-        p.glt.insert(GltEntry{request, j, r, p.regions[r].desc.type, rec->gen, off});
-    }
+    commit_set(p, *rec, plan, 0, n_blocks, out);
     p.requests.emplace(request, std::move(rec));
+}
+
+void pool_extend(Pool &p, uint64_t request, uint32_t n_new, kvp_loc *out)
+{
+    if (n_new == 0) fail(KVP_ERR_INVALID, "n_new must be positive");
+    if (!out) fail(KVP_ERR_INVALID, "map_out is null");
+    std::lock_guard<std::mutex> lock(p.mu);
+    auto it = p.requests.find(request);
+    if (it == p.requests.end()) fail(KVP_ERR_NOTFOUND, "request " + std::to_string(request) + " is not placed");
+    RequestRec &rec = *it->second;
+    if (static_cast<uint64_t>(rec.n_blocks) + n_new > 0xFFFFFFFFull) fail(KVP_ERR_INVALID, "request too large");
+    const SetPlan plan = reserve_set(p, n_new);
+    commit_set(p, rec, plan, rec.n_blocks, n_new, out);
 }
 
 namespace {

@@ -85,6 +85,7 @@ _u32, _u64, _i32, _vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, ctypes.c
 _SIGS = {
     "kv_pool_create": (_i32, [_vp, _vp, _u32, _vp, _i32, _vp]),
     "kv_pool_place": (_i32, [_vp, _u64, _u32, _vp]),
+    "kv_pool_extend": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_lookup": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_store": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
@@ -243,6 +244,12 @@ class KVPool:
         out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
         _check(_lib.kv_pool_place(self._h, request, n_blocks, out.ctypes.data))
         return out[:n_blocks]
+
+    def extend(self, request: int, n_new: int) -> np.ndarray:
+        """Entries of the request's next n_new blocks, placed as an offload set of their own."""
+        out = np.zeros(max(n_new, 1), dtype=LOC_DTYPE)
+        _check(_lib.kv_pool_extend(self._h, request, n_new, out.ctypes.data))
+        return out[:n_new]
 
     def lookup(self, request: int, n_blocks: int) -> np.ndarray:
         out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)

@@ -121,6 +121,20 @@ int main()
     HIPTRY(hipStreamSynchronize(stream));
     if (check()) return 1;
     TRY(kv_pool_release(pool, 42));
+
+    // a request extended by two more offload sets: lookup returns the three maps in order
+    std::vector<kvp_loc> a(5), b(1), c(3), all(9);
+    TRY(kv_pool_place(pool, 77, 5, a.data()));
+    TRY(kv_pool_extend(pool, 77, 1, b.data()));
+    TRY(kv_pool_extend(pool, 77, 3, c.data()));
+    TRY(kv_pool_lookup(pool, 77, 9, all.data()));
+    std::vector<kvp_loc> cat(a);
+    cat.insert(cat.end(), b.begin(), b.end());
+    cat.insert(cat.end(), c.begin(), c.end());
+    for (uint32_t i = 0; i < 9; ++i)
+        bad += all[i].region != cat[i].region || all[i].gen != cat[i].gen || all[i].offset != cat[i].offset;
+    if (kv_pool_extend(pool, 78, 1, b.data()) != KVP_ERR_NOTFOUND) ++bad;
+    TRY(kv_pool_release(pool, 77));
     kv_pool_destroy(pool);
     HIPTRY(hipStreamDestroy(stream));
     for (void *p : src) HIPTRY(hipFree(p));

@@ -625,3 +625,65 @@ def test_store_batch_and_retrieve_into_very_many_slots():
         check_full(wl, run, host)
     finally:
         run.close()
+
+
+@pytest.mark.parametrize("upload", [False, True])
+@pytest.mark.parametrize("layout", [0, 1])
+def test_extended_request_round_trip(layout, upload):
+    """A request placed, then extended three times (an offload set per decoding step); each set is
+    stored as it arrives and the whole request is retrieved by id.  Maps, pool bytes and destination
+    against the oracle carrying the same place / extend history."""
+    import dataclasses
+
+    import oracle
+    sizes = [23, 1, 5, 11]
+    n = sum(sizes)
+    base = workloads.make(2, max_blocks=n, layout=layout)
+    regions = [dataclasses.replace(r) for r in base.regions]
+    workloads._size_regions(regions, [n, n], base.shape.block_bytes)    # room for several sets
+    q = base.requests[0]
+    wl = workloads.Workload(2, base.name + "-ext", base.seed, base.shape, layout, regions, [q],
+                            base.src_num_slots, base.dst_num_slots)
+    say("case extend", layout, upload, sizes)
+    run = make_run(wl)
+    try:
+        if upload:
+            run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, 0, K.LAUNCH_NT_STORE | K.LAUNCH_UPLOAD)
+            run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, (K.LAUNCH_LDS if layout else 0) | K.LAUNCH_UPLOAD)
+        host = run.fill_source(keep_host=True)
+        run.fill_dst()
+        sh = wl.shape
+        L = sh.layers
+        ora = oracle.Pool([r.weight for r in regions], [r.capacity_bytes for r in regions], sh.block_bytes)
+        kp_s, vp_s = run.layer_ptrs(run.src)
+        s = torch.cuda.current_stream().cuda_stream
+        sets, first = [], 0
+        for k, m in enumerate(sizes):
+            lm = run.pool.place(q.request_id, m) if k == 0 else run.pool.extend(q.request_id, m)
+            om = ora.place(q.request_id, m) if k == 0 else ora.extend(q.request_id, m)
+            assert np.array_equal(lm.view(np.uint8), om.view(np.uint8)), "set %d placed differently" % k
+            run.pool.store(lm, q.src_slots[first:first + m], wl.src_num_slots, kp_s, vp_s, s)
+            sets.append(om)
+            first += m
+        whole = np.concatenate(sets)
+        assert np.array_equal(run.pool.lookup(q.request_id, n), whole)
+        kp, vp = run.layer_ptrs(run.dst)
+        run.pool.retrieve_request(q.request_id, q.dst_slots, wl.dst_num_slots, kp, vp, s)
+        torch.cuda.synchronize()
+        shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
+        oregions = [np.zeros(r.capacity_bytes, np.uint8) for r in regions]
+        oracle.store(whole, q.src_slots, oregions, [host[l, 0] for l in range(L)], [host[l, 1] for l in range(L)],
+                     shape, layout)
+        expect = np.full(tuple(run.dst.shape), SENTINEL, np.uint16)
+        oracle.gather(whole, q.dst_slots, oregions, [expect[l, 0] for l in range(L)],
+                      [expect[l, 1] for l in range(L)], shape, layout)
+        for r in range(len(regions)):
+            offs = whole["offset"][whole["region"] == r]
+            if len(offs):
+                lo, hi = int(offs.min()), int(offs.max()) + sh.block_bytes
+                assert np.array_equal(run.pool.region_read(r, lo, hi - lo), oregions[r][lo:hi]), "region %d" % r
+        got = run.dst.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, expect)
+        run.pool.release(q.request_id)
+    finally:
+        run.close()

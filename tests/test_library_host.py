@@ -80,6 +80,67 @@ def test_placement_equals_oracle(weights, layers, ops):
     lib_pool.close()
 
 
+@settings(max_examples=60, deadline=None)
+@given(st.lists(st.integers(1, 9), min_size=1, max_size=6), st.integers(1, 3),
+       st.lists(st.tuples(st.sampled_from(["place", "extend", "extend", "release"]), st.integers(1, 60)),
+                min_size=1, max_size=40))
+def test_placement_with_extensions_equals_oracle(weights, layers, ops):
+    """Place, extend (the next offload set of a placed request) and release in random order: every
+    map, every full lookup and every refusal as the oracle's."""
+    bb = 2 * layers * 256
+    caps = [(w * 40 + 7) * bb + 3000 for w in weights]
+    lib_pool, _ = _pool(weights, caps, layers)
+    ora = oracle.Pool(weights, caps, bb)
+    live, req = {}, 100                           # request -> blocks placed so far
+    for op, n in ops:
+        if op == "release" and live:
+            r = sorted(live)[n % len(live)]
+            del live[r]
+            assert ora.release(r) == 0
+            lib_pool.release(r)
+        elif op == "extend" and live:
+            r = sorted(live)[n % len(live)]
+            rc, om = ora.try_extend(r, n)
+            if rc == 0:
+                lm = lib_pool.extend(r, n)
+                assert np.array_equal(lm.view(np.uint8), om.view(np.uint8))
+                live[r] += n
+            else:
+                with pytest.raises(K.KVPoolError) as ei:
+                    lib_pool.extend(r, n)
+                assert ei.value.code == rc == -3
+            assert np.array_equal(lib_pool.lookup(r, live[r]), ora.lookup(r, live[r]))
+        else:
+            rc, om = ora.try_place(req, n)
+            if rc == 0:
+                assert np.array_equal(lib_pool.place(req, n).view(np.uint8), om.view(np.uint8))
+                live[req] = n
+            else:
+                with pytest.raises(K.KVPoolError) as ei:
+                    lib_pool.place(req, n)
+                assert ei.value.code == rc == -3
+            req += 1
+    lib_pool.close()
+
+
+def test_extend_errors():
+    p, spec = _pool([2, 1], [8 * 4096, 4 * 4096], bb_layers=8)  # one block = one 4096-byte sector
+    assert spec.block_bytes == 4096
+    m = p.place(1, 6)
+    assert _err(p.extend, 2, 3) == "NOTFOUND"
+    assert _err(p.extend, 1, 0) == "INVALID"
+    assert _err(p.extend, 1, 9) == "NOSPACE"                    # device 0 has room for 4 more only
+    assert np.array_equal(p.lookup(1, 6), m)                     # nothing changed
+    e = p.extend(1, 3)
+    assert list(e["region"]) == [0, 1, 0] and set(e["gen"].tolist()) == {int(m["gen"][0])}
+    assert np.array_equal(p.lookup(1, 9), np.concatenate([m, e]))
+    assert _err(p.lookup, 1, 6) == "INVALID"                      # the count is now 9
+    p.release(1)
+    assert _err(p.extend, 1, 1) == "NOTFOUND"
+    assert p.place(2, 12) is not None                            # every range came back
+    p.close()
+
+
 def test_workload_scale_placement_equals_oracle():
     from kvgen import workloads
     for cfg in (1, 2, 3, 4, 5):
