@@ -176,6 +176,7 @@ struct Pool {
     hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's);
                                        // with KVP_LAUNCH_SDMA the host-link copies' stream instead
     hipEvent_t fork = nullptr, stage_done = nullptr;
+    hipEvent_t uploaded = nullptr;     // a call's work list is in device memory (s_stage)
     // host link, per direction [op]: the last host-class kernel enqueued; the
     // next one (any stream) waits for it, so calls take the link in turn
     hipEvent_t link_done[2] = {nullptr, nullptr};

@@ -187,7 +187,7 @@ void release_gpu(Pool &p)
         if (kv.second->stored) (void)hipEventDestroy(kv.second->stored);
         if (kv.second->busy) (void)hipEventDestroy(kv.second->busy);
     }
-    hipEvent_t *evs[] = {&p.fork, &p.stage_done, &p.link_done[0], &p.link_done[1]};
+    hipEvent_t *evs[] = {&p.fork, &p.stage_done, &p.uploaded, &p.link_done[0], &p.link_done[1]};
     for (auto e : evs)
         if (*e) (void)hipEventDestroy(*e), *e = nullptr;
     for (auto &tc : p.timed)
@@ -310,6 +310,7 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         for (auto &r : p->regions) alloc_region(r);
         check_hip(hipStreamCreateWithFlags(&p->s_stage, hipStreamNonBlocking), "hipStreamCreate");
         check_hip(hipEventCreateWithFlags(&p->fork, hipEventDisableTiming), "hipEventCreate");
+        check_hip(hipEventCreateWithFlags(&p->uploaded, hipEventDisableTiming), "hipEventCreate");
         check_hip(hipEventCreateWithFlags(&p->stage_done, hipEventDisableTiming), "hipEventCreate");
         for (auto &e : p->link_done) check_hip(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate");
         p->ring.resize(kRingSlots);

@@ -350,8 +350,16 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::copy(items[0].begin(), items[0].end(), list);
     std::copy(items[1].begin(), items[1].end(), list + items[0].size());
 
-    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
+    // The upload goes on the pool's stream, which runs it as soon as the
+    // previous call's staging kernel there is done -- typically while that
+    // call's host-link kernel still runs -- rather than in line on the
+    // caller's stream between two host-link kernels, where it left the link
+    // idle for about 70 us per call.  The slot is free on the device: it was
+    // reclaimed only after the last call that read it.
+    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, p.s_stage), "hipMemcpyAsync");
     slot.pending = true;  // from here on the slot is in use even if a launch fails
+    check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
+    check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
     if (fork_staging || !batches.empty()) check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
 
     const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
