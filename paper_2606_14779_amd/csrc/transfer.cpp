@@ -350,16 +350,31 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::copy(items[0].begin(), items[0].end(), list);
     std::copy(items[1].begin(), items[1].end(), list + items[0].size());
 
-    // The upload goes on the pool's stream, which runs it as soon as the
-    // previous call's staging kernel there is done -- typically while that
-    // call's host-link kernel still runs -- rather than in line on the
-    // caller's stream between two host-link kernels, where it left the link
-    // idle for about 70 us per call.  The slot is free on the device: it was
-    // reclaimed only after the last call that read it.
-    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, p.s_stage), "hipMemcpyAsync");
+    // With earlier work still running on the caller's stream (calls issued
+    // back to back, e.g. one per layer), the upload goes on the pool's stream:
+    // it is done while the previous call's host-link kernel still runs, where
+    // in line it would leave the link idle between the two kernels (74 us per
+    // layer call, against 36.5 us).  On an idle caller stream it stays in
+    // line, which costs less host time (9.5 against 26 us per call: the wait
+    // on a pending event from another stream is what costs).  The slot is free
+    // on the device: it was reclaimed only after the last call that read it.
+    bool ahead = false;
+    if (hipPeekAtLastError() == hipSuccess) {   // never clear an error the caller has yet to read
+        const hipError_t q = hipStreamQuery(s);
+        if (q == hipErrorNotReady) {
+            (void)hipGetLastError();   // "not ready" is the answer, not an error to leave behind
+            ahead = true;
+        } else {
+            check_hip(q, "hipStreamQuery");
+        }
+    }
+    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, ahead ? p.s_stage : s),
+              "hipMemcpyAsync");
     slot.pending = true;  // from here on the slot is in use even if a launch fails
-    check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
-    check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
+    if (ahead) {
+        check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
+        check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
+    }
     if (fork_staging || !batches.empty()) check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
 
     const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
