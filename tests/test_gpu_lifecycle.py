@@ -2,9 +2,10 @@
 
 Requests are placed, stored, retrieved and released in random order, on
 three streams with no host synchronisation between the operations of a
-round; released ranges are placed again; the host-class transport is
-switched between the zero-copy kernel and the copy engines along the way,
-and small calls between their one-launch form and the upload path.
+round; released ranges are placed again; placed requests grow by further
+offload sets (kv_pool_extend); the host-class transport is switched between
+the zero-copy kernel and the copy engines along the way, and small calls
+between their one-launch form and the upload path.
 Checked against what placement and the round trip fix:
 
 - every map equals the oracle's, the oracle pool carrying the same place /
@@ -50,6 +51,7 @@ def _need_gpu():
 def test_random_lifecycle(layout):
     rng = np.random.default_rng(SEED + layout)
     path_rng = np.random.default_rng(SEED + 17 + layout)   # upload bit: apart, so rng's sequence is unchanged
+    ext_rng = np.random.default_rng(SEED + 29 + layout)    # extensions: apart as well
     shape = workloads.KVShape("lifecycle", L, H, D)
     bb = shape.block_bytes
     weights = [3, 1, 2, 2]
@@ -73,7 +75,7 @@ def test_random_lifecycle(layout):
     live = {}                              # request -> dict(n, map, src, vals, stored)
     next_req = 1
     sdma = {K.OP_RETRIEVE: False, K.OP_STORE: False}
-    counts = dict(place=0, nospace=0, store=0, retrieve=0, release=0, toggle=0)
+    counts = dict(place=0, nospace=0, store=0, retrieve=0, release=0, toggle=0, extend=0)
     try:
         for rnd in range(12):
             for s in streams:
@@ -148,7 +150,7 @@ def test_random_lifecycle(layout):
                     free_src.extend(int(x) for x in live[r]["src"])
                     del live[r]
                     counts["release"] += 1
-                else:
+                elif op == "toggle":
                     o = int(rng.integers(2))
                     sdma[o] = not sdma[o]
                     # back to the library's defaults for the zero-copy kernel
@@ -156,6 +158,31 @@ def test_random_lifecycle(layout):
                     upload = K.LAUNCH_UPLOAD if path_rng.random() < 0.5 else 0
                     pool.set_launch(K.CLASS_HOST, o, 0, (K.LAUNCH_SDMA if sdma[o] else default) | upload)
                     counts["toggle"] += 1
+                if live and ext_rng.random() < 0.2:
+                    # the next offload set of a live request: new blocks, their own ranges
+                    r = int(ext_rng.choice(sorted(live)))
+                    q = live[r]
+                    m = int(ext_rng.integers(1, 13))
+                    if len(free_src) >= m:
+                        rc, om = ora.try_extend(r, m)
+                        if rc != 0:
+                            with pytest.raises(K.KVPoolError):
+                                pool.extend(r, m)
+                        else:
+                            em = pool.extend(r, m)
+                            assert np.array_equal(em.view(np.uint8), om.view(np.uint8)), "extension differs"
+                            slots = np.array([free_src.pop() for _ in range(m)], np.int64)
+                            vals = np.stack([kvgen.block_values(SEED, r, b, L, H, BS, D)
+                                             for b in range(q["n"], q["n"] + m)], 2)
+                            src[:, :, torch.from_numpy(slots).to(dev)] = torch.from_numpy(vals.view(np.int16)).to(dev)
+                            for s_ in streams:
+                                s_.wait_stream(torch.cuda.current_stream())
+                            q["map"] = np.concatenate([q["map"], em])
+                            q["src"] = np.concatenate([q["src"], slots.astype(np.int32)])
+                            q["vals"] = np.concatenate([q["vals"], vals], 2)
+                            q["n"] += m
+                            q["stored"] = False          # the new blocks hold nothing until stored
+                            counts["extend"] += 1
             torch.cuda.synchronize()
             got = dst.cpu().numpy().view(np.uint16)
             if not np.array_equal(got, expect):
@@ -163,7 +190,7 @@ def test_random_lifecycle(layout):
                 raise AssertionError("round %d: %d elements differ, first %s" % (rnd, len(bad), bad[:4].tolist()))
         say("lifecycle", layout, counts)
         assert counts["retrieve"] >= 10 and counts["release"] >= 5 and counts["toggle"] >= 3
-        assert counts["nospace"] >= 1
+        assert counts["nospace"] >= 1 and counts["extend"] >= 5
     finally:
         torch.cuda.synchronize()
         pool.close()
