@@ -721,8 +721,12 @@ def main():
         log("cpu baseline done")
 
     dominant_ms = host_avg if host_blocks else stage_avg
+    # per launch: a step of a multi-request workload launches one kernel of each class per request,
+    # so the algorithmic bytes of an average launch are the step's bytes over its launches
+    host_per_launch = host_bytes * args.steps / summ["host_calls"] if summ["host_calls"] else host_bytes
+    stage_per_launch = stage_bytes * args.steps / summ["staging_calls"] if summ["staging_calls"] else stage_bytes
     if host_blocks:
-        achieved = host_bytes / (dominant_ms / 1e3) / 1e9
+        achieved = host_per_launch / (dominant_ms / 1e3) / 1e9
         tr = pmc_traffic(wl.name, "host_region_copy<true, 0,")
         roof = {"bound": "pcie", "kernel": "host_region_copy (zero-copy gather from pinned host regions)"
                 if not args.sdma else "host class by copy engines (hipMemcpy into an HBM ring) + HBM ring scatter",
@@ -730,13 +734,14 @@ def main():
                 "frac": round(achieved / PCIE5_X16_GBPS, 4),
                 "traffic": round(tr["fetch_bytes"] + tr["write_bytes"]) if tr else None,
                 "traffic_detail": {"fetch_bytes": round(tr["fetch_bytes"]), "write_bytes": round(tr["write_bytes"]),
-                                   "algorithmic_read_bytes": host_bytes, "algorithmic_write_bytes": host_bytes,
+                                   "algorithmic_read_bytes": host_per_launch, "algorithmic_write_bytes": host_per_launch,
                                    "source": "profiles/retrieve_%s_pmc.txt" % wl.name} if tr else None,
-                "bytes_per_launch": host_bytes,
+                "bytes_per_launch": round(host_per_launch),
+                "launches_per_step": round(summ["host_calls"] / args.steps, 3),
                 "measured_peak": pr["host_link_peak_gbps"] if pr else None,
                 "frac_measured": round(achieved / pr["host_link_peak_gbps"], 4) if pr else None}
     else:
-        achieved = 2 * stage_bytes / (dominant_ms / 1e3) / 1e9
+        achieved = 2 * stage_per_launch / (dominant_ms / 1e3) / 1e9
         roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather)", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None}
     hbm_roof = None
