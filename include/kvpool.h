@@ -355,9 +355,9 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
  * kernel's.
  *
  * Small calls: when a store or retrieve moves no bytes through the
- * copy-engine ring, has under 32 MiB of staging-class bytes, is not timed,
- * and its work list -- 2 * (layers moved) engine pointers plus two 8-byte
- * words per present block -- fits in 384 words (3 KiB), that list travels
+ * copy-engine ring, is not timed, and its work list -- 2 * (layers moved)
+ * engine pointers plus two 8-byte words per present block -- fits in 384
+ * words (3 KiB), that list travels
  * in the kernel arguments and both classes run in ONE launch: workgroups up
  * to each class's grid (capped at its units), the copy form of the host
  * class's flags (of the staging class's when no host-class block is moved),

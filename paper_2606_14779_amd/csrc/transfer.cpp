@@ -321,7 +321,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             check_hip(q, "hipEventQuery");
         }
     }
-    if (batches.empty() && !fork_staging && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
+    if (batches.empty() && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
         chunks + 2 * n_items <= kInlineWords) {
         // Small call: table and items in the kernel arguments, both classes in
         // one launch in the host class's copy form (the link-bound part; the
