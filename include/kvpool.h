@@ -159,7 +159,9 @@ int kv_pool_extend(kvp_pool *pool, uint64_t request_id, uint32_t n_new, kvp_loc 
 
 /*
  * GLT read (Sec. 4.3, the lookup that starts a retrieval): the map of a placed
- * request.  n_blocks must equal the placed count.  Errors: NOTFOUND, INVALID.
+ * request.  n_blocks must equal its block count over all its offload sets
+ * (kv_pool_place, then each kv_pool_extend), whose maps it returns in that
+ * order.  Errors: NOTFOUND, INVALID.
  */
 int kv_pool_lookup(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
 
@@ -187,10 +189,12 @@ int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
  * Retrieve (Sec. 4.3, "KV Retrieval"): group the present entries by region
  * type, then read the host regions (zero-copy kernel, on `stream`) and the
  * staging regions (HBM gather kernel, on the pool's internal stream forked
- * from `stream` and joined back into it) in parallel -- a call with under
- * 32 MiB of staging-region bytes runs its HBM kernel on `stream` ahead of the
- * host-region kernel instead, since forking costs more; every chunk lands in slot
- * dst_block_table[b] of layer l's K or V buffer in the engine layout.
+ * from `stream` and joined back into it) in parallel.  A small call (see
+ * kv_pool_set_launch) runs both in one launch on `stream`; otherwise a call
+ * with under 32 MiB of staging-region bytes runs its HBM kernel on `stream`
+ * ahead of the host-region kernel, since forking costs more.  Every chunk
+ * lands in slot dst_block_table[b] of layer l's K or V buffer in the engine
+ * layout.
  * Absent entries are skipped and every slot not named by a present entry is
  * left untouched.  Entries may belong to several requests: a batch retrieved
  * by one call shares one work list and one kernel per region class.
@@ -207,7 +211,8 @@ int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
 /*
  * Retrieve by request (Sec. 4.3 as one call): read the GLT entries of blocks
  * 0..n_blocks-1 of request_id, then retrieve them exactly as kv_pool_retrieve
- * does with that map.  n_blocks must equal the placed count.
+ * does with that map.  n_blocks must equal the request's block count over
+ * all its offload sets.
  *   dst_block_table[n_blocks]  destination slot of every block.
  * Errors: NOTFOUND, INVALID, HIP.
  */
