@@ -253,7 +253,8 @@ uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
     if (cls == KVP_CLASS_HOST && op == KVP_OP_STORE) f |= KVP_LAUNCH_NT_STORE;
     // token-major pools stage each chunk through LDS (contiguous on both
     // sides), except the host-class store: there the direct conversion keeps
-    // the host-link side contiguous and measured faster (207 vs 211 ms)
+    // the host-link side contiguous and measured faster (16 workgroups:
+    // 207.4-208.7 ms against 210.6-211.9 through LDS)
     if (spec.pool_layout == 1 && !(cls == KVP_CLASS_HOST && op == KVP_OP_STORE)) f |= KVP_LAUNCH_LDS;
     // plain HBM retrieve: half-chunk units (the copy shape that measured best)
     if (spec.pool_layout == 0 && cls == KVP_CLASS_STAGING && op == KVP_OP_RETRIEVE) f |= KVP_LAUNCH_SPLIT2;
