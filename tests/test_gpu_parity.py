@@ -687,3 +687,31 @@ def test_extended_request_round_trip(layout, upload):
         run.pool.release(q.request_id)
     finally:
         run.close()
+
+
+@pytest.mark.parametrize("two_streams", [False, True])
+def test_back_to_back_upload_calls(two_streams):
+    """One call per layer for 300 blocks -- too many for the kernel arguments, so every call uploads
+    its work list -- issued back to back: from the second call on the caller's stream is still
+    busy and the upload goes ahead on the pool's stream.  Against the oracle."""
+    wl = workloads.make(2, max_blocks=300)
+    say("case back-to-back uploads", two_streams)
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        m = run.retrieve_maps[q.request_id]
+        cur = torch.cuda.current_stream()
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()] if two_streams else [cur]
+        for s_ in streams:
+            s_.wait_stream(cur)
+        for l in range(wl.shape.layers):
+            run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, l, l + 1, kp, vp,
+                                     streams[l % len(streams)].cuda_stream)
+        for s_ in streams:
+            cur.wait_stream(s_)
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
