@@ -412,6 +412,54 @@ def latency(args):
     run.close()
 
 
+def decode(args):
+    """Offload during decoding (Sec. 4.1.3: the KV caches of each decoding step form an offload set):
+    the 128K request is placed and stored, then grows one block at a time -- kv_pool_extend by one
+    block and kv_pool_store of that block, synchronised after each -- as an engine offloading every
+    16 generated tokens would.  Reports host and call-to-complete time per step and where the new
+    blocks land (Eq. 2 sends every one-block set to the region with the largest weight)."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    base = workloads.make(3)
+    n_steps = 256
+    regions = [dataclasses.replace(r) for r in base.regions]
+    workloads._size_regions(regions, [base.requests[0].n_present, 3 * n_steps], base.shape.block_bytes)
+    wl = dataclasses.replace(base, regions=regions)
+    run = WorkloadRun(wl, device=0)
+    run.setup()
+    q = wl.requests[0]
+    kp, vp = run.layer_ptrs(run.src)
+    cur = torch.cuda.current_stream()
+    host_us, total_us, landed = [], [], []
+    for i in range(n_steps):
+        slot = np.array([q.src_slots[i % q.n_present]], np.int32)    # the new block's values: any source slot
+        t = time.perf_counter()
+        m = run.pool.extend(q.request_id, 1)
+        run.pool.store(m, slot, wl.src_num_slots, kp, vp, cur.cuda_stream)
+        th = time.perf_counter()
+        torch.cuda.synchronize()
+        host_us.append((th - t) * 1e6)
+        total_us.append((time.perf_counter() - t) * 1e6)
+        landed.append(int(m["region"][0]))
+    counts = np.bincount(landed, minlength=len(regions))
+    out = {"metric": "per-step offload while decoding: extend by one block + store it (call to complete)",
+           "workload": wl.name, "steps": n_steps, "block_bytes": wl.shape.block_bytes,
+           "host_us_median": round(statistics.median(host_us[8:]), 1),
+           "call_to_complete_us_median": round(statistics.median(total_us[8:]), 1),
+           "call_to_complete_us_p99": round(float(np.percentile(total_us[8:], 99)), 1),
+           "blocks_per_region": counts.tolist(),
+           "request_blocks_after": q.n_present + n_steps}
+    print(json.dumps(out), flush=True)
+    run.close()
+
+
 def duplex(args):
     """The host link is full duplex: store (offload) one 128K LLaMA-shaped request while another is
     retrieved, on two streams, against each alone.  Two requests are placed in one pool with the
@@ -507,6 +555,8 @@ def main():
                     help="workload 3 with this many tokens instead of 128K (e.g. 524288)")
     ap.add_argument("--batch", action="store_true",
                     help="retrieve all requests of the workload in one call (concatenated maps) per step")
+    ap.add_argument("--decode", action="store_true",
+                    help="instead of the bench line, time per-step offload (extend by one block + store)")
     ap.add_argument("--duplex", action="store_true",
                     help="instead of the bench line, store one request while retrieving another")
     ap.add_argument("--latency", action="store_true",
@@ -535,6 +585,9 @@ def main():
         return
     if args.gpus == 1 and args.duplex:
         duplex(args)
+        return
+    if args.gpus == 1 and args.decode:
+        decode(args)
         return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the retrieval path has no cross-GPU step; "

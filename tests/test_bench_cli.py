@@ -28,7 +28,7 @@ def test_help_lists_every_mode():
     for flag in ("--gpus", "--steps", "--warmup", "--config", "--layout", "--sdma", "--copy-ring-mib", "--flush",
                  "--pipeline", "--latency", "--duplex", "--ablation", "--layerwise", "--no-cpu-baseline",
                  "--no-probes", "--no-copy-engine", "--host-grid", "--staging-grid", "--store-grid", "--stand-in",
-                 "--batch", "--context", "--upload", "--store-flags"):
+                 "--batch", "--context", "--upload", "--store-flags", "--decode"):
         assert flag in r.stdout, flag
 
 
