@@ -627,12 +627,13 @@ def test_store_batch_and_retrieve_into_very_many_slots():
         run.close()
 
 
-@pytest.mark.parametrize("upload", [False, True])
+@pytest.mark.parametrize("transport", ["small", "upload", "sdma"])
 @pytest.mark.parametrize("layout", [0, 1])
-def test_extended_request_round_trip(layout, upload):
+def test_extended_request_round_trip(layout, transport):
     """A request placed, then extended three times (an offload set per decoding step); each set is
     stored as it arrives and the whole request is retrieved by id.  Maps, pool bytes and destination
-    against the oracle carrying the same place / extend history."""
+    against the oracle carrying the same place / extend history.  With the copy engines, each
+    region holds the request in several ranges, so its blocks cross the link in several runs."""
     import dataclasses
 
     import oracle
@@ -644,12 +645,16 @@ def test_extended_request_round_trip(layout, upload):
     q = base.requests[0]
     wl = workloads.Workload(2, base.name + "-ext", base.seed, base.shape, layout, regions, [q],
                             base.src_num_slots, base.dst_num_slots)
-    say("case extend", layout, upload, sizes)
+    say("case extend", layout, transport, sizes)
     run = make_run(wl)
     try:
-        if upload:
+        if transport == "upload":
             run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, 0, K.LAUNCH_NT_STORE | K.LAUNCH_UPLOAD)
             run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, (K.LAUNCH_LDS if layout else 0) | K.LAUNCH_UPLOAD)
+        elif transport == "sdma":
+            run.pool.set_copy_ring(64 << 20)
+            for op in (K.OP_STORE, K.OP_RETRIEVE):
+                run.pool.set_launch(K.CLASS_HOST, op, 0, K.LAUNCH_SDMA)
         host = run.fill_source(keep_host=True)
         run.fill_dst()
         sh = wl.shape
