@@ -1,6 +1,7 @@
-"""The library's host data structures under AddressSanitizer and
-UndefinedBehaviorSanitizer (CPU only).  Builds tests/native/host_structures_fuzz.cpp
-with placement.cpp and glt.cpp and runs it."""
+"""The library's host code under AddressSanitizer and UndefinedBehaviorSanitizer
+(CPU only): tests/native/host_structures_fuzz.cpp built with placement.cpp,
+glt.cpp and bounce.cpp, and tests/native/placement_fuzz.cpp driving
+placement-only pools through the C ABI of the host-sanitized library."""
 import os
 import shutil
 import subprocess
@@ -23,6 +24,27 @@ def test_host_structures_under_asan_ubsan(tmp_path):
            "-o", exe]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all checks passed" in r.stdout
+
+
+SAN_LIB = os.path.join(ROOT, "tests", "abi_client", "asan", "libkvpool.so")
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_placement_through_the_abi_under_asan_ubsan(tmp_path):
+    """Random place / extend / release / lookup on placement-only pools, through the C ABI of the
+    host-sanitized library (built by the package build), with no GPU."""
+    if not os.path.exists(SAN_LIB):
+        pytest.skip("host-sanitized library not built (run the package build first)")
+    exe = str(tmp_path / "placement_fuzz")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "tests", "native", "placement_fuzz.cpp"),
+           "-o", exe, "-L", os.path.dirname(SAN_LIB), "-lkvpool", "-Wl,-rpath," + os.path.dirname(SAN_LIB),
+           "-L", os.path.join(ROCM, "lib"), "-Wl,-rpath-link," + os.path.join(ROCM, "lib")]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "all checks passed" in r.stdout
