@@ -112,3 +112,37 @@ def check_sampled(wl, run, n_sample=48, seed=0):
 def make_run(wl, **kw):
     run = WorkloadRun(wl, device=0, **kw)
     return run
+
+
+def tag_cache(L, S, H, bs, D):
+    """Source cache whose every 16-byte vector names itself: (slot, layer, K/V, head, token, vector,
+    0x5A5A, 0x0F0F) as eight 16-bit words, [L][2][S][H][bs][D]."""
+    nv = D // 8
+    t = np.zeros((L, 2, S, H, bs, nv, 8), np.int16)
+    t[..., 0] = np.arange(S, dtype=np.int16)[None, None, :, None, None, None]
+    t[..., 1] = np.arange(L, dtype=np.int16)[:, None, None, None, None, None]
+    t[..., 2] = np.arange(2, dtype=np.int16)[None, :, None, None, None, None]
+    t[..., 3] = np.arange(H, dtype=np.int16)[None, None, None, :, None, None]
+    t[..., 4] = np.arange(bs, dtype=np.int16)[None, None, None, None, :, None]
+    t[..., 5] = np.arange(nv, dtype=np.int16)[None, None, None, None, None, :]
+    t[..., 6] = 0x5A5A
+    t[..., 7] = 0x0F0F
+    return t.reshape(L, 2, S, H, bs, D)
+
+
+def check_tags(tags, dst, src_slots, dst_slots, sentinel):
+    """Every destination slot dst_slots[b] must hold, vector for vector, the tags of source slot
+    src_slots[b] (same layer, K/V, head, token, vector); every other slot the sentinel.  A wrong
+    vector is reported by the coordinates it sits at and the tag it holds."""
+    L, _, S, H, bs, D = tags.shape
+    t = tags.reshape(L, 2, S, H, bs, D // 8, 8)
+    got = dst.reshape(L, 2, dst.shape[2], H, bs, D // 8, 8)
+    for b in range(len(src_slots)):
+        want, have = t[:, :, src_slots[b]], got[:, :, dst_slots[b]]
+        if not np.array_equal(have, want):
+            bad = np.argwhere(np.any(have != want, axis=-1))[0]
+            raise AssertionError("block %d, slot %d, (layer, kv, head, token, vector) %s holds tag %s, expected %s"
+                                 % (b, dst_slots[b], bad.tolist(), have[tuple(bad)].tolist(),
+                                    want[tuple(bad)].tolist()))
+    untouched = np.setdiff1d(np.arange(dst.shape[2]), np.asarray(dst_slots))
+    assert np.all(got[:, :, untouched] == sentinel), "a slot no block names was written"

@@ -10,7 +10,7 @@ from kvgen import workloads
 from paper_2606_14779_amd import kvpool as K
 from paper_2606_14779_amd.runner import SENTINEL
 
-from gpu_util import check_full, check_sampled, make_run, oracle_pool, say
+from gpu_util import check_full, check_sampled, check_tags, make_run, oracle_pool, say, tag_cache
 
 pytestmark = pytest.mark.gpu
 
@@ -718,5 +718,30 @@ def test_back_to_back_upload_calls(two_streams):
             cur.wait_stream(s_)
         torch.cuda.synchronize()
         check_full(wl, run, host)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_tagged_pattern_localises_every_vector(layout):
+    """Independent of the oracle: with every source vector tagged with its own coordinates, each
+    destination vector must carry (source slot of its block, its own layer, K/V, head, token,
+    vector index); a wrong one is reported by what it holds instead."""
+    wl = workloads.make(2, max_blocks=61, layout=layout)
+    say("case tagged", layout)
+    run = make_run(wl)
+    try:
+        sh = wl.shape
+        L, H, bs, D = sh.layers, sh.kv_heads, sh.block_size, sh.head_dim
+        tags = tag_cache(L, wl.src_num_slots, H, bs, D)
+        run.src.copy_(torch.from_numpy(tags))
+        run.fill_dst()
+        run.place_all()
+        run.store_all()
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        q = wl.requests[0]
+        check_tags(tags, run.dst.cpu().numpy(), q.src_slots[:q.n_present], q.dst_slots[:q.n_present],
+                   np.int16(np.uint16(SENTINEL).view(np.int16)))
     finally:
         run.close()
