@@ -745,3 +745,20 @@ def test_tagged_pattern_localises_every_vector(layout):
                    np.int16(np.uint16(SENTINEL).view(np.int16)))
     finally:
         run.close()
+
+
+def test_upload_ring_wraps_under_four_streams():
+    """The 32-slot work-list ring wrapped five times by 160 upload-path calls of four requests on four
+    streams, with no host synchronisation: a slot is reused only after the call that last read it."""
+    wl = workloads.make(5, max_blocks=40)
+    say("case ring wrap", [q.n_present for q in wl.requests])
+    run = make_run(wl)
+    try:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_UPLOAD)
+        host = run.setup(keep_host=True)
+        for _ in range(40):
+            run.retrieve_all()
+        torch.cuda.synchronize()
+        check_full(wl, run, host)
+    finally:
+        run.close()
