@@ -1,7 +1,8 @@
 """The library's host code under AddressSanitizer and UndefinedBehaviorSanitizer
 (CPU only): tests/native/host_structures_fuzz.cpp built with placement.cpp,
-glt.cpp and bounce.cpp, and tests/native/placement_fuzz.cpp driving
-placement-only pools through the C ABI of the host-sanitized library."""
+glt.cpp and bounce.cpp; tests/native/placement_fuzz.cpp driving
+placement-only pools through the C ABI of the host-sanitized library; and the
+oracle itself (tests/native/oracle_fuzz.c)."""
 import os
 import shutil
 import subprocess
@@ -45,6 +46,21 @@ def test_placement_through_the_abi_under_asan_ubsan(tmp_path):
            "-L", os.path.join(ROCM, "lib"), "-Wl,-rpath-link," + os.path.join(ROCM, "lib")]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1", UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all checks passed" in r.stdout
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
+def test_oracle_under_asan_ubsan(tmp_path):
+    """The oracle itself under the sanitizers, with leak checking: place / extend / release and store /
+    gather round trips into exactly-sized buffers (tests/native/oracle_fuzz.c)."""
+    exe = str(tmp_path / "oracle_fuzz")
+    cmd = ["gcc", "-std=c11", "-O1", "-g", "-Wall", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           os.path.join(ROOT, "tests", "native", "oracle_fuzz.c"), os.path.join(ROOT, "oracle", "oracle.c"),
+           "-o", exe]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "all checks passed" in r.stdout
