@@ -212,6 +212,13 @@ def test_errors_leave_destination_untouched():
         same = m.copy()
         same[9] = same[0]                                     # other regions' entries in between
         assert code(run.pool.store, same, q.src_slots, wl.src_num_slots, *run.layer_ptrs(run.src), 0) == "INVALID"
+        # the smallest call whose unit count would not fit 32 bits: refused before its map is read
+        import ctypes
+        L = wl.shape.layers
+        too_many = (1 << 32) // (4 * L)
+        rc = K._lib.kv_pool_retrieve(run.pool._h, m.ctypes.data, too_many, q.dst_slots.ctypes.data,
+                                     wl.dst_num_slots, K._ptrs(kp), K._ptrs(vp), ctypes.c_void_p(0))
+        assert K.ERRORS[rc] == "INVALID" and b"too large" in K._lib.kv_pool_last_error()
         torch.cuda.synchronize()
         got = run.dst.cpu().numpy().view(np.uint16)
         assert np.all(got == SENTINEL)                        # no failed call touched it

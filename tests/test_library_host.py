@@ -141,6 +141,20 @@ def test_extend_errors():
     p.close()
 
 
+def test_maximum_counts():
+    """The largest counts the ABI takes: 2^32-1 blocks are refused for room, and a request cannot grow
+    past 2^32-1 blocks in all; nothing changes either way."""
+    p, spec = _pool([3, 1], [1 << 20, 1 << 20])
+    one = np.zeros(1, dtype=K.LOC_DTYPE)        # the library refuses before it writes the map
+    raw = lambda fn, req, n: K.ERRORS.get(fn(p._h, req, n, one.ctypes.data), "OK")   # noqa: E731
+    assert raw(K._lib.kv_pool_place, 1, 2 ** 32 - 1) == "NOSPACE"
+    m = p.place(1, 5)
+    assert raw(K._lib.kv_pool_extend, 1, 2 ** 32 - 5) == "INVALID"
+    assert raw(K._lib.kv_pool_extend, 1, 2 ** 32 - 6) == "NOSPACE"
+    assert np.array_equal(p.lookup(1, 5), m)
+    p.close()
+
+
 def test_workload_scale_placement_equals_oracle():
     from kvgen import workloads
     for cfg in (1, 2, 3, 4, 5):
