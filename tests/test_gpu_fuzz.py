@@ -1,6 +1,8 @@
 """Seeded random GPU parity cases: shapes, region mixes and weights, tables,
 absent entries, layouts, launch shapes and flags; every case is compared with
 the oracle element by element (pool bytes and destination cache)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -53,7 +55,8 @@ def _case(seed):
     return rng, layout, (L, H, bs, D), kinds, weights, n, grid, flags
 
 
-@pytest.mark.parametrize("seed", list(range(40)))
+# KVP_FUZZ_SEEDS widens the run (e.g. 540 for a longer soak); 40 by default
+@pytest.mark.parametrize("seed", list(range(int(os.environ.get("KVP_FUZZ_SEEDS", "40")))))
 def test_random_case(seed):
     rng, layout, (L, H, bs, D), kinds, weights, n, grid, flags = _case(seed)
     say("fuzz", seed, dict(layout=layout, L=L, H=H, bs=bs, D=D, kinds=kinds, w=weights, n=n, grid=grid, flags=flags))
