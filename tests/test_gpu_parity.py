@@ -769,3 +769,57 @@ def test_upload_ring_wraps_under_four_streams():
         check_full(wl, run, host)
     finally:
         run.close()
+
+
+@pytest.mark.parametrize("elem_bytes", [1, 4])
+@pytest.mark.parametrize("layout", [0, 1])
+def test_other_element_sizes(elem_bytes, layout):
+    """fp8-sized (1 byte) and fp32-sized (4 bytes) KV elements: the path copies bytes, so any element
+    size whose chunks and (token-major) rows are 16-byte multiples works.  Random bytes, a mixed pool,
+    a random table with absent entries; against the oracle byte for byte."""
+    import oracle
+    L, H, bs, D, n = 4, 8, 16, 128, 50
+    spec = K.KVSpec(L, H, D, bs, elem_bytes, layout)
+    bb = spec.block_bytes
+    weights = [3, 2, 1]
+    caps = [((w * n // sum(weights) + 2) * bb + 4095) // 4096 * 4096 for w in weights]
+    regions = [K.Region("host", caps[0], 0), K.Region("staging", caps[1]), K.Region("host", caps[2], 0)]
+    say("case element size", elem_bytes, layout)
+    rng = np.random.default_rng(77 + elem_bytes * 3 + layout)
+    S = n + 7
+    row = D * elem_bytes
+    src_h = rng.integers(0, 256, size=(L, 2, S, H, bs, row), dtype=np.uint8)
+    src_slots = rng.permutation(S)[:n].astype(np.int32)
+    dst_slots = rng.permutation(S)[:n].astype(np.int32)
+    dev = torch.device("cuda", 0)
+    src = torch.from_numpy(src_h).to(dev)
+    dst = torch.zeros((L, 2, S, H, bs, row), dtype=torch.uint8, device=dev)
+    kp = lambda t: [t[l, 0].data_ptr() for l in range(L)]           # noqa: E731
+    vp = lambda t: [t[l, 1].data_ptr() for l in range(L)]           # noqa: E731
+    with K.KVPool(regions, weights, spec, 0) as pool:
+        m = pool.place(1, n)
+        ora = oracle.Pool(weights, caps, bb)
+        om = ora.place(1, n)
+        assert np.array_equal(m, om)
+        s = torch.cuda.current_stream().cuda_stream
+        pool.store(m, src_slots, S, kp(src), vp(src), s)
+        rm = m.copy()
+        absent = rng.random(n) < 0.2
+        rm["region"][absent] = K.ABSENT
+        pool.retrieve(rm, dst_slots, S, kp(dst), vp(dst), s)
+        torch.cuda.synchronize()
+        shape = (L, H, bs, D, elem_bytes)
+        oregions = [np.zeros(c, np.uint8) for c in caps]
+        oracle.store(om, src_slots, oregions, [src_h[l, 0] for l in range(L)], [src_h[l, 1] for l in range(L)],
+                     shape, layout)
+        for r in range(len(regions)):
+            offs = om["offset"][om["region"] == r]
+            if len(offs):
+                lo, hi = int(offs.min()), int(offs.max()) + bb
+                assert np.array_equal(pool.region_read(r, lo, hi - lo), oregions[r][lo:hi]), "region %d" % r
+        expect = np.zeros_like(src_h)
+        orm = om.copy()
+        orm["region"][absent] = oracle.ABSENT
+        oracle.gather(orm, dst_slots, oregions, [expect[l, 0] for l in range(L)], [expect[l, 1] for l in range(L)],
+                      shape, layout)
+        assert np.array_equal(dst.cpu().numpy(), expect)
