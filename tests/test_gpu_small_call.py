@@ -65,17 +65,18 @@ def test_both_paths_match_oracle(cfg, n, layout, upload):
         run.close()
 
 
+@pytest.mark.parametrize("layout", [0, 1])
 @pytest.mark.parametrize("upload", [False, True])
 @pytest.mark.parametrize("n,lo,hi", [(191, 7, 8), (192, 7, 8), (23, 0, 1), (23, 30, 32), (23, 29, 32)])
-def test_layer_range(n, lo, hi, upload):
+def test_layer_range(n, lo, hi, upload, layout):
     """A layer range shortens the pointer table: the capacity grows to 191 blocks for one layer, and
     the table starts at the range's first layer (first and last layers covered)."""
-    wl = workloads.make(2, max_blocks=n)
-    say("case small-call layers", n, lo, hi, "upload", upload)
+    wl = workloads.make(2, max_blocks=n, layout=layout)
+    say("case small-call layers", n, lo, hi, "upload", upload, "layout", layout)
     run = make_run(wl)
     try:
         if upload:
-            _upload(run, 0)
+            _upload(run, layout)
         host = run.setup(keep_host=True)
         q = wl.requests[0]
         kp, vp = run.layer_ptrs(run.dst)
