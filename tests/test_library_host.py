@@ -310,3 +310,39 @@ def test_placement_from_threads_keeps_invariants():
         s.sort()
         assert all(a[1] <= b[0] for a, b in zip(s, s[1:]))
     p.close()
+
+
+def test_header_is_c99_and_callable_from_c(tmp_path):
+    """include/kvpool.h is plain C: a C99 program (-pedantic -Werror) includes it, links the library
+    and places and extends a request on a placement-only pool."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("needs gcc")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    src = tmp_path / "c_client.c"
+    src.write_text(r"""
+#include "kvpool.h"
+#include <stdio.h>
+int main(void)
+{
+    kvp_kv_spec spec = {2, 1, 8, 16, 2, 0};
+    kvp_region_desc r = {KVP_REGION_HOST, -1, 1u << 20, KVP_HOST_DEFAULT, 0};
+    uint64_t bw = 1;
+    kvp_pool *p = NULL;
+    kvp_loc m[5];
+    if (kv_pool_create(&r, &bw, 1, &spec, -1, &p) != KVP_OK) { printf("%s\n", kv_pool_last_error()); return 1; }
+    if (kv_pool_place(p, 1, 3, m) != KVP_OK || kv_pool_extend(p, 1, 2, m + 3) != KVP_OK) return 2;
+    if (kv_pool_lookup(p, 1, 5, m) != KVP_OK || kv_pool_lookup(p, 1, 4, m) != KVP_ERR_INVALID) return 3;
+    kv_pool_destroy(p);
+    printf("c client ok\n");
+    return 0;
+}
+""")
+    exe = str(tmp_path / "c_client")
+    lib_dir = os.path.dirname(K.LIB_PATH)
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(root, "include"),
+                    str(src), "-o", exe, "-L", lib_dir, "-lkvpool", "-Wl,-rpath," + lib_dir],
+                   check=True, capture_output=True, text=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and "c client ok" in r.stdout, r.stdout + r.stderr
