@@ -702,6 +702,26 @@ def main():
         stage_only = {"ms_avg": round(avg, 3), "ms_min": round(ss["staging_ms_min"], 3),
                       "copied_gbps": round(stage_bytes / (avg / 1e3) / 1e9, 1)}
 
+    # zero-copy gather alone, from a map without the staging blocks (the link with nothing beside it)
+    host_only = None
+    if host_blocks and stage_blocks and len(wl.requests) == 1 and not args.sdma:
+        q = wl.requests[0]
+        m = run.retrieve_maps[q.request_id].copy()
+        stage_idx = [i for i, r in enumerate(wl.regions) if r.kind != "host"]
+        m["region"][np.isin(m["region"], stage_idx)] = K.ABSENT
+        kp, vp = run.layer_ptrs(run.dst)
+        for _ in range(args.warmup):
+            run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
+        torch.cuda.synchronize()
+        run.pool.set_timing(True)
+        for _ in range(args.steps):
+            run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
+        sh_ = run.pool.timing_summary()
+        run.pool.set_timing(False)
+        avg = sh_["host_ms_sum"] / sh_["host_calls"]
+        host_only = {"ms_avg": round(avg, 3), "ms_min": round(sh_["host_ms_min"], 3),
+                     "gbps": round(host_bytes / (avg / 1e3) / 1e9, 2)}
+
     log("timed region done: %.3f ms per retrieve" % ms_per_step)
     # store (offload) direction: the same request written back into its placed ranges
     store = None
@@ -842,6 +862,8 @@ def main():
                          "host_enqueue_median": round(statistics.median(enqueue_ms), 3)},
         "roofline": roof,
         "roofline_staging": hbm_roof,
+        "host_alone": dict(host_only, frac_measured=round(host_only["gbps"] / pr["host_link_peak_gbps"], 4)
+                           if pr else None) if host_only else None,
         "probes": pr,
         "store": store,
         "roofline_store": store_roof,
