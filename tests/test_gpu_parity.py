@@ -165,6 +165,17 @@ def test_absent_entries_and_all_absent():
         m["region"][:] = K.ABSENT                            # nothing to do, nothing launched
         run.pool.retrieve(m, table, wl.dst_num_slots, kp, vp, 0)
         torch.cuda.synchronize()
+        # empty calls: zero-length arrays, and NULL map and table with n_blocks = 0
+        import ctypes
+        before = run.dst.cpu().numpy().copy()
+        empty, no_slots = np.zeros(0, dtype=K.LOC_DTYPE), np.zeros(0, np.int32)
+        run.pool.retrieve(empty, no_slots, wl.dst_num_slots, kp, vp, 0)
+        run.pool.store(empty, no_slots, wl.src_num_slots, *run.layer_ptrs(run.src), 0)
+        run.pool.retrieve_layers(empty, no_slots, wl.dst_num_slots, 2, 5, kp, vp, 0)
+        assert K._lib.kv_pool_retrieve(run.pool._h, None, 0, None, wl.dst_num_slots, K._ptrs(kp), K._ptrs(vp),
+                                       ctypes.c_void_p(0)) == 0
+        torch.cuda.synchronize()
+        assert np.array_equal(run.dst.cpu().numpy(), before)
     finally:
         run.close()
 
