@@ -265,6 +265,35 @@ def test_release_and_reuse():
         run.close()
 
 
+def test_release_waits_for_a_retrieve_in_flight():
+    """Release a request while its retrieve runs on another stream, then place a new request over the
+    same ranges and store other values there at once: release waits for the retrieve, so the
+    destination holds the original values."""
+    from gpu_util import oracle_expectation
+    wl = workloads.make(2, max_blocks=300)
+    say("case release in flight")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        a = torch.cuda.Stream()
+        a.wait_stream(torch.cuda.current_stream())
+        run.pool.retrieve_request(q.request_id, q.dst_slots, wl.dst_num_slots, kp, vp, a.cuda_stream)
+        run.pool.release(q.request_id)                       # returns once the retrieve is done
+        new = run.pool.place(q.request_id + 1, q.n_present)
+        assert set(zip(new["region"].tolist(), new["offset"].tolist())) == \
+            set(zip(run.maps[q.request_id]["region"].tolist(), run.maps[q.request_id]["offset"].tolist()))
+        run.src.bitwise_not_()                               # other values, then stored over the same bytes
+        run.pool.store(new, q.src_slots, wl.src_num_slots, *run.layer_ptrs(run.src),
+                       torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        _, _, expect = oracle_expectation(wl, run, host)
+        assert np.array_equal(run.dst.cpu().numpy().view(np.uint16), expect)
+    finally:
+        run.close()
+
+
 def test_store_then_retrieve_across_streams():
     """A retrieve on another stream, enqueued right after the store, waits for it."""
     wl = workloads.make(3, max_blocks=200)
