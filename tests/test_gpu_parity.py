@@ -294,6 +294,28 @@ def test_release_waits_for_a_retrieve_in_flight():
         run.close()
 
 
+def test_destroy_waits_for_a_retrieve_in_flight():
+    """Destroy the pool while a retrieve runs on another stream: destroy waits for the work on its
+    requests before freeing the regions, and the retrieve completes intact."""
+    from gpu_util import oracle_expectation
+    wl = workloads.make(2, max_blocks=300)
+    say("case destroy in flight")
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        q = wl.requests[0]
+        kp, vp = run.layer_ptrs(run.dst)
+        a = torch.cuda.Stream()
+        a.wait_stream(torch.cuda.current_stream())
+        run.pool.retrieve_request(q.request_id, q.dst_slots, wl.dst_num_slots, kp, vp, a.cuda_stream)
+        run.pool.close()                                     # returns once the retrieve is done
+        torch.cuda.synchronize()
+        _, _, expect = oracle_expectation(wl, run, host)
+        assert np.array_equal(run.dst.cpu().numpy().view(np.uint16), expect)
+    finally:
+        run.close()
+
+
 def test_store_then_retrieve_across_streams():
     """A retrieve on another stream, enqueued right after the store, waits for it."""
     wl = workloads.make(3, max_blocks=200)
