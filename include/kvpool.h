@@ -299,8 +299,8 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
 int kv_pool_measure_bandwidth(kvp_pool *pool, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_out);
 
 /*
- * Replace the bandwidth weights b_i (Eq. 1) used by later kv_pool_place
- * calls; existing placements keep their locations.
+ * Replace the bandwidth weights b_i (Eq. 1) used by later kv_pool_place and
+ * kv_pool_extend calls; existing placements keep their locations.
  *   bandwidths[n_regions]  positive integers.  Errors: INVALID.
  */
 int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);

@@ -155,6 +155,19 @@ def test_maximum_counts():
     p.close()
 
 
+def test_extension_uses_the_current_weights():
+    """After kv_pool_set_bandwidths, an extension is placed by the new weights, as a new placement is;
+    the request's earlier blocks stay where they were."""
+    p, spec = _pool([1, 1], [1 << 20, 1 << 20])
+    first = p.place(1, 4)
+    assert list(first["region"]) == [0, 1, 0, 1]
+    p.set_bandwidths([1, 3])
+    ext = p.extend(1, 4)
+    assert sorted(ext["region"].tolist()) == [0, 1, 1, 1]          # Eq. 2 with the new weights
+    assert np.array_equal(p.lookup(1, 8), np.concatenate([first, ext]))
+    p.close()
+
+
 def test_workload_scale_placement_equals_oracle():
     from kvgen import workloads
     for cfg in (1, 2, 3, 4, 5):
