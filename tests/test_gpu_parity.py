@@ -885,3 +885,35 @@ def test_other_element_sizes(elem_bytes, layout):
         oracle.gather(orm, dst_slots, oregions, [expect[l, 0] for l in range(L)], [expect[l, 1] for l in range(L)],
                       shape, layout)
         assert np.array_equal(dst.cpu().numpy(), expect)
+
+
+def test_two_pools_at_once():
+    """Two pools on one GPU, their calls interleaved on two streams (each pool stores on one and
+    retrieves on the other): the pools share nothing, and both results equal the oracle's."""
+    wls = [workloads.make(2, max_blocks=70, seed=11), workloads.make(4, max_blocks=90, seed=12)]
+    say("case two pools")
+    runs = [make_run(w) for w in wls]
+    try:
+        hosts = []
+        for r in runs:
+            hosts.append(r.fill_source(keep_host=True))
+            r.fill_dst()
+            r.place_all()
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        for s_ in streams:
+            s_.wait_stream(torch.cuda.current_stream())
+        for i, r in enumerate(runs):                          # pool i stores on stream i ...
+            r.store_all(streams[i])
+        streams[0].wait_stream(streams[1])
+        streams[1].wait_stream(streams[0])
+        for i, r in enumerate(runs):                          # ... and retrieves on the other one
+            for q in r.wl.requests:
+                r.retrieve(q, streams[1 - i])
+        for s_ in streams:
+            torch.cuda.current_stream().wait_stream(s_)
+        torch.cuda.synchronize()
+        for w, r, h in zip(wls, runs, hosts):
+            check_full(w, r, h)
+    finally:
+        for r in runs:
+            r.close()
