@@ -134,8 +134,9 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths,
  * order; block k of region i's share sits at base_i + k*block_bytes.  The
  * GLT records every block (UpdateGLT).
  *   map_out[n_blocks]    caller-owned, receives (region, gen, offset).
- * Atomic: on KVP_ERR_NOSPACE nothing is placed.  Errors: INVALID (n_blocks
- * == 0 or request already placed), NOSPACE.
+ * Atomic: on any error (KVP_ERR_NOSPACE, or KVP_ERR_NOMEM when the library's
+ * own host memory runs out) nothing is placed.  Errors: INVALID (n_blocks
+ * == 0 or request already placed), NOSPACE, NOMEM, HIP.
  */
 int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_loc *map_out);
 
@@ -152,8 +153,8 @@ int kv_pool_place(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_lo
  * one-block set goes to the region with the largest p_i (lowest index on
  * ties).
  *   map_out[n_new]    caller-owned, receives the new blocks' entries.
- * Atomic: on KVP_ERR_NOSPACE nothing changes.  Errors: INVALID (n_new == 0,
- * more than 2^32-1 blocks in all), NOTFOUND, NOSPACE.
+ * Atomic: on any error nothing changes.  Errors: INVALID (n_new == 0, more
+ * than 2^32-1 blocks in all), NOTFOUND, NOSPACE, NOMEM.
  */
 int kv_pool_extend(kvp_pool *pool, uint64_t request_id, uint32_t n_new, kvp_loc *map_out);
 
@@ -245,7 +246,8 @@ int kv_pool_store_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
  * Release a request: its ranges go back to the regions' free lists (merged
  * with free neighbours) and its GLT entries are removed.  Waits for store /
  * retrieve work already enqueued on this request to finish.  Maps of it
- * become stale.  Errors: NOTFOUND.
+ * become stale.  Atomic: on any error the request stays placed and whole.
+ * Errors: NOTFOUND, NOMEM, HIP.
  */
 int kv_pool_release(kvp_pool *pool, uint64_t request_id);
 

@@ -35,25 +35,41 @@ struct kvp_pool {
 namespace {
 
 thread_local std::string g_last_error;
+thread_local const char *g_fixed_error = nullptr;   // set when the message itself could not be stored
+
+// Record the message of a failure without throwing: a message that cannot be
+// copied (out of host memory) is replaced by a fixed one; the code returned is
+// the failure's own either way.
+void set_error(const char *msg) noexcept
+{
+    try {
+        g_last_error = msg;
+        g_fixed_error = nullptr;
+    } catch (...) {
+        g_last_error.clear();
+        g_fixed_error = "out of host memory (the error message could not be stored)";
+    }
+}
 
 template <class F>
-int guarded(F &&f)
+int guarded(F &&f) noexcept
 {
     try {
         f();
         g_last_error.clear();
+        g_fixed_error = nullptr;
         return KVP_OK;
     } catch (const kvp::Error &e) {
-        g_last_error = e.msg;
+        set_error(e.msg.c_str());
         return e.code;
     } catch (const std::bad_alloc &) {
-        g_last_error = "host allocation failed";
+        set_error("host allocation failed");
         return KVP_ERR_NOMEM;
     } catch (const std::exception &e) {
-        g_last_error = e.what();
+        set_error(e.what());
         return KVP_ERR_INVALID;
     } catch (...) {
-        g_last_error = "unknown error";
+        set_error("unknown error");
         return KVP_ERR_INVALID;
     }
 }
@@ -164,7 +180,7 @@ void kv_pool_destroy(kvp_pool *pool)
     delete pool;
 }
 
-const char *kv_pool_last_error(void) { return g_last_error.c_str(); }
+const char *kv_pool_last_error(void) { return g_fixed_error ? g_fixed_error : g_last_error.c_str(); }
 
 int kv_pool_region_info(const kvp_pool *pool, uint32_t region, kvp_region_info *out)
 {

@@ -2,7 +2,7 @@
 // offloaded block with its key, device index, device type and location.
 // The key is a hash of the block identifier (request, block index); the full
 // identifier is stored too, so two blocks whose hashes collide never alias.
-// Linear probing with backward-shift deletion; grows at load factor 1/2.
+// Linear probing with backward-shift deletion; kept at load factor 1/2 or below.
 
 #include "internal.hpp"
 
@@ -23,22 +23,9 @@ uint64_t Glt::hash(uint64_t request, uint32_t block)
     return mix64(request ^ mix64(0x4B56ull << 32 | block));
 }
 
-void Glt::grow()
+// Probe from the entry's home slot to its own or the first empty slot.
+void Glt::place(const GltEntry &e)
 {
-    std::vector<GltEntry> old;
-    old.reserve(count_);
-    for (size_t i = 0; i < slots_.size(); ++i)
-        if (used_[i]) old.push_back(slots_[i]);
-    const size_t cap = slots_.size() * 2;
-    slots_.assign(cap, GltEntry{});
-    used_.assign(cap, 0);
-    count_ = 0;
-    for (const auto &e : old) insert(e);
-}
-
-void Glt::insert(const GltEntry &e)
-{
-    if ((count_ + 1) * 2 > slots_.size()) grow();
     const size_t mask = slots_.size() - 1;
     size_t i = hash(e.request, e.block) & mask;
     while (used_[i]) {
@@ -51,6 +38,26 @@ void Glt::insert(const GltEntry &e)
     slots_[i] = e;
     used_[i] = 1;
     ++count_;
+}
+
+void Glt::reserve(size_t extra)
+{
+    size_t cap = slots_.size();
+    while ((count_ + extra) * 2 > cap) cap *= 2;
+    if (cap == slots_.size()) return;
+    Glt bigger;                      // built aside, swapped in only when complete
+    bigger.slots_.assign(cap, GltEntry{});
+    bigger.used_.assign(cap, 0);
+    for (size_t i = 0; i < slots_.size(); ++i)
+        if (used_[i]) bigger.place(slots_[i]);
+    slots_.swap(bigger.slots_);
+    used_.swap(bigger.used_);
+}
+
+void Glt::insert(const GltEntry &e)
+{
+    reserve(1);
+    place(e);
 }
 
 const GltEntry *Glt::find(uint64_t request, uint32_t block) const

@@ -64,12 +64,20 @@ class RangeAllocator {
 public:
     explicit RangeAllocator(uint64_t capacity = 0);
     bool first_fit(uint64_t len, uint64_t *start) const;
+    // All-or-nothing; allocates nothing (cannot fail) when start begins a free range,
+    // as every range that first_fit finds does.
     void take(uint64_t start, uint64_t len);
+    // Makes the next k calls of give() allocation-free.  May throw (out of
+    // host memory), leaving the free ranges as they were.
+    void reserve_gives(size_t k);
+    // Cannot fail within the reserved count.
     void give(uint64_t start, uint64_t len);
     uint64_t largest() const;
 
 private:
-    std::map<uint64_t, uint64_t> free_;  // start -> length
+    using Free = std::map<uint64_t, uint64_t>;
+    Free free_;                             // start -> length
+    std::vector<Free::node_type> spare_;    // unlinked nodes for give()
 };
 
 // ---------------------------------------------------------------- GLT (Sec. 4.1.1)
@@ -83,10 +91,13 @@ struct GltEntry {
     uint64_t offset;    // location
 };
 
-// Open-addressing hash table keyed by (request, block).
+// Open-addressing hash table keyed by (request, block).  reserve() makes room
+// for that many further entries and is all-or-nothing; inserts within the
+// reserved room allocate nothing, so they cannot fail.
 class Glt {
 public:
     Glt();
+    void reserve(size_t extra);
     void insert(const GltEntry &e);
     const GltEntry *find(uint64_t request, uint32_t block) const;
     bool erase(uint64_t request, uint32_t block);
@@ -94,7 +105,7 @@ public:
 
 private:
     static uint64_t hash(uint64_t request, uint32_t block);
-    void grow();
+    void place(const GltEntry &e);
     std::vector<GltEntry> slots_;
     std::vector<uint8_t> used_;
     size_t count_ = 0;

@@ -88,17 +88,52 @@ void RangeAllocator::take(uint64_t start, uint64_t len)
     auto it = free_.upper_bound(start);
     --it;  // the free range containing start (first_fit guarantees it exists)
     const uint64_t fs = it->first, fl = it->second;
-    free_.erase(it);
-    if (start > fs) free_.emplace(fs, start - fs);
-    if (start + len < fs + fl) free_.emplace(start + len, fs + fl - start - len);
+    const uint64_t tail = fs + fl - start - len;
+    if (start == fs) {
+        if (tail == 0) {
+            if (spare_.size() < spare_.capacity())
+                spare_.push_back(free_.extract(it));   // kept for a later give()
+            else
+                free_.erase(it);
+            return;
+        }
+        auto node = free_.extract(it);   // re-keyed in place: no allocation
+        node.key() = start + len;
+        node.mapped() = tail;
+        free_.insert(std::move(node));
+        return;
+    }
+    if (tail) free_.emplace(start + len, tail);   // the only step that can fail, taken first
+    it->second = start - fs;
+}
+
+void RangeAllocator::reserve_gives(size_t k)
+{
+    if (spare_.size() >= k) return;
+    spare_.reserve(k);
+    Free scratch;   // nodes are made by inserting and unlinking them
+    while (spare_.size() < k) {
+        scratch.emplace(0, 0);
+        spare_.push_back(scratch.extract(scratch.begin()));
+    }
 }
 
 void RangeAllocator::give(uint64_t start, uint64_t len)
 {
     auto next = free_.lower_bound(start);
-    if (next != free_.end() && start + len == next->first) {
-        len += next->second;
-        next = free_.erase(next);
+    if (next != free_.end() && start + len == next->first) {   // merge with the range after
+        auto node = free_.extract(next);
+        node.key() = start;
+        node.mapped() += len;
+        next = free_.insert(std::move(node)).position;
+        if (next != free_.begin()) {                           // and with the one before
+            auto prev = std::prev(next);
+            if (prev->first + prev->second == start) {
+                prev->second += next->second;
+                free_.erase(next);
+            }
+        }
+        return;
     }
     if (next != free_.begin()) {
         auto prev = std::prev(next);
@@ -107,7 +142,15 @@ void RangeAllocator::give(uint64_t start, uint64_t len)
             return;
         }
     }
-    free_.emplace(start, len);
+    if (spare_.empty()) {
+        free_.emplace(start, len);
+        return;
+    }
+    auto node = std::move(spare_.back());
+    spare_.pop_back();
+    node.key() = start;
+    node.mapped() = len;
+    free_.insert(std::move(node));
 }
 
 uint64_t RangeAllocator::largest() const

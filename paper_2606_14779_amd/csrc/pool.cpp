@@ -370,24 +370,38 @@ SetPlan reserve_set(Pool &p, uint32_t n)
 }
 
 // Take the planned ranges for blocks first .. first+n-1 of rec, stripe the
-// blocks over them (R3) and record their GLT entries.
+// blocks over them (R3) and record their GLT entries.  All or nothing: every
+// step that allocates host memory runs before the pool changes, or is undone
+// if a later one fails; what follows them cannot fail.
 void commit_set(Pool &p, RequestRec &rec, const SetPlan &s, uint32_t first, uint32_t n, kvp_loc *out)
 {
     const uint32_t N = static_cast<uint32_t>(p.regions.size());
-    for (uint32_t i = 0; i < N; ++i) {
-        if (!s.len[i]) continue;
-        p.regions[i].alloc.take(s.base[i], s.len[i]);
-        rec.ranges.push_back(Allocation{&rec, i, rec.gen, s.base[i], s.counts[i], s.len[i]});
-        p.regions[i].live[s.base[i]] = &rec.ranges.back();
-    }
     std::vector<uint32_t> region_of;
     stripe(s.counts, n, region_of);
     std::vector<uint64_t> next(N, 0);
+    p.glt.reserve(n);
+    const size_t ranges_before = rec.ranges.size();
+    uint32_t linked = 0;   // regions whose new range is in their live map
+    try {
+        for (uint32_t i = 0; i < N; ++i) {
+            if (!s.len[i]) continue;
+            rec.ranges.push_back(Allocation{&rec, i, rec.gen, s.base[i], s.counts[i], s.len[i]});
+            p.regions[i].live.emplace(s.base[i], &rec.ranges.back());
+            linked = i + 1;
+        }
+    } catch (...) {
+        for (uint32_t i = 0; i < linked; ++i)
+            if (s.len[i]) p.regions[i].live.erase(s.base[i]);
+        while (rec.ranges.size() > ranges_before) rec.ranges.pop_back();
+        throw;
+    }
+    for (uint32_t i = 0; i < N; ++i)
+        if (s.len[i]) p.regions[i].alloc.take(s.base[i], s.len[i]);   // first-fit starts: no allocation
     for (uint32_t j = 0; j < n; ++j) {
         const uint32_t r = region_of[j];
         const uint64_t off = s.base[r] + next[r]++ * p.block_bytes;
         out[j] = kvp_loc{r, rec.gen, off};
-        p.glt.insert(GltEntry{rec.id, first + j, r, p.regions[r].desc.type, rec.gen, off});
+        p.glt.insert(GltEntry{rec.id, first + j, r, p.regions[r].desc.type, rec.gen, off});   // reserved
     }
     rec.n_blocks = first + n;
 }
@@ -413,9 +427,23 @@ void pool_place(Pool &p, uint64_t request, uint32_t n_blocks, kvp_loc *out)
         }
     }
     rec->id = request;
-    rec->gen = p.next_gen++;
-    commit_set(p, *rec, plan, 0, n_blocks, out);
-    p.requests.emplace(request, std::move(rec));
+    rec->gen = p.next_gen;
+    RequestRec *r = rec.get();
+    const hipEvent_t stored = rec->stored, busy = rec->busy;   // the record may be gone in the handler
+    try {
+        auto slot = p.requests.emplace(request, std::move(rec)).first;
+        try {
+            commit_set(p, *r, plan, 0, n_blocks, out);
+        } catch (...) {
+            p.requests.erase(slot);
+            throw;
+        }
+    } catch (...) {
+        if (stored) (void)hipEventDestroy(stored);
+        if (busy) (void)hipEventDestroy(busy);
+        throw;
+    }
+    ++p.next_gen;
 }
 
 void pool_extend(Pool &p, uint64_t request, uint32_t n_new, kvp_loc *out)
@@ -469,6 +497,11 @@ void pool_release(Pool &p, uint64_t request)
     auto it = p.requests.find(request);
     if (it == p.requests.end()) fail(KVP_ERR_NOTFOUND, "request " + std::to_string(request) + " is not placed");
     RequestRec &rec = *it->second;
+    // the only steps that can fail come first; from the first change on, nothing can
+    std::vector<size_t> gives(p.regions.size(), 0);
+    for (const auto &a : rec.ranges) ++gives[a.region];
+    for (size_t i = 0; i < gives.size(); ++i)
+        if (gives[i]) p.regions[i].alloc.reserve_gives(gives[i]);
     if (!p.placement_only) {
         DeviceScope dev(p.device);
         if (rec.busy_rec) check_hip(hipEventSynchronize(rec.busy), "hipEventSynchronize");

@@ -1,7 +1,9 @@
 // Randomised check of the library's host-side data structures, built with
 // AddressSanitizer and UndefinedBehaviorSanitizer by tests/test_native_asan.py.
 //
-//   RangeAllocator   against a byte-granular model of the free space
+//   RangeAllocator   against a byte-granular model of the free space, taking
+//                    ranges at and inside free runs, with and without spare
+//                    nodes reserved for give()
 //   Glt              against std::map, through inserts, finds and the
 //                    backward-shift deletions
 //   target_counts    sum and per-region bounds of Eq. 2
@@ -44,6 +46,7 @@ static void allocator_against_model(std::mt19937_64 &rng)
     for (int step = 0; step < 400; ++step) {
         if (!live.empty() && rng() % 3 == 0) {
             const size_t k = rng() % live.size();
+            if (rng() % 2) a.reserve_gives(rng() % 4);   // spare nodes for give()
             a.give(live[k].first, live[k].second);
             for (uint64_t i = 0; i < live[k].second; ++i) used[live[k].first + i] = 0;
             live.erase(live.begin() + k);
@@ -63,6 +66,10 @@ static void allocator_against_model(std::mt19937_64 &rng)
             CHECK(ok == (expect != UINT64_MAX));
             if (!ok) continue;
             CHECK(start == expect);
+            // now and then a range from inside the free run instead of its start
+            uint64_t run_end = start;
+            while (run_end < cap && !used[run_end]) ++run_end;
+            if (rng() % 4 == 0 && run_end - start > len) start += rng() % (run_end - start - len + 1);
             a.take(start, len);
             for (uint64_t i = 0; i < len; ++i) {
                 CHECK(!used[start + i]);

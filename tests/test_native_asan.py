@@ -1,8 +1,9 @@
 """The library's host code under AddressSanitizer and UndefinedBehaviorSanitizer
 (CPU only): tests/native/host_structures_fuzz.cpp built with placement.cpp,
 glt.cpp and bounce.cpp; tests/native/placement_fuzz.cpp driving
-placement-only pools through the C ABI of the host-sanitized library; and the
-oracle itself (tests/native/oracle_fuzz.c)."""
+placement-only pools through the C ABI of the host-sanitized library;
+tests/native/alloc_failure.cpp failing host allocations inside place, extend
+and release; and the oracle itself (tests/native/oracle_fuzz.c)."""
 import os
 import shutil
 import subprocess
@@ -46,6 +47,25 @@ def test_placement_through_the_abi_under_asan_ubsan(tmp_path):
            "-L", os.path.join(ROCM, "lib"), "-Wl,-rpath-link," + os.path.join(ROCM, "lib")]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1", UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all checks passed" in r.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_host_allocation_failures_change_nothing(tmp_path):
+    """Every place, extend and release retried with each of its host allocations failing in turn:
+    each failed try returns KVP_ERR_NOMEM and leaves the pool as it was, checked against a twin pool
+    that never fails (tests/native/alloc_failure.cpp), with leak checking."""
+    if not os.path.exists(SAN_LIB):
+        pytest.skip("host-sanitized library not built (run the package build first)")
+    exe = str(tmp_path / "alloc_failure")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "tests", "native", "alloc_failure.cpp"),
+           "-o", exe, "-L", os.path.dirname(SAN_LIB), "-lkvpool", "-Wl,-rpath," + os.path.dirname(SAN_LIB),
+           "-L", os.path.join(ROCM, "lib"), "-Wl,-rpath-link," + os.path.join(ROCM, "lib")]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:halt_on_error=1", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "all checks passed" in r.stdout
