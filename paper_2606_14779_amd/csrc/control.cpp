@@ -95,6 +95,7 @@ void pool_region_info(const Pool &p, uint32_t region, kvp_region_info *out)
     if (!out) fail(KVP_ERR_INVALID, "null output");
     if (region >= p.regions.size()) fail(KVP_ERR_INVALID, "region index out of range");
     const Region &r = p.regions[region];
+    std::lock_guard<std::mutex> lock(p.mu);   // the bandwidth may be set meanwhile
     *out = kvp_region_info{r.desc.type, r.desc.numa_node, r.numa_actual, r.flags_used, r.capacity,
                            r.bandwidth, r.host, r.dev};
 }

@@ -182,7 +182,7 @@ struct Pool {
     std::unordered_map<uint64_t, std::unique_ptr<RequestRec>> requests;
     Glt glt;
     uint32_t next_gen = 1;
-    std::mutex mu;
+    mutable std::mutex mu;
 
     hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's);
                                        // with KVP_LAUNCH_SDMA the host-link copies' stream instead

@@ -4,8 +4,8 @@
 // Each thread owns its own request ids and runs a seeded sequence of place,
 // extend, lookup and release calls, checking every lookup against the maps
 // it was given and that its error messages are its own (the message is
-// thread-local).  Other threads read region descriptions and compute Eq. 2
-// counts meanwhile.  After the join, the blocks of all live requests must sit
+// thread-local).  Other threads meanwhile set the weights (to the values they
+// already have), read region descriptions and compute Eq. 2 counts.  After the join, the blocks of all live requests must sit
 // in distinct places, and releasing them all must give every byte back: a
 // request that fills every region exactly then fits.
 #include <atomic>
@@ -92,11 +92,12 @@ void worker(kvp_pool *pool, int id, Live *out, std::atomic<uint64_t> *refusals)
     }
 }
 
-void reader(const kvp_pool *pool, const std::atomic<bool> *stop)
+void reader(kvp_pool *pool, const std::atomic<bool> *stop)
 {
     const uint64_t w[kRegions] = {4, 4, 1, 1};
     uint64_t c[kRegions];
     while (!stop->load()) {
+        CHECK(kv_pool_set_bandwidths(pool, w) == KVP_OK);   // the same weights: maps stay as they are
         for (uint32_t i = 0; i < kRegions; ++i) {
             kvp_region_info info;
             CHECK(kv_pool_region_info(pool, i, &info) == KVP_OK);
