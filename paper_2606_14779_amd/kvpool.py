@@ -9,6 +9,7 @@ module raises on import: there is no fallback path.
 from __future__ import annotations
 
 import ctypes
+import operator
 import os
 from dataclasses import dataclass
 
@@ -79,7 +80,7 @@ except ImportError:
 if not os.path.exists(LIB_PATH):
     raise ImportError("libkvpool.so is not built (%s); run `python -m paper_2606_14779_amd.build`"
                       % LIB_PATH)
-_lib = ctypes.CDLL(LIB_PATH)
+_cdll = ctypes.CDLL(LIB_PATH)
 
 _u32, _u64, _i32, _vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p
 _SIGS = {
@@ -108,10 +109,35 @@ _SIGS = {
     "kv_probe_copy_kernel": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp]),
     "kv_probe_memcpy": (_i32, [_vp, _vp, _u64, _vp]),
 }
+# ctypes wraps an integer outside its C type's range silently (-1 becomes
+# 2^32-1 for a uint32_t: a slot count that every table entry passes), so every
+# integer argument is checked against its type's range first.
+_RANGES = {_u32: (0, 1 << 32), _u64: (0, 1 << 64), _i32: (-(1 << 31), 1 << 31)}
+
+
+def _range_checked(name, f, argtypes):
+    checks = [(i, _RANGES[t]) for i, t in enumerate(argtypes) if t in _RANGES]
+
+    def call(*args):
+        for i, (lo, hi) in checks:
+            v = operator.index(args[i])
+            if not lo <= v < hi:
+                raise ValueError("%s: argument %d = %d is outside [%d, %d)" % (name, i, v, lo, hi))
+        return f(*args)
+    call.__name__ = name
+    return call
+
+
+class _Lib:
+    """The library's entry points, with their integer arguments range-checked."""
+
+
+_lib = _Lib()
 for _name, (_res, _args) in _SIGS.items():
-    _f = getattr(_lib, _name)
+    _f = getattr(_cdll, _name)
     _f.restype = _res
     _f.argtypes = _args
+    setattr(_lib, _name, _range_checked(_name, _f, _args))
 
 EXPORTED = tuple(_SIGS)
 
@@ -130,6 +156,14 @@ def _check(rc: int) -> None:
 
 def _ptrs(ptrs) -> ctypes.Array:
     return (ctypes.c_void_p * len(ptrs))(*[int(p) for p in ptrs])
+
+
+def _block_count(n) -> int:
+    """A block count as the ABI's uint32_t, checked before an output array of that size is made."""
+    n = operator.index(n)
+    if not 0 <= n < 1 << 32:
+        raise ValueError("block count %d is outside [0, 2^32)" % n)
+    return n
 
 
 def _loc_array(m) -> np.ndarray:
@@ -241,17 +275,20 @@ class KVPool:
 
     # ---- placement / GLT
     def place(self, request: int, n_blocks: int) -> np.ndarray:
+        n_blocks = _block_count(n_blocks)
         out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
         _check(_lib.kv_pool_place(self._h, request, n_blocks, out.ctypes.data))
         return out[:n_blocks]
 
     def extend(self, request: int, n_new: int) -> np.ndarray:
         """Entries of the request's next n_new blocks, placed as an offload set of their own."""
+        n_new = _block_count(n_new)
         out = np.zeros(max(n_new, 1), dtype=LOC_DTYPE)
         _check(_lib.kv_pool_extend(self._h, request, n_new, out.ctypes.data))
         return out[:n_new]
 
     def lookup(self, request: int, n_blocks: int) -> np.ndarray:
+        n_blocks = _block_count(n_blocks)
         out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
         _check(_lib.kv_pool_lookup(self._h, request, n_blocks, out.ctypes.data))
         return out[:n_blocks]
@@ -307,7 +344,8 @@ class KVPool:
     def region_read(self, region: int, offset: int, nbytes: int, out: np.ndarray | None = None) -> np.ndarray:
         if out is None:
             out = np.empty(nbytes, dtype=np.uint8)
-        assert out.flags.c_contiguous and out.nbytes >= nbytes
+        if not (out.flags.c_contiguous and out.nbytes >= nbytes):
+            raise ValueError("out must be C-contiguous and hold nbytes")
         _check(_lib.kv_pool_region_read(self._h, region, offset, nbytes, out.ctypes.data))
         return out
 

@@ -241,6 +241,40 @@ def test_transfers_rejected_without_device():
     p.close()
 
 
+def test_binding_rejects_integers_outside_their_c_type():
+    """ctypes would wrap -1 to 2^32-1 (a slot count every table entry passes); the binding refuses it
+    before the call, for every integer argument of every entry point."""
+    p, spec = _pool([1], [1 << 20])
+    ptrs = [16 * 1024] * spec.num_layers
+    with pytest.raises(ValueError, match="outside"):
+        p.place(1, -1)
+    with pytest.raises(ValueError, match="outside"):
+        p.place(-1, 2)
+    with pytest.raises(ValueError, match="outside"):
+        p.extend(1, 2 ** 32)
+    m = p.place(1, 2)
+    with pytest.raises(ValueError, match="outside"):
+        p.retrieve(m, [0, 1], -1, ptrs, ptrs)
+    with pytest.raises(ValueError, match="outside"):
+        p.retrieve_layers(m, [0, 1], 2, 0, -1, ptrs, ptrs)
+    with pytest.raises(ValueError, match="outside"):
+        p.region_read(0, -16, 16)
+    with pytest.raises(ValueError, match="outside"):
+        K.counts([1, 1], -5)
+    with pytest.raises(ValueError, match="outside"):
+        p.set_launch(0, 0, 2 ** 32, 0)
+    for name, (_, args) in K._SIGS.items():                       # every wrapper checks
+        ints = [i for i, t in enumerate(args) if t in K._RANGES]
+        if not ints:
+            continue
+        call = [None if t is K._vp else 0 for t in args]
+        call[ints[-1]] = K._RANGES[args[ints[-1]]][1]                   # one past the type's maximum
+        with pytest.raises(ValueError, match=name):
+            getattr(K._lib, name)(*call)
+    assert np.array_equal(p.lookup(1, 2), m)                      # nothing reached the pool
+    p.close()
+
+
 def test_glt_survives_many_requests():
     """Table growth and backward-shift deletion keep every lookup exact."""
     p, spec = _pool([3, 1, 2], [1 << 34] * 3)
