@@ -133,6 +133,7 @@ struct RequestRec {
     hipEvent_t busy = nullptr;     // recorded after each store / retrieve touching it
     bool stored_rec = false;
     bool busy_rec = false;
+    uint64_t call_mark = 0;         // the last store / retrieve call that listed it (pool lock held)
 };
 
 struct Region {
@@ -182,6 +183,7 @@ struct Pool {
     std::unordered_map<uint64_t, std::unique_ptr<RequestRec>> requests;
     Glt glt;
     uint32_t next_gen = 1;
+    uint64_t call_epoch = 0;        // numbers the store / retrieve calls
     mutable std::mutex mu;
 
     hipStream_t s_stage = nullptr;     // the staging-class kernel's stream (host class: caller's);

@@ -165,6 +165,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::vector<CopyItem> items[2];
     std::vector<HostBlock> host_blocks;   // copy-engine transport: placed in ring slots below
     std::vector<RequestRec *> touched;
+    const uint64_t epoch = ++p.call_epoch;
     // No two present entries may write the same place: a destination slot on
     // retrieve, a pool block on store.  One pass over bitmaps -- of the
     // destination slots, or of the blocks of each allocation a store touches
@@ -215,7 +216,10 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             }
             mark(region_word[e.region] * 64 + (e.offset - hint->base) / p.block_bytes);
         }
-        if (std::find(touched.begin(), touched.end(), hint->owner) == touched.end()) touched.push_back(hint->owner);
+        if (new_hint && hint->owner->call_mark != epoch) {   // each request listed once
+            hint->owner->call_mark = epoch;
+            touched.push_back(hint->owner);
+        }
         const Region &r = p.regions[e.region];
         const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
         if (cls == KVP_CLASS_HOST && sdma)

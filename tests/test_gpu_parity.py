@@ -917,3 +917,42 @@ def test_two_pools_at_once():
     finally:
         for r in runs:
             r.close()
+
+
+@pytest.mark.parametrize("sdma", [False, True])
+def test_hundreds_of_requests_in_one_call(sdma):
+    """300 requests of 1-6 blocks each, placed separately on a mixed pool, then stored in one call and
+    retrieved in one call (maps and tables concatenated, a permuted destination), through the kernel
+    and through the copy engines: every request is listed once for its ordering events, and every
+    destination vector carries its own tags.  Releasing each request then waits on those events."""
+    L, H, bs, D = 4, 2, 16, 64
+    spec = K.KVSpec(L, H, D, bs)
+    rng = np.random.default_rng(300)
+    sizes = rng.integers(1, 7, size=300)
+    n = int(sizes.sum())
+    S = n + 40
+    weights = [2, 1, 1]                      # a 3-block set already reaches the staging region
+    caps = [((w * n // sum(weights) + 320) * spec.block_bytes + 4095) // 4096 * 4096 for w in weights]
+    regions = [K.Region("host", caps[0], 0), K.Region("staging", caps[1]), K.Region("host", caps[2], 0)]
+    say("case many requests", n, "sdma", sdma)
+    dev = torch.device("cuda", 0)
+    tags = tag_cache(L, S, H, bs, D)
+    src = torch.from_numpy(tags).to(dev)
+    sentinel = np.int16(np.uint16(SENTINEL).view(np.int16))
+    dst = torch.full(tuple(tags.shape), int(sentinel), dtype=torch.int16, device=dev)
+    kp = lambda t: [t[l, 0].data_ptr() for l in range(L)]           # noqa: E731
+    vp = lambda t: [t[l, 1].data_ptr() for l in range(L)]           # noqa: E731
+    src_slots = rng.permutation(S)[:n].astype(np.int32)
+    dst_slots = rng.permutation(S)[:n].astype(np.int32)
+    with K.KVPool(regions, weights, spec, 0) as pool:
+        if sdma:
+            pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+            pool.set_launch(K.CLASS_HOST, K.OP_STORE, 0, K.LAUNCH_SDMA)
+        m = np.concatenate([pool.place(1000 + i, int(c)) for i, c in enumerate(sizes)])
+        s = torch.cuda.current_stream().cuda_stream
+        pool.store(m, src_slots, S, kp(src), vp(src), s)
+        pool.retrieve(m, dst_slots, S, kp(dst), vp(dst), s)
+        torch.cuda.synchronize()
+        check_tags(tags, dst.cpu().numpy(), src_slots, dst_slots, sentinel)
+        for i in range(len(sizes)):
+            pool.release(1000 + i)
