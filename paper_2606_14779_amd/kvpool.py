@@ -166,6 +166,29 @@ def _block_count(n) -> int:
     return n
 
 
+def _struct(cls, *vals):
+    """A ctypes structure of the ABI, each integer field checked against its type's range first."""
+    for (name, t), v in zip(cls._fields_, vals):
+        lo, hi = _RANGES[t]
+        if not lo <= operator.index(v) < hi:
+            raise ValueError("%s.%s = %d is outside [%d, %d)" % (cls.__name__, name, v, lo, hi))
+    return cls(*vals)
+
+
+def _int_array(t, dtype, what) -> np.ndarray:
+    """An integer array as the ABI's element type; entries of another integer type are checked
+    against that type's range, not wrapped."""
+    a = np.asarray(t)
+    dt = np.dtype(dtype)
+    if a.dtype != dt and a.size:
+        if a.dtype.kind not in "iu":
+            raise ValueError("%s must hold integers" % what)
+        info = np.iinfo(dt)
+        if int(a.min()) < info.min or int(a.max()) > info.max:
+            raise ValueError("%s entry outside the range of %s" % (what, dt.name))
+    return np.ascontiguousarray(a, dtype=dt)
+
+
 def _loc_array(m) -> np.ndarray:
     a = np.ascontiguousarray(m, dtype=LOC_DTYPE)
     return a
@@ -199,7 +222,7 @@ class KVSpec:
 
 def counts(bandwidths, n: int) -> np.ndarray:
     """The library's per-region target counts for n blocks (kv_pool_counts)."""
-    bw = np.ascontiguousarray(bandwidths, dtype=np.uint64)
+    bw = _int_array(bandwidths, np.uint64, "bandwidths")
     out = np.zeros(len(bw), dtype=np.uint64)
     _check(_lib.kv_pool_counts(bw.ctypes.data if len(bw) else None, len(bw), n, out.ctypes.data))
     return out
@@ -246,13 +269,13 @@ class KVPool:
         descs = (_RegionDesc * n)()
         for i, r in enumerate(regions):
             kind = {"host": REGION_HOST, "staging": REGION_STAGING}[r.kind]
-            descs[i] = _RegionDesc(kind, r.numa_node, r.capacity_bytes, r.coherence, 0)
-        bw = None if bandwidths is None else np.ascontiguousarray(bandwidths, dtype=np.uint64)
+            descs[i] = _struct(_RegionDesc, kind, r.numa_node, r.capacity_bytes, r.coherence, 0)
+        bw = None if bandwidths is None else _int_array(bandwidths, np.uint64, "bandwidths")
         if bw is not None and len(bw) != n:
             raise ValueError("one bandwidth per region")
         self.spec = spec
         self.n_regions = n
-        cs = _KVSpec(spec.num_layers, spec.num_kv_heads, spec.head_dim, spec.block_size,
+        cs = _struct(_KVSpec, spec.num_layers, spec.num_kv_heads, spec.head_dim, spec.block_size,
                      spec.elem_bytes, spec.pool_layout)
         h = ctypes.c_void_p()
         _check(_lib.kv_pool_create(ctypes.addressof(descs), None if bw is None else bw.ctypes.data, n,
@@ -299,7 +322,7 @@ class KVPool:
     # ---- data path
     def _transfer(self, fn, loc_map, table, num_slots, k_ptrs, v_ptrs, stream, layers=None):
         m = _loc_array(loc_map)
-        t = np.ascontiguousarray(table, dtype=np.int32)
+        t = _int_array(table, np.int32, "block table")
         if len(m) != len(t):
             raise ValueError("map and block table differ in length")
         ks, vs = _ptrs(k_ptrs), _ptrs(v_ptrs)
@@ -317,7 +340,7 @@ class KVPool:
         self._transfer(_lib.kv_pool_retrieve, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream)
 
     def retrieve_request(self, request: int, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
-        t = np.ascontiguousarray(dst_table, dtype=np.int32)
+        t = _int_array(dst_table, np.int32, "block table")
         ks, vs = _ptrs(k_ptrs), _ptrs(v_ptrs)
         if len(ks) != self.spec.num_layers or len(vs) != self.spec.num_layers:
             raise ValueError("one K and one V pointer per layer")
@@ -356,7 +379,7 @@ class KVPool:
         return out
 
     def set_bandwidths(self, bandwidths) -> None:
-        bw = np.ascontiguousarray(bandwidths, dtype=np.uint64)
+        bw = _int_array(bandwidths, np.uint64, "bandwidths")
         if len(bw) != self.n_regions:
             raise ValueError("one bandwidth per region")
         _check(_lib.kv_pool_set_bandwidths(self._h, bw.ctypes.data))

@@ -271,6 +271,14 @@ def test_binding_rejects_integers_outside_their_c_type():
         call[ints[-1]] = K._RANGES[args[ints[-1]]][1]                   # one past the type's maximum
         with pytest.raises(ValueError, match=name):
             getattr(K._lib, name)(*call)
+    with pytest.raises(ValueError, match="block table"):            # int64 table: checked, not wrapped
+        p.retrieve(m, np.array([0, 2 ** 32 + 1], np.int64), 2, ptrs, ptrs)
+    with pytest.raises(ValueError, match="bandwidths"):
+        p.set_bandwidths(np.array([-1], np.int64))
+    with pytest.raises(ValueError, match="capacity_bytes"):
+        K.KVPool([K.Region("host", -4096)], [1], spec, device=-1)
+    with pytest.raises(ValueError, match="num_layers"):
+        K.KVPool([K.Region("host", 1 << 20)], [1], K.KVSpec(-1, 1, 8), device=-1)
     assert np.array_equal(p.lookup(1, 2), m)                      # nothing reached the pool
     p.close()
 
