@@ -28,6 +28,7 @@ void target_counts(const uint64_t *bandwidth, uint32_t n_dev, uint64_t n_blocks,
         if (bandwidth[i] == 0) fail(KVP_ERR_INVALID, "bandwidth of region " + std::to_string(i) + " is 0");
         sum_b += bandwidth[i];
     }
+    std::vector<uint32_t> rank(n_dev);   // allocated before counts is written: a failure leaves it as it was
     // floor(p_i * n) = floor(b_i * n / sum b), exact in 128-bit integers
     uint64_t floors = 0;
     for (uint32_t i = 0; i < n_dev; ++i) {
@@ -36,7 +37,6 @@ void target_counts(const uint64_t *bandwidth, uint32_t n_dev, uint64_t n_blocks,
     }
     // sum of the fractional parts is below n_dev, so fewer than n_dev leftovers
     const uint64_t leftover = n_blocks - floors;
-    std::vector<uint32_t> rank(n_dev);
     std::iota(rank.begin(), rank.end(), 0u);
     std::stable_sort(rank.begin(), rank.end(),
                      [&](uint32_t a, uint32_t b) { return bandwidth[a] > bandwidth[b]; });

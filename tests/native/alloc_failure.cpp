@@ -1,8 +1,10 @@
 // Host allocation failures inside place and extend, through the C ABI of the
 // host-sanitized library on placement-only pools (no GPU).
 //
-// Two pools go through the same random sequence of place / extend / release
-// calls.  On pool A every call is first tried with the k-th host allocation
+// Creating a pool and computing Eq. 2 counts are tried the same way first
+// (a failed create returns no pool and leaks nothing; a failed count writes
+// nothing).  Then two pools go through the same random sequence of place /
+// extend / release calls.  On pool A every call is first tried with the k-th host allocation
 // made inside it failing (k = 0, 1, 2, ... until the call makes fewer than k
 // allocations); each such try must return KVP_ERR_NOMEM (or the call's own
 // error code, with a fixed message, when the failure hits the copy of its
@@ -81,7 +83,34 @@ int main()
             regions[i] = kvp_region_desc{KVP_REGION_HOST, -1, (w[i] * 20 + 5) * bb + 4096, 0, 0};
         }
         kvp_pool *A = nullptr, *B = nullptr;
-        CHECK(kv_pool_create(regions.data(), w.data(), N, &spec, -1, &A) == KVP_OK);
+        for (long k = 0;; ++k) {                            // create: nothing leaks, no pool comes back
+            g_countdown = k;
+            const int rc = kv_pool_create(regions.data(), w.data(), N, &spec, -1, &A);
+            const bool failed_here = g_countdown < 0;
+            g_countdown = -1;
+            if (!failed_here) {
+                CHECK(rc == KVP_OK && A);
+                break;
+            }
+            CHECK(rc == KVP_ERR_NOMEM && A == nullptr);
+            ++injected;
+            CHECK(k < 100000);
+        }
+        std::vector<uint64_t> c(N, 7), c_ok(N);               // Eq. 2 counts: all written or none
+        CHECK(kv_pool_counts(w.data(), N, 1000, c_ok.data()) == KVP_OK);
+        for (long k = 0;; ++k) {
+            g_countdown = k;
+            const int rc = kv_pool_counts(w.data(), N, 1000, c.data());
+            const bool failed_here = g_countdown < 0;
+            g_countdown = -1;
+            if (!failed_here) {
+                CHECK(rc == KVP_OK && c == c_ok);
+                break;
+            }
+            CHECK(rc == KVP_ERR_NOMEM);
+            for (uint64_t x : c) CHECK(x == 7);
+            ++injected;
+        }
         CHECK(kv_pool_create(regions.data(), w.data(), N, &spec, -1, &B) == KVP_OK);
         std::map<uint64_t, std::vector<kvp_loc>> live;      // request -> its map on both pools
         uint64_t next_req = 1;
