@@ -401,3 +401,19 @@ int main(void)
                    check=True, capture_output=True, text=True)
     r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0 and "c client ok" in r.stdout, r.stdout + r.stderr
+
+
+def test_binding_raises_without_the_library(tmp_path):
+    """No fallback: the binding, imported from a package directory that holds no libkvpool.so,
+    raises ImportError instead of loading anything else."""
+    import shutil
+    import subprocess
+    import sys
+    pkg = tmp_path / "kvp_copy"
+    pkg.mkdir()
+    (pkg / "__init__.py").write_text("")
+    shutil.copy(os.path.join(ROOT, "paper_2606_14779_amd", "kvpool.py"), pkg / "kvpool.py")
+    r = subprocess.run([sys.executable, "-c", "import kvp_copy.kvpool"], cwd=tmp_path, capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "libkvpool.so is not built" in r.stderr, r.stderr
