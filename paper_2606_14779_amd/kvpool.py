@@ -288,7 +288,10 @@ class KVPool:
             self._h = ctypes.c_void_p()
 
     def __del__(self):
-        self.close()
+        try:
+            self.close()
+        except Exception:   # interpreter shutdown: module globals may already be gone
+            pass
 
     def __enter__(self):
         return self
