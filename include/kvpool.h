@@ -251,7 +251,9 @@ int kv_pool_store_layers(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
  */
 int kv_pool_release(kvp_pool *pool, uint64_t request_id);
 
-/* Destroy the pool: waits for its internal streams, frees everything.  NULL is a no-op. */
+/* Destroy the pool: waits for its internal streams and for every store / retrieve
+ * it enqueued, then frees everything.  NULL is a no-op.  No other call on the
+ * pool may be running in another thread, or start afterwards. */
 void kv_pool_destroy(kvp_pool *pool);
 
 /* Message for the calling thread's last failed call ("" if none). */
