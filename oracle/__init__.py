@@ -109,7 +109,16 @@ class Pool:
 
     __del__ = close
 
+    @staticmethod
+    def _count(n) -> int:
+        # the C side takes uint32_t; ctypes would wrap a negative count into a huge one
+        n = int(n)
+        if not 0 <= n < 1 << 32:
+            raise ValueError("block count %d outside [0, 2^32)" % n)
+        return n
+
     def place(self, request: int, n_blocks: int) -> np.ndarray:
+        n_blocks = self._count(n_blocks)
         out = np.zeros(n_blocks, dtype=LOC_DTYPE)
         rc = _load().oracle_place(self._p, request, n_blocks, out.ctypes.data)
         if rc:
@@ -117,12 +126,14 @@ class Pool:
         return out
 
     def try_place(self, request: int, n_blocks: int):
+        n_blocks = self._count(n_blocks)
         out = np.zeros(max(n_blocks, 1), dtype=LOC_DTYPE)
         rc = _load().oracle_place(self._p, request, n_blocks, out.ctypes.data)
         return rc, out[:n_blocks]
 
     def extend(self, request: int, n_new: int) -> np.ndarray:
         """The next offload set of a placed request: entries of its blocks n_old .. n_old+n_new-1."""
+        n_new = self._count(n_new)
         out = np.zeros(n_new, dtype=LOC_DTYPE)
         rc = _load().oracle_extend(self._p, request, n_new, out.ctypes.data)
         if rc:
@@ -130,11 +141,13 @@ class Pool:
         return out
 
     def try_extend(self, request: int, n_new: int):
+        n_new = self._count(n_new)
         out = np.zeros(max(n_new, 1), dtype=LOC_DTYPE)
         rc = _load().oracle_extend(self._p, request, n_new, out.ctypes.data)
         return rc, out[:n_new]
 
     def lookup(self, request: int, n_blocks: int) -> np.ndarray:
+        n_blocks = self._count(n_blocks)
         out = np.zeros(n_blocks, dtype=LOC_DTYPE)
         rc = _load().oracle_lookup(self._p, request, n_blocks, out.ctypes.data)
         if rc:
