@@ -19,8 +19,11 @@
  *   - Return 0 (KVP_OK) on success or a negative KVP_ERR_* code.  Nothing
  *     throws across the ABI.  kv_pool_last_error() gives a message for the
  *     calling thread's last failure.
- *   - All arguments are checked before any GPU work is enqueued; a failed
- *     call has no side effects.
+ *   - All arguments are checked before any GPU work is enqueued.  A call
+ *     that fails (its checks, or the library's host memory running out) has
+ *     no side effects, with one exception: a HIP runtime error
+ *     (KVP_ERR_HIP) met while a store or retrieve enqueues its work may
+ *     leave part of that work enqueued.
  *   - "stream" is a hipStream_t passed as void* (NULL = the null stream).
  *   - Host arrays passed in (maps, block tables, pointer tables) may be freed
  *     as soon as the call returns: the library copies what it keeps.
