@@ -213,6 +213,38 @@ int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
                      void *const *k_layers, void *const *v_layers, void *stream);
 
 /*
+ * Allocation-free retrieve, for callers that cannot allocate memory during the
+ * call (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, semantics, validation, stream ordering
+ * and results as kv_pool_retrieve, except:
+ *   - The work list (the engine pointers of the moved chunks, 8 bytes each,
+ *     rounded up to 16, then 16 bytes per present block) goes through a
+ *     static device array of KVP_NOALLOC_SCRATCH_BYTES (1 MiB) that the
+ *     library holds once per GPU from the first kv_pool_create on that GPU
+ *     until the process ends, with a pinned host buffer of the same size set
+ *     up beside it.  A call whose list is larger -- more than 65,504 present
+ *     blocks for a 32-layer model -- fails with KVP_ERR_INVALID before any
+ *     work is enqueued.
+ *   - The call makes no device or pinned allocation (no hipMalloc,
+ *     hipHostMalloc, hipFree or other allocating routine) and creates no
+ *     stream or event.  The host class always runs the zero-copy kernel
+ *     (KVP_LAUNCH_SDMA is ignored: its ring is memory of its own); the call
+ *     is never a small-call launch and is not timed.
+ *   - The array is shared by every pool and every call on that GPU, and it
+ *     keeps the last call's list; nothing in it needs to start at zero.  The
+ *     library orders its users: a call's upload waits on the device for the
+ *     kernels of the previous such call on that GPU (any pool, any stream),
+ *     and the host waits, if need be, until the previous call's upload has
+ *     left the pinned buffer.  Calls on one GPU therefore run in the order
+ *     they were enqueued rather than overlapping.
+ * Errors: as kv_pool_retrieve.
+ */
+#define KVP_NOALLOC_SCRATCH_BYTES (1u << 20)
+int kv_pool_retrieve_noalloc(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,
+                             const int32_t *dst_block_table, uint32_t dst_num_slots,
+                             void *const *k_layers, void *const *v_layers, void *stream);
+
+/*
  * Retrieve by request (Sec. 4.3 as one call): read the GLT entries of blocks
  * 0..n_blocks-1 of request_id, then retrieve them exactly as kv_pool_retrieve
  * does with that map.  n_blocks must equal the request's block count over

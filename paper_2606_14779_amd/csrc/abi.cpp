@@ -16,7 +16,7 @@ void pool_lookup(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_lookup_vector(Pool &, uint64_t, uint32_t, std::vector<kvp_loc> &);
 void pool_release(Pool &, uint64_t);
 void pool_transfer(Pool &, const kvp_loc *, uint32_t, const int32_t *, uint32_t, uint32_t, uint32_t,
-                   void *const *, void *const *, void *, bool);
+                   void *const *, void *const *, void *, bool, bool = false);
 void pool_region_info(const Pool &, uint32_t, kvp_region_info *);
 void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
 void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
@@ -142,6 +142,16 @@ int kv_pool_retrieve(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, cons
         kvp::Pool &p = impl(pool);
         kvp::pool_transfer(p, map, n_blocks, dst_block_table, dst_num_slots, 0, p.spec.num_layers, k_layers,
                            v_layers, stream, true);
+    });
+}
+
+int kv_pool_retrieve_noalloc(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks, const int32_t *dst_block_table,
+                             uint32_t dst_num_slots, void *const *k_layers, void *const *v_layers, void *stream)
+{
+    return guarded([&] {
+        kvp::Pool &p = impl(pool);
+        kvp::pool_transfer(p, map, n_blocks, dst_block_table, dst_num_slots, 0, p.spec.num_layers, k_layers,
+                           v_layers, stream, true, true);
     });
 }
 

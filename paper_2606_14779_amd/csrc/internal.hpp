@@ -169,6 +169,33 @@ struct TimedCall {                // one store / retrieve recorded while timing 
     bool ran[2] = {false, false};
 };
 
+// Work-list scratch of kv_pool_retrieve_noalloc: one static device array per
+// GPU (kernels.hip), shared by every pool and call on that GPU.  `dev` is the
+// array's device address on that GPU (never the array's host-side name);
+// `host` is a pinned buffer of the same size, allocated once with it, in
+// which the host writes a call's list before the upload.  `staged` is
+// recorded after a call's upload (the host buffer may then be rewritten),
+// `free` after its kernels (the device array may then be overwritten).
+// Nothing here is ever released: each GPU keeps them until the process ends,
+// and no destructor makes a HIP call at exit.
+constexpr uint64_t kScratchBytes = 1ull << 20;
+
+struct ScratchDevice {
+    std::mutex mu;          // serialises the calls that use the array, in enqueue order
+    bool ready = false;
+    void *dev = nullptr;
+    void *host = nullptr;
+    hipEvent_t staged = nullptr, free = nullptr;
+    bool staged_rec = false, free_rec = false;
+};
+
+// Set up the scratch of `device` (the current device) on first use: the
+// array's address by hipGetSymbolAddress, the pinned buffer and the events.
+// Thread safe.  Throws HIP / NOMEM.
+ScratchDevice &scratch_setup(int device);
+// The scratch of a device whose set-up is done (INVALID otherwise); allocates nothing.
+ScratchDevice &scratch_device(int device);
+
 constexpr uint32_t kBounceSlots = 2;                 // copy-engine transport: ring slots
 constexpr uint64_t kBounceSlotMin = 1ull << 30;      //   default bytes per slot (one block at least)
 

@@ -334,6 +334,61 @@ __global__ __launch_bounds__(kThreads) void probe_copy_kernel(const v4u *__restr
     }
 }
 
+// ---------------------------------------------------------------- static work-list scratch
+
+// The work list of kv_pool_retrieve_noalloc lives here instead of in memory
+// the library allocates.  Host code never passes this name to a kernel or a
+// copy: on the host it is only a stand-in for the symbol, and its device
+// address (one per GPU) comes from hipGetSymbolAddress in scratch_setup.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+ScratchDevice g_scratch[kMaxScratchDevices];
+std::mutex g_scratch_setup;
+}  // namespace
+
+ScratchDevice &scratch_setup(int device)
+{
+    if (device < 0 || device >= kMaxScratchDevices)
+        fail(KVP_ERR_INVALID, "device " + std::to_string(device) + " outside the scratch table");
+    ScratchDevice &sd = g_scratch[device];
+    std::lock_guard<std::mutex> lock(g_scratch_setup);
+    if (sd.ready) return sd;
+    void *dev = nullptr;
+    check_hip(hipGetSymbolAddress(&dev, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!dev || (reinterpret_cast<uintptr_t>(dev) & 255))
+        fail(KVP_ERR_HIP, "scratch symbol has no 256-byte aligned device address");
+    void *host = nullptr;
+    if (hipHostMalloc(&host, kScratchBytes, hipHostMallocDefault) != hipSuccess || !host) {
+        clear_hip_error();
+        fail(KVP_ERR_NOMEM, "pinned staging buffer of the static scratch");
+    }
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    for (auto &e : ev) {
+        const hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (r != hipSuccess) {
+            for (auto &x : ev)
+                if (x) (void)hipEventDestroy(x);
+            (void)hipHostFree(host);
+            check_hip(r, "hipEventCreate");
+        }
+    }
+    sd.dev = dev;
+    sd.host = host;
+    sd.staged = ev[0];
+    sd.free = ev[1];
+    sd.ready = true;
+    return sd;
+}
+
+ScratchDevice &scratch_device(int device)
+{
+    if (device < 0 || device >= kMaxScratchDevices || !g_scratch[device].ready)
+        fail(KVP_ERR_INVALID, "static scratch of device " + std::to_string(device) + " is not set up");
+    return g_scratch[device];
+}
+
 // ---------------------------------------------------------------- host-side dispatch
 
 constexpr uint32_t kClassSmall = 3;   // dispatch only: small_call_copy

@@ -316,6 +316,7 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         for (auto &e : p->link_done) check_hip(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate");
         p->ring.resize(kRingSlots);
         for (auto &s : p->ring) check_hip(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreate");
+        (void)scratch_setup(hip_device);   // once per device: the static work-list scratch
         if (!bandwidths) {
             // Eq. 1 from measured bandwidths: each region's read rate into HBM
             std::vector<uint64_t> mbps(n_regions);

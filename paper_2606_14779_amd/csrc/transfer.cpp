@@ -136,9 +136,14 @@ void drain_timed(Pool &p, kvp_timing_summary *sum)
     if (sum) *sum = s;
 }
 
+// noalloc (retrieve only): the work list goes through the device's static
+// scratch instead of the upload ring, and the host class always takes the
+// zero-copy kernel (the copy-engine ring is memory of its own); no small-call
+// launch and no timing, so that the call makes no allocation and creates no
+// HIP object.
 void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t *table, uint32_t num_slots,
                    uint32_t layer_begin, uint32_t layer_end, void *const *k_layers, void *const *v_layers,
-                   void *stream_ptr, bool gather)
+                   void *stream_ptr, bool gather, bool noalloc)
 {
     if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to copy");
     if (n_blocks && (!map || !table)) fail(KVP_ERR_INVALID, "null map or block table");
@@ -157,7 +162,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::lock_guard<std::mutex> lock(p.mu);
     DeviceScope dev(p.device);
     const uint32_t op = gather ? KVP_OP_RETRIEVE : KVP_OP_STORE;
-    const bool sdma = (p.launch[KVP_CLASS_HOST][op].flags & KVP_LAUNCH_SDMA) != 0;
+    if (noalloc && !gather) fail(KVP_ERR_INVALID, "the static-scratch path is a retrieve");
+    const bool sdma = !noalloc && (p.launch[KVP_CLASS_HOST][op].flags & KVP_LAUNCH_SDMA) != 0;
     if (sdma && !p.bounce)   // only after a kv_pool_set_copy_ring that could not allocate
         fail(KVP_ERR_NOMEM, "copy-engine ring not allocated: set a smaller ring or clear KVP_LAUNCH_SDMA");
 
@@ -249,7 +255,12 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     }
 
     const size_t n_items = items[0].size() + items[1].size();
-    if (p.timing) {
+    const size_t ptr_bytes = round_up(static_cast<size_t>(2 * (layer_end - layer_begin)) * sizeof(uint64_t), 16);
+    const size_t list_bytes = ptr_bytes + n_items * sizeof(CopyItem);
+    if (noalloc && list_bytes > kScratchBytes)
+        fail(KVP_ERR_INVALID, "work list of " + std::to_string(list_bytes) + " bytes (" + std::to_string(n_items) +
+                                  " blocks) exceeds the static scratch of " + std::to_string(kScratchBytes) + " bytes");
+    if (p.timing && !noalloc) {
         if (p.timed.size() >= kMaxTimedCalls) drain_timed(p, nullptr);   // bound the history
         TimedCall tc;
         for (int c = 0; c < 2; ++c) {
@@ -325,7 +336,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             check_hip(q, "hipEventQuery");
         }
     }
-    if (batches.empty() && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
+    if (!noalloc && batches.empty() && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
         chunks + 2 * n_items <= kInlineWords) {
         // Small call: table and items in the kernel arguments, both classes in
         // one launch in the host class's copy form (the link-bound part; the
@@ -345,12 +356,27 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         return;
     }
 
-    // work list: [chunks cache pointers][host items][staging items]
-    const size_t ptr_bytes = round_up(static_cast<size_t>(chunks) * sizeof(uint64_t), 16);
-    const size_t bytes = ptr_bytes + n_items * sizeof(CopyItem);
-    Slot &slot = acquire_slot(p, bytes);
-    fill_table(static_cast<uint64_t *>(slot.host));
-    auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(slot.host) + ptr_bytes);
+    // work list: [chunks cache pointers][host items][staging items], in a
+    // ring slot of the pool, or in the device's static scratch (noalloc)
+    const size_t bytes = list_bytes;
+    Slot *slot = nullptr;
+    ScratchDevice *sd = nullptr;
+    std::unique_lock<std::mutex> scratch_lock;
+    void *host_list = nullptr, *dev_base = nullptr;
+    if (noalloc) {
+        sd = &scratch_device(p.device);   // set up when the pool was created
+        scratch_lock = std::unique_lock<std::mutex>(sd->mu);
+        // the pinned buffer is rewritten only after the previous upload from it
+        if (sd->staged_rec) check_hip(hipEventSynchronize(sd->staged), "hipEventSynchronize");
+        host_list = sd->host;
+        dev_base = sd->dev;
+    } else {
+        slot = &acquire_slot(p, bytes);
+        host_list = slot->host;
+        dev_base = slot->dev;
+    }
+    fill_table(static_cast<uint64_t *>(host_list));
+    auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(host_list) + ptr_bytes);
     std::copy(items[0].begin(), items[0].end(), list);
     std::copy(items[1].begin(), items[1].end(), list + items[0].size());
 
@@ -363,7 +389,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     // on a pending event from another stream is what costs).  The slot is free
     // on the device: it was reclaimed only after the last call that read it.
     bool ahead = false;
-    if (hipPeekAtLastError() == hipSuccess) {   // never clear an error the caller has yet to read
+    if (!noalloc && hipPeekAtLastError() == hipSuccess) {   // never clear an error the caller has yet to read
         const hipError_t q = hipStreamQuery(s);
         if (q == hipErrorNotReady) {
             (void)hipGetLastError();   // "not ready" is the answer, not an error to leave behind
@@ -372,16 +398,25 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             check_hip(q, "hipStreamQuery");
         }
     }
-    check_hip(hipMemcpyAsync(slot.dev, slot.host, bytes, hipMemcpyHostToDevice, ahead ? p.s_stage : s),
-              "hipMemcpyAsync");
-    slot.pending = true;  // from here on the slot is in use even if a launch fails
+    if (noalloc) {
+        // the array is overwritten only after the previous call's kernels
+        // (from any pool, on any stream) have read it
+        if (sd->free_rec) check_hip(hipStreamWaitEvent(s, sd->free, 0), "hipStreamWaitEvent");
+        check_hip(hipMemcpyAsync(dev_base, host_list, bytes, hipMemcpyHostToDevice, s), "hipMemcpyAsync");
+        check_hip(hipEventRecord(sd->staged, s), "hipEventRecord");
+        sd->staged_rec = true;
+    } else {
+        check_hip(hipMemcpyAsync(dev_base, host_list, bytes, hipMemcpyHostToDevice, ahead ? p.s_stage : s),
+                  "hipMemcpyAsync");
+        slot->pending = true;  // from here on the slot is in use even if a launch fails
+    }
     if (ahead) {
         check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
         check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
     }
     if (fork_staging || !batches.empty()) check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
 
-    const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(slot.dev) + ptr_bytes);
+    const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(dev_base) + ptr_bytes);
     // Staging class forked onto the internal stream first, then the host
     // class on the caller's stream itself; the caller's stream then waits for
     // the staging kernel.  One extra stream keeps the pool within the few
@@ -391,11 +426,11 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     CopyArgs args[2] = {geo, geo};
     for (uint32_t c = 0; c < 2; ++c) {
         args[c].items = dev_list + first;
-        args[c].cache = static_cast<const uint64_t *>(slot.dev);
+        args[c].cache = static_cast<const uint64_t *>(dev_base);
         args[c].n_items = static_cast<uint32_t>(items[c].size());
         first += items[c].size();
     }
-    TimedCall *tc = p.timing ? &p.timed.back() : nullptr;
+    TimedCall *tc = p.timing && !noalloc ? &p.timed.back() : nullptr;
     auto launch = [&](uint32_t c, hipStream_t st) {
         const LaunchCfg &lc = c == KVP_CLASS_HOST ? lh : p.launch[c][op];
         if (tc) check_hip(hipEventRecord(tc->t0[c], st), "hipEventRecord");
@@ -486,7 +521,12 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             tc->ran[KVP_CLASS_HOST] = true;
         }
     }
-    check_hip(hipEventRecord(slot.done, s), "hipEventRecord");
+    if (noalloc) {
+        check_hip(hipEventRecord(sd->free, s), "hipEventRecord");
+        sd->free_rec = true;
+    } else {
+        check_hip(hipEventRecord(slot->done, s), "hipEventRecord");
+    }
     mark_requests();
 }
 

@@ -91,6 +91,7 @@ _SIGS = {
     "kv_pool_store": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve_request": (_i32, [_vp, _u64, _u32, _vp, _u32, _vp, _vp, _vp]),
+    "kv_pool_retrieve_noalloc": (_i32, [_vp, _vp, _u32, _vp, _u32, _vp, _vp, _vp]),
     "kv_pool_retrieve_layers": (_i32, [_vp, _vp, _u32, _vp, _u32, _u32, _u32, _vp, _vp, _vp]),
     "kv_pool_store_layers": (_i32, [_vp, _vp, _u32, _vp, _u32, _u32, _u32, _vp, _vp, _vp]),
     "kv_pool_release": (_i32, [_vp, _u64]),
@@ -341,6 +342,9 @@ class KVPool:
 
     def retrieve(self, loc_map, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
         self._transfer(_lib.kv_pool_retrieve, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream)
+
+    def retrieve_noalloc(self, loc_map, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
+        self._transfer(_lib.kv_pool_retrieve_noalloc, loc_map, dst_table, dst_num_slots, k_ptrs, v_ptrs, stream)
 
     def retrieve_request(self, request: int, dst_table, dst_num_slots: int, k_ptrs, v_ptrs, stream: int = 0):
         t = _int_array(dst_table, np.int32, "block table")
