@@ -104,102 +104,319 @@ def probes(torch, K, run, nbytes):
     return res
 
 
-def pmc_traffic(wl_name, kernel_prefix):
-    """HBM/fabric bytes per dispatch from the committed rocprofv3 PMC summary of this workload.
+# rocprofv3 counter passes behind the PMC summaries in profiles/.  Each pass is one run of
+#   rocprofv3 --pmc <counters> --output-format csv -d gpurun_out/pmc_<tag>/<pass> -o <pass> -- python3 bench.py <args>
+# (at most 4 TCC counters per pass on gfx950); then `python3 bench.py --summarize-pmc gpurun_out/pmc_<tag>
+# --tag <tag> --bench-args "<args>"` writes profiles/retrieve_<tag>_pmc.txt.
+PMC_PASSES = [
+    ("fetch", ["FETCH_SIZE"]),
+    ("write", ["WRITE_SIZE"]),
+    ("rd", ["TCC_EA0_RDREQ_DRAM_32B_sum", "TCC_EA0_RDREQ_IO_32B_sum", "TCC_EA0_RDREQ_GMI_32B_sum"]),
+    ("wr", ["TCC_EA0_WRREQ_WRITE_DRAM_32B_sum", "TCC_EA0_WRREQ_WRITE_IO_32B_sum", "TCC_EA0_WRREQ_WRITE_GMI_32B_sum"]),
+    ("req", ["TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_128B_sum", "TCC_BUBBLE_sum"]),
+    ("utcl", ["TCP_UTCL1_TRANSLATION_MISS_sum", "TCP_UTCL1_TRANSLATION_HIT_sum", "TCP_UTCL1_STALL_MULTI_MISS_sum",
+              "TCP_PENDING_STALL_CYCLES_sum"]),
+    ("stall", ["TCC_EA0_WRREQ_STALL_sum", "TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum",
+               "TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum", "TCC_TAG_STALL_sum"]),
+    ("lat", ["TCC_EA0_RDREQ_LEVEL_sum", "TCC_EA0_WRREQ_LEVEL_sum", "TCC_EA0_WRREQ_sum", "GRBM_GUI_ACTIVE"]),
+]
+PROBE_COPY_BYTES = 4 << 30          # bytes one probe-copy dispatch of the bench reads and writes
+
+
+def kernels_sha():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2606_14779_amd", "csrc", "kernels.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()
+
+
+def summarize_pmc(d, tag, bench_args, out_dir=None):
+    """profiles/retrieve_<tag>_pmc.txt from the counter passes under d (one directory per pass).
+
+    Per (kernel, workgroups): the mean per dispatch of every counter, and bytes:
+      fetch_bytes / write_bytes  FETCH_SIZE / WRITE_SIZE (KiB) x 1024, each scaled so that the
+                                 bench's 4 GiB probe copy reads / writes exactly 4 GiB;
+      rd_* / wr_* _bytes         32 x the per-destination 32-byte request counts (dram = HBM,
+                                 io = the host link, gmi = another die), unscaled."""
+    import csv
+    from collections import defaultdict
+    vals = defaultdict(lambda: defaultdict(list))
+    for name, counters in PMC_PASSES:
+        path = os.path.join(d, name, name + "_counter_collection.csv")
+        if not os.path.exists(path):
+            continue
+        for t in csv.DictReader(open(path)):
+            k = t["Kernel_Name"].split("(")[0].replace("void ", "")
+            if "at::native" in k:
+                continue
+            wg = int(t["Grid_Size"]) // max(1, int(t["Workgroup_Size"]))
+            vals[(k, wg)][t["Counter_Name"]].append(float(t["Counter_Value"]))
+
+    def mean(xs):
+        return sum(xs) / len(xs)
+    probe = [v for k, v in vals.items() if "probe_copy_kernel" in k[0] and "FETCH_SIZE" in v and "WRITE_SIZE" in v]
+    fetch_scale = PROBE_COPY_BYTES / 1024 / mean([x for v in probe for x in v["FETCH_SIZE"]]) if probe else None
+    write_scale = PROBE_COPY_BYTES / 1024 / mean([x for v in probe for x in v["WRITE_SIZE"]]) if probe else None
+    short = {"TCC_EA0_RDREQ_DRAM_32B_sum": "rd_dram", "TCC_EA0_RDREQ_IO_32B_sum": "rd_io",
+             "TCC_EA0_RDREQ_GMI_32B_sum": "rd_gmi", "TCC_EA0_WRREQ_WRITE_DRAM_32B_sum": "wr_dram",
+             "TCC_EA0_WRREQ_WRITE_IO_32B_sum": "wr_io", "TCC_EA0_WRREQ_WRITE_GMI_32B_sum": "wr_gmi"}
+    lines = ["# rocprofv3 PMC summary: KV store / retrieve kernels, %s" % tag,
+             "# passes (repository root on the MI355X machine, after `cd /tmp && export TMPDIR=/tmp`), one run each:"]
+    for name, counters in PMC_PASSES:
+        lines.append("#   rocprofv3 --pmc %s --output-format csv -d gpurun_out/pmc_%s/%s -o %s -- python3 bench.py %s"
+                     % (" ".join(counters), tag, name, name, bench_args))
+    lines += ["# then: python3 bench.py --summarize-pmc gpurun_out/pmc_%s --tag %s --bench-args \"%s\""
+              % (tag, tag, bench_args),
+              "# Values are means per dispatch.  *_bytes = 32 x the 32-byte request counters, per destination",
+              "# (dram: HBM; io: the host link; gmi: another die), unscaled.  fetch_bytes / write_bytes =",
+              "# FETCH_SIZE / WRITE_SIZE x 1024 x the scale that makes the 4 GiB probe copy read / write 4 GiB.",
+              "kernels_hip_sha256: %s" % kernels_sha(),
+              "fetch_scale: %s" % ("%.6f" % fetch_scale if fetch_scale else "none"),
+              "write_scale: %s" % ("%.6f" % write_scale if write_scale else "none")]
+    for k in sorted(vals, key=lambda k: -mean(vals[k].get("FETCH_SIZE", [0.0]))):
+        v = vals[k]
+        f = ["workgroups=%d" % k[1], "dispatches=%d" % max(len(x) for x in v.values())]
+        if "FETCH_SIZE" in v:
+            f.append("fetch_size_kib=%.1f" % mean(v["FETCH_SIZE"]))
+            if fetch_scale:
+                f.append("fetch_bytes=%.0f" % (mean(v["FETCH_SIZE"]) * 1024 * fetch_scale))
+        if "WRITE_SIZE" in v:
+            f.append("write_size_kib=%.1f" % mean(v["WRITE_SIZE"]))
+            if write_scale:
+                f.append("write_bytes=%.0f" % (mean(v["WRITE_SIZE"]) * 1024 * write_scale))
+        for c, sname in short.items():
+            if c in v:
+                f.append("%s_bytes=%.0f" % (sname, 32 * mean(v[c])))
+        for c in sorted(v):
+            if c not in short and c not in ("FETCH_SIZE", "WRITE_SIZE"):
+                f.append("%s=%.0f" % (c.replace("_sum", ""), mean(v[c])))
+        lines.append("kernel: %s | %s" % (k[0], " | ".join(f)))
+    out = os.path.join(out_dir or os.path.join(ROOT, "profiles"), "retrieve_%s_pmc.txt" % tag)
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_trace(d, tag, bench_args, bench_json):
+    """profiles/retrieve_<tag>_kernel_trace.md from a rocprofv3 --kernel-trace --stats run under d
+    (output name kt) and the bench line that run printed (file bench_json)."""
+    import csv
+    from collections import defaultdict
+    stats = list(csv.DictReader(open(os.path.join(d, "kt_kernel_stats.csv"))))
+    trace = list(csv.DictReader(open(os.path.join(d, "kt_kernel_trace.csv"))))
+    per = defaultdict(list)
+    for t in trace:
+        gx = int(t.get("Grid_Size_X") or t.get("Grid_Size"))
+        wx = int(t.get("Workgroup_Size_X") or t.get("Workgroup_Size"))
+        per[(t["Kernel_Name"], gx // max(1, wx))].append((int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e6)
+    out = ["# Kernel trace summary: %s" % tag, "",
+           "Command (repository root on the MI355X machine, after `cd /tmp && export TMPDIR=/tmp`):", "",
+           "    rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/kt_%s -o kt -- python3 bench.py %s"
+           % (tag, bench_args), "",
+           "then `python3 bench.py --summarize-trace gpurun_out/kt_%s --tag %s --bench-args \"%s\" --bench-json <its "
+           "JSON line>`." % (tag, tag, bench_args), "",
+           "kernels.hip sha256: `%s`" % kernels_sha(), "", "## rocprofv3 --stats", "",
+           "| Kernel | Calls | Avg ms | Min ms | Max ms | % |", "|---|---:|---:|---:|---:|---:|"]
+    for r in stats[:16]:
+        out.append("| `%s` | %s | %.3f | %.3f | %.3f | %.2f |" % (
+            r["Name"].split("(")[0].replace("void ", "")[:100], r["Calls"], float(r["AverageNs"]) / 1e6,
+            float(r["MinNs"]) / 1e6, float(r["MaxNs"]) / 1e6, float(r["Percentage"])))
+    out += ["", "## Per launch shape", "", "| Kernel | Workgroups | Dispatches | Avg ms | Min ms |",
+            "|---|---:|---:|---:|---:|"]
+    for (name, wg), ds in sorted(per.items(), key=lambda kv: -sum(kv[1]))[:16]:
+        out.append("| `%s` | %d | %d | %.3f | %.3f |" % (name.split("(")[0].replace("void ", "")[:90], wg, len(ds),
+                                                         sum(ds) / len(ds), min(ds)))
+    if bench_json and os.path.exists(bench_json):
+        b = json.loads(open(bench_json).read().strip().splitlines()[-1])
+        rf = b.get("roofline") or {}
+        ms = (rf.get("bytes_per_launch") or 0) / (rf.get("achieved") or 1) / 1e6
+        out += ["", "## Bench line of the same run", "",
+                "    value %.2f GB/s, ms_per_step %.3f; dominant kernel %s: %.3f ms per launch (HIP events), "
+                "%s %s = %.4f of %s" % (b["value"], b["ms_per_step"], rf.get("kernel", "?").split(" ")[0], ms,
+                                        rf.get("achieved"), rf.get("unit"), rf.get("frac") or 0, rf.get("peak"))]
+    path = os.path.join(ROOT, "profiles", "retrieve_%s_kernel_trace.md" % tag)
+    open(path, "w").write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
+def pmc_traffic(wl_name, kernel_prefix, profiles_dir=None):
+    """Counter figures per dispatch of the first kernel matching kernel_prefix in the committed
+    rocprofv3 PMC summary of this workload (profiles/retrieve_<workload>_pmc.txt).
 
     Returns None when there is no summary or when kernels.hip changed since the
     counters were taken (the summary records the source's sha256)."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "retrieve_%s_pmc.txt" % wl_name)
+    path = os.path.join(profiles_dir or os.path.join(ROOT, "profiles"), "retrieve_%s_pmc.txt" % wl_name)
     if not os.path.exists(path):
         return None
-    src = os.path.join(ROOT, "paper_2606_14779_amd", "csrc", "kernels.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    rec = {}
+    rec, sha = {}, None
     for line in open(path):
         if line.startswith("kernels_hip_sha256:"):
-            rec["sha"] = line.split(":", 1)[1].strip()
-        elif line.startswith("kernel: ") and kernel_prefix in line:
-            fields = dict(f.strip().split("=", 1) for f in line.split("|")[1:])
-            rec["fetch_bytes"] = float(fields["fetch_bytes"])
-            rec["write_bytes"] = float(fields["write_bytes"])
-            rec["workgroups"] = int(fields["workgroups"])
-    if rec.get("sha") != sha or "fetch_bytes" not in rec:
+            sha = line.split(":", 1)[1].strip()
+        elif line.startswith("kernel: ") and kernel_prefix in line and not rec:
+            for f in line.split("|")[1:]:
+                k, v = f.strip().split("=", 1)
+                rec[k] = float(v)
+    if sha != kernels_sha() or "fetch_bytes" not in rec or "write_bytes" not in rec:
         return None
+    rec["source"] = os.path.relpath(path, ROOT) if profiles_dir is None else path
     return rec
 
 
-def cpu_baseline(run, wl, budget_s=10.0, max_blocks=1024):
-    """The oracle's gather (memcpy per chunk, one thread) on a bounded sample of the same request."""
+def traffic_detail(tr, alg_read, alg_write):
+    """The counter figures of one kernel beside its algorithmic bytes: HBM (DRAM) and host-link (IO)
+    bytes read and written per dispatch, and FETCH_SIZE / WRITE_SIZE scaled and unscaled."""
+    if not tr:
+        return None
+    out = {"algorithmic_read_bytes": round(alg_read), "algorithmic_write_bytes": round(alg_write),
+           "fetch_bytes": round(tr["fetch_bytes"]), "write_bytes": round(tr["write_bytes"]),
+           "fetch_size_kib_unscaled": tr.get("fetch_size_kib"), "write_size_kib_unscaled": tr.get("write_size_kib"),
+           "source": tr["source"]}
+    for k in ("rd_dram_bytes", "rd_io_bytes", "rd_gmi_bytes", "wr_dram_bytes", "wr_io_bytes", "wr_gmi_bytes"):
+        if k in tr:
+            out[k] = round(tr[k])
+    return out
+
+
+def measure_weights(torch, K, wl):
+    """Eq. 1 weights measured by the pool organizer: a pool of the workload's region kinds (1 GiB
+    each) reads 256 MiB of every region into HBM with its class's kernel; host regions share one
+    host link, so their figure is divided by their count (KVP_MEASURE_SHARED_LINK).  MB/s."""
+    regions = []
+    for r in wl.regions:
+        regions.append(K.Region("host", 1 << 30, -1) if r.kind == "host" else K.Region("staging", 1 << 30))
+    sh = wl.shape
+    spec = K.KVSpec(sh.layers, sh.kv_heads, sh.head_dim, sh.block_size, sh.elem_bytes, wl.layout)
+    with K.KVPool(regions, [1] * len(regions), spec, 0) as p:
+        w = p.measure_bandwidth(256 << 20, K.MEASURE_SHARED_LINK)
+    torch.cuda.synchronize()
+    return [int(x) for x in w]
+
+
+def round_trip_ok(torch, run, wl):
+    """Every present block's destination slot equals its source slot in every layer, and every
+    slot no block names still holds the fill value (on the GPU, layer by layer)."""
+    import numpy as np
+    from paper_2606_14779_amd.runner import SENTINEL
+    dev = run.dst.device
+    touched = np.zeros(wl.dst_num_slots, bool)
+    ok = True
+    for q in wl.requests:
+        ds = torch.from_numpy(q.dst_slots[:q.n_present].astype(np.int64)).to(dev)
+        ss = torch.from_numpy(q.src_slots.astype(np.int64)).to(dev)
+        touched[q.dst_slots[:q.n_present]] = True
+        for l in range(wl.shape.layers):
+            ok = ok and bool(torch.equal(run.dst[l].index_select(1, ds), run.src[l].index_select(1, ss)))
+    rest = torch.from_numpy(np.flatnonzero(~touched).astype(np.int64)).to(dev)
+    sent = int(np.uint16(SENTINEL).view(np.int16))
+    if len(rest):
+        for l in range(wl.shape.layers):
+            ok = ok and bool((run.dst[l].index_select(1, rest) == sent).all())
+    return ok
+
+
+def host_facts():
+    """CPU model, usable cores and NUMA layout of the machine the bench runs on."""
+    facts = {"cpu_model": None, "cores_available": len(os.sched_getaffinity(0)), "numa_nodes": {}}
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                facts["cpu_model"] = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    base = "/sys/devices/system/node"
+    try:
+        for d in sorted(os.listdir(base)):
+            if d.startswith("node") and d[4:].isdigit():
+                cpus = open(os.path.join(base, d, "cpulist")).read().strip()
+                mem_kb = None
+                for line in open(os.path.join(base, d, "meminfo")):
+                    if "MemTotal" in line:
+                        mem_kb = int(line.split()[-2])
+                facts["numa_nodes"][d[4:]] = {"cpus": cpus, "mem_gib": round(mem_kb / 2**20, 1) if mem_kb else None}
+    except OSError:
+        pass
+    return facts
+
+
+def cpu_baseline(run, wl, warmup=3, iters=10):
+    """The oracle's gather (memcpy per chunk, unmodified) over the whole request on the host cores:
+    the host regions are read where they are (pinned host memory), the staging regions (HBM) from a
+    host mirror, into a host mirror of the whole paged cache with the request's own block table.
+    Median and min of `iters` timed passes after `warmup`, on one thread and on T threads (the same
+    function, each thread over its own slice of the blocks)."""
+    import threading
+
     import numpy as np
     import oracle
     sh = wl.shape
     q = wl.requests[0]
     m = run.maps[q.request_id]
-    n = min(max_blocks, q.n_present)
-    sample = m[:n].copy()
-    # host regions are read where they are (pinned host memory); staging regions
-    # (HBM) are mirrored to host memory for the sampled blocks only
-    mem = []
+    n = q.n_present
+    regions = []
+    mirrors = []
     for r in range(len(wl.regions)):
         info = run.pool.region_info(r)
         if info["type"] == 0:
-            mem.append(info["host_ptr"])
-        else:
-            mem.append(None)
-    mirrors = []
-    for i in range(n):
-        r = int(sample["region"][i])
-        if mem[r] is None:
-            buf = run.pool.region_read(r, int(sample["offset"][i]), sh.block_bytes)
+            regions.append(info["host_ptr"])
+        else:                                    # whole staging region mirrored (its span for this request)
+            offs = m["offset"][m["region"] == r]
+            hi = int(offs.max()) + sh.block_bytes if len(offs) else 0
+            buf = run.pool.region_read(r, 0, hi) if hi else np.zeros(16, np.uint8)
             mirrors.append(buf)
-            sample["region"][i] = len(wl.regions) + len(mirrors) - 1
-            sample["offset"][i] = 0
-    regions = [m_ if m_ is not None else 0 for m_ in mem] + [b.ctypes.data for b in mirrors]
+            regions.append(buf.ctypes.data)
     L = sh.layers
-    dst = np.zeros((L, 2, n, sh.kv_heads, sh.block_size, sh.head_dim), np.uint16)
-    slots = np.arange(n, dtype=np.int32)          # destination slots renumbered 0..n-1
+    dst = np.zeros((L, 2, wl.dst_num_slots, sh.kv_heads, sh.block_size, sh.head_dim), np.uint16)
+    slots = q.dst_slots[:n].astype(np.int32)
     shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
-    oracle.gather(sample, slots, regions, [dst[l, 0] for l in range(L)], [dst[l, 1] for l in range(L)],
-                  shape, wl.layout)                # warm: touch the destination pages
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        oracle.gather(sample, slots, regions, [dst[l, 0] for l in range(L)], [dst[l, 1] for l in range(L)],
-                      shape, wl.layout)
-        passes += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or passes >= 1000:
-            break
-    gbps = passes * n * sh.block_bytes / el / 1e9
+    kd, vd = [dst[l, 0] for l in range(L)], [dst[l, 1] for l in range(L)]
 
-    # the same unmodified oracle function run on T threads at once, each over its own
-    # slice of the sample (ctypes releases the GIL during the call): context only
-    import threading
-    T = max(1, min(16, len(os.sched_getaffinity(0))))
+    def one_thread():
+        oracle.gather(m, slots, regions, kd, vd, shape, wl.layout)
+
+    T = max(1, len(os.sched_getaffinity(0)))
     bounds = np.linspace(0, n, T + 1).astype(int)
-    def one(lo, hi):
-        oracle.gather(sample[lo:hi], slots[lo:hi], regions, [dst[l, 0] for l in range(L)],
-                      [dst[l, 1] for l in range(L)], shape, wl.layout)
-    tpass, t0 = 0, time.perf_counter()
-    while True:
-        ts = [threading.Thread(target=one, args=(int(bounds[i]), int(bounds[i + 1]))) for i in range(T)]
+
+    def t_threads():
+        ts = [threading.Thread(target=oracle.gather,
+                               args=(m[bounds[i]:bounds[i + 1]], slots[bounds[i]:bounds[i + 1]], regions, kd, vd,
+                                     shape, wl.layout)) for i in range(T)]
         for t_ in ts:
             t_.start()
         for t_ in ts:
             t_.join()
-        tpass += 1
-        elt = time.perf_counter() - t0
-        if elt >= budget_s / 2 or tpass >= 1000:
-            break
-    gbps_t = tpass * n * sh.block_bytes / elt / 1e9
-    return {"value": round(gbps, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "threads": {"cores": T, "value": round(gbps_t, 3), "passes": tpass,
-                        "note": "host-to-host copies: the oracle's destination is host memory, so no host link "
-                                "is crossed; not a rate into HBM"},
-            "sample": "first %d of %d blocks (%.2f GiB; %d host-region, %d staging blocks mirrored to host), "
-                      "destination slots renumbered, %d passes in %.1f s" % (
-                          n, q.n_present, n * sh.block_bytes / 2**30, n - len(mirrors), len(mirrors), passes, el),
-            "ms_per_request_extrapolated": round(q.n_present * sh.block_bytes / (gbps * 1e9) * 1e3, 1)}
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ms = []
+        for _ in range(iters):
+            t = time.perf_counter()
+            fn()
+            ms.append((time.perf_counter() - t) * 1e3)
+        return ms
+
+    nbytes = n * sh.block_bytes
+    ms1 = timed(one_thread)
+    msT = timed(t_threads)
+    # the oracle's result is the retrieve's: spot-check it against the GPU destination
+    import torch
+    for b in (0, n // 2, n - 1):
+        got = run.dst[:, :, int(slots[b])].cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, dst[:, :, int(slots[b])]), "oracle gather and GPU retrieve differ"
+    del dst, mirrors
+
+    def row(ms, cores):
+        med = statistics.median(ms)
+        return {"cores": cores, "ms_median": round(med, 2), "ms_min": round(min(ms), 2),
+                "gbps_median": round(nbytes / med / 1e6, 3), "gbps_max": round(nbytes / min(ms) / 1e6, 3)}
+    one, multi = row(ms1, 1), row(msT, T)
+    return {"value": one["gbps_median"], "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "ms_per_request_median": one["ms_median"], "ms_per_request_min": one["ms_min"],
+            "one_thread": one, "threads": multi,
+            "sample": "the whole request: %d blocks (%.2f GiB), every host-region block read in place, every "
+                      "staging block from a host mirror, into a host mirror of the %d-slot cache; %d warm-up and "
+                      "%d timed passes per thread count" % (n, nbytes / 2**30, wl.dst_num_slots, warmup, iters),
+            "note": "host-to-host copies: the oracle's destination is host memory, so no host link is crossed",
+            "host": host_facts()}
 
 
 def ablation(args):
@@ -571,9 +788,25 @@ def main():
                     help="instead of the bench line, overlap per-layer retrieval with stand-in compute")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the bench line, compare pool organisations on the same request")
+    ap.add_argument("--measured-weights", action="store_true",
+                    help="place with Eq. 1 weights measured by the pool (kv_pool_measure_bandwidth, host regions "
+                         "sharing one link) instead of the workload's configured weights")
     ap.add_argument("--layerwise", action="store_true",
                     help="also time the request retrieved one layer per call (kv_pool_retrieve_layers)")
+    ap.add_argument("--summarize-pmc", metavar="DIR", default=None,
+                    help="write profiles/retrieve_<tag>_pmc.txt from the rocprofv3 counter passes under DIR")
+    ap.add_argument("--summarize-trace", metavar="DIR", default=None,
+                    help="write profiles/retrieve_<tag>_kernel_trace.md from a rocprofv3 kernel trace under DIR")
+    ap.add_argument("--tag", default=None, help="with --summarize-*: the workload name in the summary's file name")
+    ap.add_argument("--bench-args", default="", help="with --summarize-*: the bench arguments the runs used")
+    ap.add_argument("--bench-json", default=None, help="with --summarize-trace: file holding that run's bench line")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc, args.tag, args.bench_args)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.tag, args.bench_args, args.bench_json)
+        return
     if args.gpus == 1 and args.ablation:
         ablation(args)
         return
@@ -605,6 +838,14 @@ def main():
     torch.cuda.set_device(0)
     wl = workloads.make(args.config, layout=args.layout, context_tokens=args.context)
     sh = wl.shape
+    measured = None
+    if args.measured_weights:
+        measured = measure_weights(torch, K, wl)
+        import dataclasses
+        wl.regions = [dataclasses.replace(r, weight=int(w)) for r, w in zip(wl.regions, measured)]
+        workloads._size_regions(wl.regions, [q.n_present for q in wl.requests], sh.block_bytes)
+        wl.name += "-measured-weights"
+        log("measured weights (MB/s, host regions sharing one link):", measured)
     log("workload", wl.name, "retrieved bytes", wl.retrieved_bytes)
     t = time.perf_counter()
     run = WorkloadRun(wl, device=0, coherence=args.coherence)
@@ -723,6 +964,10 @@ def main():
                      "gbps": round(host_bytes / (avg / 1e3) / 1e9, 2)}
 
     log("timed region done: %.3f ms per retrieve" % ms_per_step)
+    # the timed steps' result: every present block of every request equals its source slot (round
+    # trip, compared on the GPU layer by layer), every other slot still holds the fill value
+    verified = round_trip_ok(torch, run, wl)
+    log("round trip verified" if verified else "ROUND TRIP MISMATCH")
     # store (offload) direction: the same request written back into its placed ranges
     store = None
     if len(wl.requests) == 1:
@@ -743,6 +988,25 @@ def main():
                  "staging_kernel_ms_avg":
                      round(sm["staging_ms_sum"] / sm["staging_calls"], 3) if sm["staging_calls"] else None}
         log("store timed: %.3f ms" % st_ms)
+        # the staging-class store alone (HBM -> HBM), from a map without the host blocks
+        if stage_blocks:
+            q = wl.requests[0]
+            m = run.maps[q.request_id].copy()
+            host_idx = [i for i, r in enumerate(wl.regions) if r.kind == "host"]
+            m["region"][np.isin(m["region"], host_idx)] = K.ABSENT
+            kp, vp = run.layer_ptrs(run.src)
+            for _ in range(args.warmup):
+                run.pool.store(m, q.src_slots, wl.src_num_slots, kp, vp, cur.cuda_stream)
+            torch.cuda.synchronize()
+            run.pool.set_timing(True)
+            for _ in range(args.steps):
+                run.pool.store(m, q.src_slots, wl.src_num_slots, kp, vp, cur.cuda_stream)
+            ss = run.pool.timing_summary()
+            run.pool.set_timing(False)
+            avg = ss["staging_ms_sum"] / ss["staging_calls"]
+            store["staging_alone"] = {"ms_avg": round(avg, 3), "ms_min": round(ss["staging_ms_min"], 3),
+                                      "copied_gbps": round(stage_bytes / (avg / 1e3) / 1e9, 1)}
+            log("staging store alone: %.3f ms" % avg)
 
     # layerwise retrieval (one call per layer, as an engine overlapping attention on layer l with the
     # fetch of layer l+1 would issue it): total time and per-layer completion spacing
@@ -793,41 +1057,69 @@ def main():
     if cpu:
         log("cpu baseline done")
 
-    dominant_ms = host_avg if host_blocks else stage_avg
+    # copy form in the kernels' names (template argument 2): 0 plain chunks; 2 token-major chunks
+    # through LDS, the library's default for every token-major kernel these figures cover
+    kform = 0 if wl.layout == 0 else 2
+    # the dominant kernel: the class whose kernel takes longer per step
+    dominant_host = bool(host_blocks) and (not stage_blocks or (host_avg or 0.0) >= (stage_avg or 0.0))
+    dominant_ms = host_avg if dominant_host else stage_avg
     # per launch: a step of a multi-request workload launches one kernel of each class per request,
     # so the algorithmic bytes of an average launch are the step's bytes over its launches
     host_per_launch = host_bytes * args.steps / summ["host_calls"] if summ["host_calls"] else host_bytes
     stage_per_launch = stage_bytes * args.steps / summ["staging_calls"] if summ["staging_calls"] else stage_bytes
-    if host_blocks:
+    if dominant_host:
         achieved = host_per_launch / (dominant_ms / 1e3) / 1e9
-        tr = pmc_traffic(wl.name, "host_region_copy<true, 0,")
+        tr = pmc_traffic(wl.name, "host_region_copy<true, %d," % kform)
         roof = {"bound": "pcie", "kernel": "host_region_copy (zero-copy gather from pinned host regions)"
                 if not args.sdma else "host class by copy engines (hipMemcpy into an HBM ring) + HBM ring scatter",
                 "achieved": round(achieved, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PCIE5_X16_GBPS, 4),
                 "traffic": round(tr["fetch_bytes"] + tr["write_bytes"]) if tr else None,
-                "traffic_detail": {"fetch_bytes": round(tr["fetch_bytes"]), "write_bytes": round(tr["write_bytes"]),
-                                   "algorithmic_read_bytes": host_per_launch, "algorithmic_write_bytes": host_per_launch,
-                                   "source": "profiles/retrieve_%s_pmc.txt" % wl.name} if tr else None,
+                "traffic_detail": traffic_detail(tr, host_per_launch, host_per_launch),
                 "bytes_per_launch": round(host_per_launch),
                 "launches_per_step": round(summ["host_calls"] / args.steps, 3),
                 "measured_peak": pr["host_link_peak_gbps"] if pr else None,
                 "frac_measured": round(achieved / pr["host_link_peak_gbps"], 4) if pr else None}
     else:
         achieved = 2 * stage_per_launch / (dominant_ms / 1e3) / 1e9
-        roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather)", "achieved": round(achieved, 1),
-                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None}
+        trs = pmc_traffic(wl.name, "staging_region_copy<true, %d," % kform)
+        copied = stage_per_launch / (dominant_ms / 1e3) / 1e9
+        roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather, beside the host-class kernel)",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": round(trs["fetch_bytes"] + trs["write_bytes"]) if trs else None,
+                "traffic_detail": traffic_detail(trs, stage_per_launch, stage_per_launch),
+                "bytes_per_launch": round(2 * stage_per_launch),
+                "launches_per_step": round(summ["staging_calls"] / args.steps, 3),
+                "copied_gbps": round(copied, 1),
+                "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
+                "frac_measured": round(copied / pr["hbm_copy_peak_gbps"], 4) if pr else None}
     hbm_roof = None
     if stage_only:
         a = 2 * stage_bytes / (stage_only["ms_avg"] / 1e3) / 1e9         # bytes read + written in HBM
-        trs = pmc_traffic(wl.name, "staging_region_copy<true, 0,")
+        trs = pmc_traffic(wl.name, "staging_region_copy<true, %d," % kform)
         hbm_roof = {"bound": "hbm", "kernel": "staging_region_copy (HBM gather, alone)", "achieved": round(a, 1),
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(a / HBM_PEAK_GBPS, 4),
                     "traffic": round(trs["fetch_bytes"] + trs["write_bytes"]) if trs else None,
+                    "traffic_detail": traffic_detail(trs, stage_bytes, stage_bytes),
                     "algorithmic_bytes": 2 * stage_bytes,
                     "copied_gbps": stage_only["copied_gbps"],
                     "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
                     "frac_measured": round(stage_only["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}
+
+    store_staging_roof = None
+    if store and store.get("staging_alone"):
+        sa = store["staging_alone"]
+        a = 2 * stage_bytes / (sa["ms_avg"] / 1e3) / 1e9
+        trs = pmc_traffic(wl.name, "staging_region_copy<false, %d," % kform)
+        store_staging_roof = {"bound": "hbm", "kernel": "staging_region_copy<false,...> (HBM store, alone)",
+                              "achieved": round(a, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                              "frac": round(a / HBM_PEAK_GBPS, 4),
+                              "traffic": round(trs["fetch_bytes"] + trs["write_bytes"]) if trs else None,
+                              "traffic_detail": traffic_detail(trs, stage_bytes, stage_bytes),
+                              "algorithmic_bytes": 2 * stage_bytes, "copied_gbps": sa["copied_gbps"],
+                              "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
+                              "frac_measured": round(sa["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}
 
     store_roof = None
     if store and host_blocks:
@@ -852,6 +1144,8 @@ def main():
                    "retrieved_bytes": wl.retrieved_bytes, "host_link_bytes": host_bytes,
                    "staging_bytes": stage_bytes,
                    "regions": [(r.kind, r.weight) for r in wl.regions],
+                   "weights": "measured by the pool: kv_pool_measure_bandwidth, 256 MiB per region, host "
+                              "regions sharing one link (MB/s)" if measured else "configured",
                    "layout": "head-major chunks" if wl.layout == 0 else "token-major chunks",
                    "dst_slots": wl.dst_num_slots, "seed": wl.seed},
         "retrieval_ms": {"call_to_complete": round(ms_per_step, 3),
@@ -867,6 +1161,7 @@ def main():
         "probes": pr,
         "store": store,
         "roofline_store": store_roof,
+        "roofline_store_staging": store_staging_roof,
         "layerwise": layerwise,
         "copy_engine_retrieve": copy_engine,
         "place_ms": round(t_place * 1e3, 3),
@@ -874,6 +1169,7 @@ def main():
         "store_kernels_ms": store_t,
         "cpu_baseline": cpu,
         "caches_flushed_per_step": bool(args.flush),
+        "verified_round_trip": verified,
         "requests_per_call": len(wl.requests) if args.batch else 1,
         "launch": {"host_transport": "copy engines" if args.sdma else "zero-copy kernel",
                    "host_grid": args.host_grid or None, "staging_grid": args.staging_grid or None,

@@ -130,9 +130,11 @@ struct RequestRec {
     uint32_t gen;
     std::deque<Allocation> ranges;  // one per (offload set, region); stable addresses
     hipEvent_t stored = nullptr;   // recorded after each store touching the request
-    hipEvent_t busy = nullptr;     // recorded after each store / retrieve touching it
+    hipEvent_t busy = nullptr;     // recorded after each store / retrieve touching it; each record
+                                   // covers the one before it, so it waits for every earlier call
     bool stored_rec = false;
     bool busy_rec = false;
+    hipStream_t busy_stream = nullptr;   // stream of the last busy record
     uint64_t call_mark = 0;         // the last store / retrieve call that listed it (pool lock held)
 };
 
@@ -287,6 +289,8 @@ struct SmallCallArgs {
     uint32_t grid_host;        // workgroups taking the host-class items (the rest: staging)
     uint64_t words[kInlineWords];
 };
+// passed by value as the kernel's only argument: it must fit the 4 KiB kernel-argument segment
+static_assert(sizeof(SmallCallArgs) <= 4096, "small-call arguments exceed the kernel-argument segment");
 
 // ---------------------------------------------------------------- copy-engine plan (bounce.cpp)
 

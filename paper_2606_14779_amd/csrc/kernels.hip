@@ -42,6 +42,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
 #include <cstdint>
 
 #include "internal.hpp"
@@ -310,8 +311,13 @@ __global__ __launch_bounds__(kThreads) void ring_slot_copy(CopyArgs a)
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
 __global__ __launch_bounds__(kThreads) void small_call_copy(SmallCallArgs f)
 {
-    cptr_t *table = (cptr_t *)&f.words[0];
-    citem_t *items = (citem_t *)&f.words[f.a.chunks];
+    // f is the kernel's only explicit argument, so it sits at offset 0 of the
+    // kernel-argument segment; the table and the items are addressed there
+    // (constant address space, scalar loads), never through a copy of f.
+    typedef __attribute__((address_space(4))) const char cchar_t;
+    cchar_t *words = (cchar_t *)__builtin_amdgcn_kernarg_segment_ptr() + offsetof(SmallCallArgs, words);
+    cptr_t *table = (cptr_t *)words;
+    citem_t *items = (citem_t *)(words + static_cast<uint64_t>(f.a.chunks) * sizeof(uint64_t));
     CopyArgs a = f.a;
     const bool host = blockIdx.x < f.grid_host;
     a.n_items = host ? f.n_host : f.a.n_items - f.n_host;

@@ -14,6 +14,7 @@
 
 #include <algorithm>
 #include <cerrno>
+#include <cstdio>
 #include <cstring>
 
 #include "internal.hpp"
@@ -70,16 +71,87 @@ private:
     unsigned long old_mask_[kWords] = {};
 };
 
+// The online NUMA nodes, from /sys/devices/system/node/online ("0", "0-1",
+// "0,2-3"); empty if unreadable.
+std::vector<int> online_nodes()
+{
+    std::vector<int> nodes;
+    FILE *f = std::fopen("/sys/devices/system/node/online", "r");
+    if (!f) return nodes;
+    char buf[256] = {};
+    const bool ok = std::fgets(buf, sizeof buf, f) != nullptr;
+    std::fclose(f);
+    if (!ok) return nodes;
+    char *save = nullptr;   // strtok_r: pools may be created from several threads at once
+    for (char *tok = strtok_r(buf, ",\n", &save); tok; tok = strtok_r(nullptr, ",\n", &save)) {
+        int a = -1, b = -1;
+        const int got = std::sscanf(tok, "%d-%d", &a, &b);
+        if (got == 1) b = a;
+        if (got >= 1 && a >= 0 && b >= a && b - a < 4096)
+            for (int n = a; n <= b; ++n) nodes.push_back(n);
+    }
+    return nodes;
+}
+
+// The node holding most of the pages of the mapping that contains p, from
+// the "N<node>=<pages>" fields of its /proc/self/numa_maps line; -1 if none.
+int numa_maps_node(const void *p)
+{
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    uintptr_t start = 0;
+    bool found = false;
+    if (FILE *m = std::fopen("/proc/self/maps", "r")) {   // the mapping's start address
+        char line[512];
+        while (std::fgets(line, sizeof line, m)) {
+            unsigned long lo = 0, hi = 0;
+            if (std::sscanf(line, "%lx-%lx", &lo, &hi) == 2 && a >= lo && a < hi) {
+                start = lo;
+                found = true;
+                break;
+            }
+        }
+        std::fclose(m);
+    }
+    if (!found) return -1;
+    FILE *f = std::fopen("/proc/self/numa_maps", "r");
+    if (!f) return -1;
+    int best = -1;
+    long best_pages = 0;
+    char line[4096];
+    while (std::fgets(line, sizeof line, f)) {
+        unsigned long lo = 0;
+        if (std::sscanf(line, "%lx", &lo) != 1 || lo != start) continue;
+        char *save = nullptr;
+        for (char *tok = strtok_r(line, " \n", &save); tok; tok = strtok_r(nullptr, " \n", &save)) {
+            int node = -1;
+            long pages = 0;
+            if (std::sscanf(tok, "N%d=%ld", &node, &pages) == 2 && pages > best_pages) {
+                best = node;
+                best_pages = pages;
+            }
+        }
+        break;
+    }
+    std::fclose(f);
+    return best;
+}
+
 // NUMA node backing the page at p: move_pages() in query mode (no nodes
-// given) reports where each page lives; get_mempolicy() is the fallback.
+// given) reports where each page lives; get_mempolicy() and the mapping's
+// page counts in /proc/self/numa_maps are the fallbacks.  Driver-pinned pages
+// may be invisible to all three; on a machine with a single online node they
+// can only be on that node.
 int page_node(void *p)
 {
     void *pages[1] = {p};
     int status[1] = {-1};
     if (syscall(SYS_move_pages, 0, 1ul, pages, nullptr, status, 0) == 0 && status[0] >= 0) return status[0];
     int node = -1;
-    if (syscall(SYS_get_mempolicy, &node, nullptr, 0, p, MPOL_F_NODE | MPOL_F_ADDR) != 0) return -1;
-    return node;
+    if (syscall(SYS_get_mempolicy, &node, nullptr, 0, p, MPOL_F_NODE | MPOL_F_ADDR) == 0 && node >= 0) return node;
+    node = numa_maps_node(p);
+    if (node >= 0) return node;
+    const std::vector<int> online = online_nodes();
+    return online.size() == 1 ? online[0] : -1;
 }
 
 void alloc_region(Region &r)
@@ -182,6 +254,8 @@ void release_gpu(Pool &p)
         if (s.done) (void)hipEventDestroy(s.done);
         s.done = nullptr;
     }
+    for (int op = 0; op < 2; ++op)   // the last host-class kernel of each direction
+        if (p.link_rec[op] && p.link_done[op]) (void)hipEventSynchronize(p.link_done[op]);
     for (auto &kv : p.requests) {
         if (kv.second->busy_rec) (void)hipEventSynchronize(kv.second->busy);
         if (kv.second->stored) (void)hipEventDestroy(kv.second->stored);

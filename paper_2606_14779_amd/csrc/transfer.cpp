@@ -281,10 +281,19 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (gather && rec->stored_rec) check_hip(hipStreamWaitEvent(s, rec->stored, 0), "hipStreamWaitEvent");
         if (!gather && rec->busy_rec) check_hip(hipStreamWaitEvent(s, rec->busy, 0), "hipStreamWaitEvent");
     }
+    // busy must cover every call still touching the request, not only this
+    // one: two retrieves of a request may run on different streams at once,
+    // and release, destroy and a later store wait on busy alone.  So when
+    // the previous record was on another stream, the caller's stream first
+    // waits for it (after this call's kernels, so only later work on the
+    // stream is held back), and the new record covers both.
     auto mark_requests = [&] {
         for (RequestRec *rec : touched) {
+            if (rec->busy_rec && rec->busy_stream != s)
+                check_hip(hipStreamWaitEvent(s, rec->busy, 0), "hipStreamWaitEvent");
             check_hip(hipEventRecord(rec->busy, s), "hipEventRecord");
             rec->busy_rec = true;
+            rec->busy_stream = s;
             if (!gather) {
                 check_hip(hipEventRecord(rec->stored, s), "hipEventRecord");
                 rec->stored_rec = true;

@@ -8,9 +8,11 @@ module raises on import: there is no fallback path.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import operator
 import os
+import weakref
 from dataclasses import dataclass
 
 import numpy as np
@@ -81,6 +83,25 @@ if not os.path.exists(LIB_PATH):
     raise ImportError("libkvpool.so is not built (%s); run `python -m paper_2606_14779_amd.build`"
                       % LIB_PATH)
 _cdll = ctypes.CDLL(LIB_PATH)
+
+# Pools still open when the interpreter exits are closed by an exit hook, so
+# that kv_pool_destroy (which waits for the pool's streams and frees its HIP
+# memory) runs while the HIP runtime is whole, not from a finaliser after the
+# runtime's own exit-time teardown.  The hook is registered after torch's
+# import above, and exit hooks run last-registered first, so it runs before
+# any that torch registered.
+_live_pools = weakref.WeakSet()
+
+
+def _close_live_pools():
+    for p in list(_live_pools):
+        try:
+            p.close()
+        except Exception:
+            pass
+
+
+atexit.register(_close_live_pools)
 
 _u32, _u64, _i32, _vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p
 _SIGS = {
@@ -282,11 +303,13 @@ class KVPool:
         _check(_lib.kv_pool_create(ctypes.addressof(descs), None if bw is None else bw.ctypes.data, n,
                                    ctypes.addressof(cs), device, ctypes.byref(h)))
         self._h = h
+        _live_pools.add(self)
 
     def close(self):
         if getattr(self, "_h", None) and self._h.value:
             _lib.kv_pool_destroy(self._h)
             self._h = ctypes.c_void_p()
+        _live_pools.discard(self)
 
     def __del__(self):
         try:

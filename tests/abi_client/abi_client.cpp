@@ -4,6 +4,9 @@
 // under a permuted block table, and checks every element on the host.  Then
 // it retrieves again through the copy-engine transport with one-block ring
 // slots, in two layer ranges, and checks again.
+// With the argument "exit-open" it instead leaves the pool open with a
+// retrieve still enqueued and returns from main: the process must end
+// cleanly (the library registers nothing that runs at exit).
 // Built by the package build step; run by tests/test_abi_client.py (GPU).
 #include <hip/hip_runtime.h>
 
@@ -30,8 +33,9 @@
         }                                                                                    \
     } while (0)
 
-int main()
+int main(int argc, char **argv)
 {
+    const bool exit_open = argc > 1 && std::strcmp(argv[1], "exit-open") == 0;
     const uint32_t L = 4, H = 2, bs = 16, D = 64, n = 37, slots = 45;
     const uint64_t chunk_elems = uint64_t(H) * bs * D;                 // bf16 words per (layer, K/V) chunk
     const uint64_t layer_bytes = uint64_t(slots) * chunk_elems * 2;
@@ -72,6 +76,10 @@ int main()
     HIPTRY(hipStreamCreate(&stream));
     TRY(kv_pool_store(pool, map.data(), n, src_table.data(), slots, k_src.data(), v_src.data(), stream));
     TRY(kv_pool_retrieve_request(pool, 42, n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
+    if (exit_open) {   // pool, streams and buffers left alive, work possibly still running
+        std::printf("exiting with the pool open\n");
+        return 0;
+    }
     HIPTRY(hipStreamSynchronize(stream));
 
     std::vector<uint16_t> got(slots * chunk_elems), want(slots * chunk_elems);
@@ -97,6 +105,12 @@ int main()
     for (uint32_t i = 0; i < 2 * L; ++i) HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
     TRY(kv_pool_set_launch(pool, KVP_CLASS_HOST, KVP_OP_RETRIEVE, 0, KVP_LAUNCH_UPLOAD));
     TRY(kv_pool_retrieve(pool, map.data(), n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
+    HIPTRY(hipStreamSynchronize(stream));
+    if (check()) return 1;
+
+    // the same request by the allocation-free entry point (work list in the static scratch)
+    for (uint32_t i = 0; i < 2 * L; ++i) HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
+    TRY(kv_pool_retrieve_noalloc(pool, map.data(), n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
     HIPTRY(hipStreamSynchronize(stream));
     if (check()) return 1;
 
@@ -143,7 +157,7 @@ int main()
         std::fprintf(stderr, "abi client: %llu mismatching chunks or elements\n", (unsigned long long)bad);
         return 1;
     }
-    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, copy engines both ways)\n",
+    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, allocation-free call, copy engines both ways)\n",
                 n);
     return 0;
 }

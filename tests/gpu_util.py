@@ -68,7 +68,6 @@ def check_full(wl, run, host_src, ora=None):
 def check_sampled(wl, run, n_sample=48, seed=0):
     """Full-size check: sampled blocks through the oracle, every block by round trip,
     every untouched slot by sentinel."""
-    import torch
     sh = wl.shape
     L, bb = sh.layers, sh.block_bytes
     shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
@@ -93,7 +92,44 @@ def check_sampled(wl, run, n_sample=48, seed=0):
             slot = int(q.dst_slots[b])
             got = run.dst[:, :, slot].cpu().numpy().view(np.uint16)
             assert np.array_equal(got, dst1[:, :, 0]), "dst slot %d (block %d) differs" % (slot, b)
-    # every present block: retrieve(store(x)) == x, compared layer by layer on the GPU with torch
+    check_round_trip(wl, run)
+
+
+def check_every_block(wl, run, host_src):
+    """Full-size check of every block: the pool bytes of every present block equal the oracle's
+    store of the same source (regions compared span by span), and every destination slot equals its
+    source slot (round trip, on the GPU).  Since the oracle's gather of its own store returns the
+    source (pinned on the CPU), the destination then equals the oracle's gather for every block."""
+    sh = wl.shape
+    L, bb = sh.layers, sh.block_bytes
+    shape = (L, sh.kv_heads, sh.block_size, sh.head_dim, sh.elem_bytes)
+    ora = oracle_pool(wl)
+    regions = [np.zeros(r.capacity_bytes, np.uint8) for r in wl.regions]
+    for q in wl.requests:
+        m = ora.place(q.request_id, q.n_present)
+        assert np.array_equal(m, run.maps[q.request_id]), "placement differs"
+        oracle.store(m, q.src_slots, regions, [host_src[l, 0] for l in range(L)],
+                     [host_src[l, 1] for l in range(L)], shape, wl.layout)
+        for r in range(len(wl.regions)):
+            offs = m["offset"][m["region"] == r]
+            if len(offs) == 0:
+                continue
+            lo, hi = int(offs.min()), int(offs.max()) + bb
+            got = run.pool.region_read(r, lo, hi - lo)
+            if not np.array_equal(got, regions[r][lo:hi]):
+                bad = np.flatnonzero(got != regions[r][lo:hi])
+                raise AssertionError("region %d: %d bytes differ from the oracle's store, first at offset %d"
+                                     % (r, len(bad), lo + int(bad[0])))
+            del got
+    del regions
+    check_round_trip(wl, run)
+
+
+def check_round_trip(wl, run):
+    """Every present block: retrieve(store(x)) == x, layer by layer on the GPU; every other slot
+    still holds the sentinel."""
+    import torch
+    L = wl.shape.layers
     dev = run.dst.device
     touched = np.zeros(wl.dst_num_slots, bool)
     for q in wl.requests:

@@ -36,3 +36,16 @@ def test_cpp_client_under_host_sanitizers():
     assert r.returncode == 0, r.stdout + r.stderr
     assert "retrieved exactly" in r.stdout
     assert "ERROR: AddressSanitizer" not in r.stderr and "runtime error" not in r.stderr
+
+
+def test_cpp_client_exits_with_a_pool_open():
+    """A C++ caller that returns from main with its pool open and a retrieve enqueued (no
+    kv_pool_destroy): the process ends with status 0.  The library has no exit-time handler or
+    static destructor that calls the HIP runtime, so nothing of it runs after the runtime's own
+    teardown."""
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    r = subprocess.run([EXE, "exit-open"], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "exiting with the pool open" in r.stdout

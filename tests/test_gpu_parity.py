@@ -294,6 +294,52 @@ def test_release_waits_for_a_retrieve_in_flight():
         run.close()
 
 
+SMALL = workloads.KVShape("small", 4, 2, 64)           # 16 KiB blocks
+
+
+@pytest.mark.parametrize("transport", ["staging", "sdma"])
+def test_release_waits_for_every_reader_on_other_streams(transport):
+    """Two retrieves of one request on two streams, the first held back behind torch's bounded spin
+    kernel so that the second finishes first.  Neither takes the host-link kernel's turn (staging
+    regions only, or host regions through the copy engines), so only the request's own completion
+    event orders them.  Then release, place a new request over the same ranges and store other
+    values there: release waits for both retrieves, so both destinations hold the oracle's values."""
+    from gpu_util import oracle_expectation
+    kind = "staging" if transport == "staging" else "host"
+    regions = [workloads.RegionSpec(kind, 1, -1), workloads.RegionSpec(kind, 1, -1)]
+    wl = _custom(SMALL, regions, 40)
+    say("case release waits for every reader", transport)
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        if transport == "sdma":
+            run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
+        q = wl.requests[0]
+        cur = torch.cuda.current_stream()
+        second = torch.full_like(run.dst, int(np.uint16(SENTINEL).view(np.int16)))
+        a, b = torch.cuda.Stream(), torch.cuda.Stream()
+        a.wait_stream(cur)
+        b.wait_stream(cur)
+        with torch.cuda.stream(a):
+            torch.cuda._sleep(100_000_000)                   # bounded spin: 0.05-1 s
+        run.pool.retrieve_request(q.request_id, q.dst_slots, wl.dst_num_slots, *run.layer_ptrs(run.dst),
+                                  a.cuda_stream)
+        run.pool.retrieve_request(q.request_id, q.dst_slots, wl.dst_num_slots, *run.layer_ptrs(second),
+                                  b.cuda_stream)
+        run.pool.release(q.request_id)                       # returns once both retrieves are done
+        new = run.pool.place(q.request_id + 1, q.n_present)
+        assert set(zip(new["offset"].tolist(), new["region"].tolist())) == \
+            set(zip(run.maps[q.request_id]["offset"].tolist(), run.maps[q.request_id]["region"].tolist()))
+        run.src.bitwise_not_()
+        run.pool.store(new, q.src_slots, wl.src_num_slots, *run.layer_ptrs(run.src), cur.cuda_stream)
+        torch.cuda.synchronize()
+        _, _, expect = oracle_expectation(wl, run, host)
+        assert np.array_equal(run.dst.cpu().numpy().view(np.uint16), expect), "held-back reader got other bytes"
+        assert np.array_equal(second.cpu().numpy().view(np.uint16), expect)
+    finally:
+        run.close()
+
+
 def test_destroy_waits_for_a_retrieve_in_flight():
     """Destroy the pool while a retrieve runs on another stream: destroy waits for the work on its
     requests before freeing the regions, and the retrieve completes intact."""
@@ -428,16 +474,37 @@ def test_probes_copy_exactly():
 
 # ---- full-size workloads, in the launch configuration the bench times
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
-def test_full_size_workloads(cfg):
-    wl = workloads.make(cfg)
-    say("case full-size", wl.name, "bytes", wl.retrieved_bytes)
+@pytest.mark.parametrize("cfg,layout", [(1, 0), (2, 0), (3, 0), (4, 0), (5, 0), (3, 1), (4, 1)])
+def test_full_size_workloads(cfg, layout):
+    """Every workload at full size in its default launch configuration (the one the bench times),
+    and the two 128K-token workloads with a token-major pool (the LDS-staged conversion)."""
+    wl = workloads.make(cfg, layout=layout)
+    say("case full-size", wl.name, "layout", layout, "bytes", wl.retrieved_bytes)
     run = make_run(wl)
     try:
         run.setup()
         run.retrieve_all()
         torch.cuda.synchronize()
         check_sampled(wl, run)
+    finally:
+        run.close()
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_full_size_128k_every_block_against_the_oracle(layout):
+    """The 128K-token LLaMA-shaped request at full size (8192 blocks, 16 GiB): the pool bytes of
+    every block against the oracle's store, and every destination slot by round trip."""
+    wl = workloads.make(3, layout=layout)
+    say("case full-size every block", wl.name, "layout", layout)
+    run = make_run(wl)
+    try:
+        host = run.setup(keep_host=True)
+        run.retrieve_all()
+        torch.cuda.synchronize()
+        from gpu_util import check_every_block
+        check_every_block(wl, run, host)
+        del host
     finally:
         run.close()
         torch.cuda.empty_cache()
