@@ -47,15 +47,38 @@ def _events_ms(torch, fn, iters=3):
     return out
 
 
-def probes(torch, K, run, nbytes):
-    """Copy peaks in GB/s (1e9 B/s of copied bytes), measured on this GPU in this process."""
+HBM_PROBE_GRIDS = (2048, 8192, 32768, 65536)   # grids of the 4 GiB HBM copy sweep
+SAME_BYTES_GRIDS = (16384, 131072)   # grids of the same-bytes copy probe: none of the 4 GiB sweep's
+
+
+def probes(torch, K, run, nbytes, same_bytes=0):
+    """Copy peaks in GB/s (1e9 B/s of copied bytes), measured on this GPU in this process.
+
+    same_bytes: also a contiguous HBM copy of that many bytes (the staging side's bytes of the
+    step), since a copy's rate falls as its address span grows; its grids differ from the 4 GiB
+    sweep's, so that traces and counters tell the two apart."""
     res = {}
     cur = torch.cuda.current_stream()
+    if same_bytes >= (64 << 20):
+        n = same_bytes // 16384 * 16384
+        a = torch.empty(n // 2, dtype=torch.int16, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1)
+        best, bgrid, bflags = 0.0, 0, 0
+        for grid in SAME_BYTES_GRIDS:
+            for fl in (K.LAUNCH_SPLIT2, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD):
+                ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(b.data_ptr(), a.data_ptr(), n, grid, fl,
+                                                                       cur.cuda_stream)))
+                if n / ms / 1e6 > best:
+                    best, bgrid, bflags = n / ms / 1e6, grid, fl
+        res["hbm_copy_same_bytes"] = {"bytes": n, "gbps": round(best, 1), "grid": bgrid, "flags": bflags}
+        del a, b
+        torch.cuda.empty_cache()
     a = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
     b = torch.empty_like(a)
     a.fill_(1)
     best_k, best_grid, best_flags = 0.0, 0, 0
-    for grid in (2048, 8192, 32768, 65536):
+    for grid in HBM_PROBE_GRIDS:
         for fl in (0, K.LAUNCH_NT_LOAD, K.LAUNCH_SPLIT2, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD):
             ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(b.data_ptr(), a.data_ptr(), nbytes, grid, fl,
                                                                    cur.cuda_stream)))
@@ -114,8 +137,9 @@ PMC_PASSES = [
     ("rd", ["TCC_EA0_RDREQ_DRAM_32B_sum", "TCC_EA0_RDREQ_IO_32B_sum", "TCC_EA0_RDREQ_GMI_32B_sum"]),
     ("wr", ["TCC_EA0_WRREQ_WRITE_DRAM_32B_sum", "TCC_EA0_WRREQ_WRITE_IO_32B_sum", "TCC_EA0_WRREQ_WRITE_GMI_32B_sum"]),
     ("req", ["TCC_EA0_RDREQ_sum", "TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_128B_sum", "TCC_BUBBLE_sum"]),
-    ("utcl", ["TCP_UTCL1_TRANSLATION_MISS_sum", "TCP_UTCL1_TRANSLATION_HIT_sum", "TCP_UTCL1_STALL_MULTI_MISS_sum",
-              "TCP_PENDING_STALL_CYCLES_sum"]),
+    ("utcl", ["TCP_UTCL1_TRANSLATION_MISS_sum", "TCP_UTCL1_TRANSLATION_HIT_sum",
+              "TCP_UTCL1_STALL_UTCL2_REQ_OUT_OF_CREDITS_sum", "TCP_PENDING_STALL_CYCLES_sum", "GRBM_UTCL2_BUSY",
+              "GRBM_GUI_ACTIVE"]),
     ("stall", ["TCC_EA0_WRREQ_STALL_sum", "TCC_EA0_WRREQ_DRAM_CREDIT_STALL_sum",
                "TCC_EA0_RDREQ_DRAM_CREDIT_STALL_sum", "TCC_TAG_STALL_sum"]),
     ("lat", ["TCC_EA0_RDREQ_LEVEL_sum", "TCC_EA0_WRREQ_LEVEL_sum", "TCC_EA0_WRREQ_sum", "GRBM_GUI_ACTIVE"]),
@@ -153,7 +177,10 @@ def summarize_pmc(d, tag, bench_args, out_dir=None):
 
     def mean(xs):
         return sum(xs) / len(xs)
-    probe = [v for k, v in vals.items() if "probe_copy_kernel" in k[0] and "FETCH_SIZE" in v and "WRITE_SIZE" in v]
+    # calibration: the 4 GiB HBM copy sweep only (its grids), not the host-link, device-to-host or
+    # same-bytes probes, whose sizes differ
+    probe = [v for k, v in vals.items() if "probe_copy_kernel" in k[0] and k[1] in HBM_PROBE_GRIDS
+             and "FETCH_SIZE" in v and "WRITE_SIZE" in v]
     fetch_scale = PROBE_COPY_BYTES / 1024 / mean([x for v in probe for x in v["FETCH_SIZE"]]) if probe else None
     write_scale = PROBE_COPY_BYTES / 1024 / mean([x for v in probe for x in v["WRITE_SIZE"]]) if probe else None
     short = {"TCC_EA0_RDREQ_DRAM_32B_sum": "rd_dram", "TCC_EA0_RDREQ_IO_32B_sum": "rd_io",
@@ -258,6 +285,14 @@ def pmc_traffic(wl_name, kernel_prefix, profiles_dir=None):
         return None
     rec["source"] = os.path.relpath(path, ROOT) if profiles_dir is None else path
     return rec
+
+
+def same_bytes_frac(pr, copied_gbps):
+    """The HBM kernel's copied rate against the contiguous copy of the same byte count."""
+    sb = pr.get("hbm_copy_same_bytes") if pr else None
+    if not sb:
+        return {}
+    return {"measured_copy_peak_same_bytes": sb["gbps"], "frac_measured_same_bytes": round(copied_gbps / sb["gbps"], 4)}
 
 
 def traffic_detail(tr, alg_read, alg_write):
@@ -762,6 +797,9 @@ def main():
     ap.add_argument("--store-grid", type=int, default=0, help="host-class store workgroups (0: library default)")
     ap.add_argument("--store-flags", type=int, default=-1, help="host-class store flags (-1: library default)")
     ap.add_argument("--staging-flags", type=int, default=0)
+    ap.add_argument("--store-staging-grid", type=int, default=0,
+                    help="staging-class store workgroups (0: library default)")
+    ap.add_argument("--store-staging-flags", type=int, default=-1, help="staging-class store flags (-1: library default)")
     ap.add_argument("--coherence", type=int, default=0, help="0 default, 1 coherent, 2 non-coherent host memory")
     ap.add_argument("--layout", type=int, default=0, help="pool chunk layout: 0 head-major, 1 token-major (LDS)")
     ap.add_argument("--sdma", action="store_true",
@@ -791,6 +829,9 @@ def main():
     ap.add_argument("--measured-weights", action="store_true",
                     help="place with Eq. 1 weights measured by the pool (kv_pool_measure_bandwidth, host regions "
                          "sharing one link) instead of the workload's configured weights")
+    ap.add_argument("--weights", default=None,
+                    help="with --measured-weights: comma-separated weights measured by an earlier run (MB/s), used "
+                         "instead of measuring again, so that repeated runs (profiler passes) place identically")
     ap.add_argument("--layerwise", action="store_true",
                     help="also time the request retrieved one layer per call (kv_pool_retrieve_layers)")
     ap.add_argument("--summarize-pmc", metavar="DIR", default=None,
@@ -839,8 +880,15 @@ def main():
     wl = workloads.make(args.config, layout=args.layout, context_tokens=args.context)
     sh = wl.shape
     measured = None
+    if args.weights and not args.measured_weights:
+        raise SystemExit("--weights gives measured weights: use it with --measured-weights")
     if args.measured_weights:
-        measured = measure_weights(torch, K, wl)
+        if args.weights:
+            measured = [int(x) for x in args.weights.split(",")]
+            if len(measured) != len(wl.regions) or min(measured) <= 0:
+                raise SystemExit("--weights needs one positive integer per region (%d)" % len(wl.regions))
+        else:
+            measured = measure_weights(torch, K, wl)
         import dataclasses
         wl.regions = [dataclasses.replace(r, weight=int(w)) for r, w in zip(wl.regions, measured)]
         workloads._size_regions(wl.regions, [q.n_present for q in wl.requests], sh.block_bytes)
@@ -858,6 +906,8 @@ def main():
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     if args.staging_grid or args.staging_flags:
         run.pool.set_launch(K.CLASS_STAGING, K.OP_RETRIEVE, args.staging_grid, args.staging_flags)
+    if args.store_staging_grid or args.store_staging_flags >= 0:
+        run.pool.set_launch(K.CLASS_STAGING, K.OP_STORE, args.store_staging_grid, max(0, args.store_staging_flags))
     if args.store_grid or args.store_flags >= 0:     # the host-class store the line also times
         run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, args.store_grid,
                             K.LAUNCH_NT_STORE if args.store_flags < 0 else args.store_flags)
@@ -1051,7 +1101,8 @@ def main():
                        "ring": "2 x 1 GiB HBM"}
         log("copy-engine retrieve timed: %.3f ms" % ce_ms)
 
-    pr = None if args.no_probes else probes(torch, K, run, int(args.probe_gib * 2**30) // 4096 * 4096)
+    pr = None if args.no_probes else probes(torch, K, run, int(args.probe_gib * 2**30) // 4096 * 4096,
+                                            stage_bytes // max(1, len(wl.requests)))
     log("probes done")
     cpu = None if args.no_cpu_baseline else cpu_baseline(run, wl)
     if cpu:
@@ -1094,6 +1145,7 @@ def main():
                 "copied_gbps": round(copied, 1),
                 "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
                 "frac_measured": round(copied / pr["hbm_copy_peak_gbps"], 4) if pr else None}
+        roof.update(same_bytes_frac(pr, copied))
     hbm_roof = None
     if stage_only:
         a = 2 * stage_bytes / (stage_only["ms_avg"] / 1e3) / 1e9         # bytes read + written in HBM
@@ -1106,6 +1158,7 @@ def main():
                     "copied_gbps": stage_only["copied_gbps"],
                     "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
                     "frac_measured": round(stage_only["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}
+        hbm_roof.update(same_bytes_frac(pr, stage_only["copied_gbps"]))
 
     store_staging_roof = None
     if store and store.get("staging_alone"):
@@ -1120,6 +1173,7 @@ def main():
                               "algorithmic_bytes": 2 * stage_bytes, "copied_gbps": sa["copied_gbps"],
                               "measured_copy_peak": pr["hbm_copy_peak_gbps"] if pr else None,
                               "frac_measured": round(sa["copied_gbps"] / pr["hbm_copy_peak_gbps"], 4) if pr else None}
+        store_staging_roof.update(same_bytes_frac(pr, sa["copied_gbps"]))
 
     store_roof = None
     if store and host_blocks:
@@ -1144,8 +1198,9 @@ def main():
                    "retrieved_bytes": wl.retrieved_bytes, "host_link_bytes": host_bytes,
                    "staging_bytes": stage_bytes,
                    "regions": [(r.kind, r.weight) for r in wl.regions],
-                   "weights": "measured by the pool: kv_pool_measure_bandwidth, 256 MiB per region, host "
-                              "regions sharing one link (MB/s)" if measured else "configured",
+                   "weights": ("measured by the pool: kv_pool_measure_bandwidth, 256 MiB per region, host "
+                               "regions sharing one link (MB/s)" + ("; from an earlier run (--weights)" if args.weights
+                                                                    else "")) if measured else "configured",
                    "layout": "head-major chunks" if wl.layout == 0 else "token-major chunks",
                    "dst_slots": wl.dst_num_slots, "seed": wl.seed},
         "retrieval_ms": {"call_to_complete": round(ms_per_step, 3),
@@ -1176,6 +1231,8 @@ def main():
                    "host_flags": args.host_flags, "staging_flags": args.staging_flags,
                    "store_grid": args.store_grid or None,
                    "store_flags": None if args.store_flags < 0 else args.store_flags,
+                   "store_staging_grid": args.store_staging_grid or None,
+                   "store_staging_flags": None if args.store_staging_flags < 0 else args.store_staging_flags,
                    "coherence": args.coherence},
     }
     print(json.dumps(out), flush=True)

@@ -363,11 +363,15 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
                                     flight then write neighbouring slots of one layer buffer)
                                     instead of block by block */
 #define KVP_LAUNCH_UPLOAD  128u  /* on either class of an op: no small-call launch (below) */
+#define KVP_LAUNCH_TILE    256u  /* workgroup-owned tiles: a workgroup moves one moved chunk of 8
+                                    consecutive work items at a time, so its writes run over
+                                    neighbouring slots of one per-layer buffer (instead of taking
+                                    units g, g+G, ... of the whole launch) */
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
  * class 12 workgroups (token-major pool: 16, 20 for the store); staging class 65536
- * with KVP_LAUNCH_SPLIT2 for the pool_layout 0 retrieve, else 8192;
+ * for the pool_layout 0 retrieve, else 8192, with KVP_LAUNCH_TILE for every retrieve;
  * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
  * pool_layout 1 except the host-class store.  With the default host-class
  * retrieve grid, a retrieve enqueued while a host-class store kernel of this

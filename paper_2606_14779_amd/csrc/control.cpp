@@ -121,7 +121,7 @@ void pool_set_launch(Pool &p, uint32_t cls, uint32_t op, uint32_t grid, uint32_t
 {
     if (cls > 1 || op > 1) fail(KVP_ERR_INVALID, "class and op must be 0 or 1");
     if (flags & ~(KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE | KVP_LAUNCH_LDS | KVP_LAUNCH_SPLIT2 | KVP_LAUNCH_XCD |
-                  KVP_LAUNCH_SDMA | KVP_LAUNCH_CHUNK_MAJOR | KVP_LAUNCH_UPLOAD))
+                  KVP_LAUNCH_SDMA | KVP_LAUNCH_CHUNK_MAJOR | KVP_LAUNCH_UPLOAD | KVP_LAUNCH_TILE))
         fail(KVP_ERR_INVALID, "unknown flags");
     if (grid > (1u << 20)) fail(KVP_ERR_INVALID, "grid too large");
     if ((flags & KVP_LAUNCH_SDMA) && cls != KVP_CLASS_HOST)

@@ -275,6 +275,7 @@ struct CopyArgs {
     uint32_t tokens;           //   bs
     uint32_t row_vec;          //   D*elem_bytes/16
     uint32_t layout;           // 0 head-major, 1 token-major
+    uint32_t tile_items;       // > 0: workgroup-owned tiles of this many items x 1 moved chunk
 };
 
 // A call whose work list is small enough travels in the kernel arguments,

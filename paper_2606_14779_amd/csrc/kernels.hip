@@ -58,6 +58,7 @@ typedef __attribute__((address_space(1))) v4u gv4u;
 constexpr uint32_t kThreads = 256;
 constexpr uint32_t kXcds = 8;     // MI355X: 8 accelerator complex dies, 32 CUs each
 constexpr uint64_t kMaxLdsChunk = 64 * 1024;
+constexpr uint32_t kTileItems = 8;  // KVP_LAUNCH_TILE: work items per workgroup-owned tile
 
 template <bool NT>
 __device__ __forceinline__ v4u load16(const v4u *p)
@@ -269,6 +270,55 @@ __device__ __forceinline__ void chunk_copy_body(const CopyArgs &a, citem_t *item
     }
 }
 
+// Workgroup-owned tiles (KVP_LAUNCH_TILE): tile t is moved chunk t % K of
+// the a.tile_items consecutive work items from (t / K) * a.tile_items on;
+// workgroup g takes tiles g, g+G, ... and copies each itself, item by item
+// (the parts of a chunk in turn).  Its writes then run over neighbouring
+// slots of one per-layer engine buffer, and its reads over the same chunk
+// of neighbouring pool blocks.
+template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+__device__ __forceinline__ void chunk_copy_tiles(const CopyArgs &a, citem_t *items, cptr_t *table, uint32_t g,
+                                                 uint32_t G)
+{
+    extern __shared__ v4u lds[];
+    const uint32_t K = a.chunks, TB = kTileItems;   // a.tile_items is kTileItems when set
+    const uint32_t tiles = (a.n_items + TB - 1) / TB * K;
+    const uint64_t part_bytes = a.chunk_bytes / a.parts;
+    const uint32_t nvec = static_cast<uint32_t>(part_bytes >> 4);
+    for (uint32_t t = g; t < tiles; t += G) {
+        const uint32_t grp = t / K, k = t - grp * K;
+        const uint32_t i0 = grp * TB;
+        const uint32_t ni = a.n_items - i0 < TB ? a.n_items - i0 : TB;
+        const uint64_t cache = table[k];
+        const uint64_t coff = static_cast<uint64_t>(a.chunk0 + k) * a.chunk_bytes;
+        // the tile's work items, all fetched (scalar loads) before its first copy;
+        // indices past the last item are clamped to it and never copied
+        uint64_t pool_of[kTileItems], slot_of[kTileItems];
+#pragma unroll
+        for (uint32_t j = 0; j < kTileItems; ++j) {
+            const uint32_t i = i0 + (j < ni ? j : ni - 1);
+            pool_of[j] = items[i].pool + coff;
+            slot_of[j] = cache + static_cast<uint64_t>(items[i].slot) * a.chunk_bytes;
+        }
+#pragma unroll
+        for (uint32_t j = 0; j < kTileItems; ++j) {
+            if (j >= ni) break;
+            const uint64_t pool = pool_of[j], slot = slot_of[j];
+            for (uint32_t p = 0; p < a.parts; ++p) {
+                const uint64_t off = p * part_bytes;
+                const v4u *src = reinterpret_cast<const v4u *>(GATHER ? pool + off : slot + off);
+                v4u *dst = reinterpret_cast<v4u *>(GATHER ? slot + off : pool + off);
+                if constexpr (FORM == kPlain)
+                    wg_copy<UNROLL, NTL, NTS>(src, dst, nvec);
+                else if constexpr (FORM == kConvert)
+                    wg_convert<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec);
+                else
+                    wg_convert_lds<GATHER, UNROLL, NTL, NTS>(src, dst, nvec, a.heads, a.tokens, a.row_vec, lds);
+            }
+        }
+    }
+}
+
 // A launch of one class: the work list and table in device memory, every
 // workgroup on its items.
 template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
@@ -281,7 +331,10 @@ __device__ __forceinline__ void class_body(const CopyArgs &a)
         const uint32_t per = gridDim.x / kXcds;          // grid is a multiple of 8 here
         g = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
     }
-    chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a, (citem_t *)a.items, (cptr_t *)a.cache, g, gridDim.x);
+    if (a.tile_items)
+        chunk_copy_tiles<GATHER, FORM, UNROLL, NTL, NTS>(a, (citem_t *)a.items, (cptr_t *)a.cache, g, gridDim.x);
+    else
+        chunk_copy_body<GATHER, FORM, UNROLL, NTL, NTS>(a, (citem_t *)a.items, (cptr_t *)a.cache, g, gridDim.x);
 }
 
 // One entry point per kind of source, so that traces and counters tell the
@@ -466,6 +519,12 @@ hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, ui
     // the XCD renumbering is a permutation of [0, grid) only for multiples of 8
     a.xcd_remap = (flags & KVP_LAUNCH_XCD) && grid % kXcds == 0 ? 1u : 0u;
     a.chunk_major = (flags & KVP_LAUNCH_CHUNK_MAJOR) ? 1u : 0u;
+    a.tile_items = (flags & KVP_LAUNCH_TILE) ? kTileItems : 0u;
+    if (a.tile_items) {   // a grid of at most one workgroup per tile
+        const uint64_t tiles = (static_cast<uint64_t>(a.n_items) + kTileItems - 1) / kTileItems * a.chunks;
+        if (grid > tiles) grid = static_cast<uint32_t>(tiles);
+        a.xcd_remap = (flags & KVP_LAUNCH_XCD) && grid % kXcds == 0 ? 1u : 0u;
+    }
     if (cls == KVP_CLASS_HOST)
         return gather ? launch_dir<KVP_CLASS_HOST, true>(a, grid, flags, s)
                       : launch_dir<KVP_CLASS_HOST, false>(a, grid, flags, s);
@@ -483,6 +542,7 @@ hipError_t launch_small_call(SmallCallArgs &f, bool gather, uint32_t grid_host, 
     a.parts = (a.layout == 0 && (flags & KVP_LAUNCH_SPLIT2) && a.chunk_bytes % 32 == 0) ? 2u : 1u;
     a.xcd_remap = 0;
     a.chunk_major = 0;
+    a.tile_items = 0;
     auto cap = [&](uint32_t grid, uint32_t n) {
         const uint64_t units = static_cast<uint64_t>(n) * a.chunks * a.parts;
         if (n == 0) return 0u;

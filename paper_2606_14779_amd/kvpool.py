@@ -30,6 +30,7 @@ OP_RETRIEVE, OP_STORE = 0, 1
 LAUNCH_NT_LOAD, LAUNCH_NT_STORE, LAUNCH_LDS, LAUNCH_SPLIT2, LAUNCH_XCD, LAUNCH_SDMA = 1, 2, 4, 8, 16, 32
 LAUNCH_CHUNK_MAJOR = 64
 LAUNCH_UPLOAD = 128          # no small-call launch: upload the work list, one launch per class
+LAUNCH_TILE = 256            # workgroup-owned tiles of 8 work items x 1 chunk
 MEASURE_SHARED_LINK = 1
 
 LOC_DTYPE = np.dtype([("region", "<u4"), ("gen", "<u4"), ("offset", "<u8")])

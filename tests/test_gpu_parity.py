@@ -50,7 +50,15 @@ def test_parity_scaled_workloads(cfg, layout):
                                         (64, K.LAUNCH_XCD), (96, K.LAUNCH_XCD | K.LAUNCH_SPLIT2),
                                         (12, K.LAUNCH_XCD), (65536, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD),
                                         (7, K.LAUNCH_CHUNK_MAJOR), (65536, K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_SPLIT2),
-                                        (96, K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_XCD | K.LAUNCH_SPLIT2)])
+                                        (96, K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_XCD | K.LAUNCH_SPLIT2),
+                                        # per-class launches (the 45-block call would otherwise take the
+                                        # small-call launch, which has no unit order of its own)
+                                        (96, K.LAUNCH_XCD | K.LAUNCH_SPLIT2 | K.LAUNCH_UPLOAD),
+                                        (7, K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_UPLOAD),
+                                        (5, K.LAUNCH_TILE | K.LAUNCH_UPLOAD),
+                                        (65536, K.LAUNCH_TILE | K.LAUNCH_SPLIT2 | K.LAUNCH_UPLOAD),
+                                        (96, K.LAUNCH_TILE | K.LAUNCH_XCD | K.LAUNCH_SPLIT2 | K.LAUNCH_UPLOAD),
+                                        (1, K.LAUNCH_TILE | K.LAUNCH_NT_LOAD | K.LAUNCH_UPLOAD)])
 def test_parity_launch_shapes(grid, flags):
     wl = workloads.make(2, max_blocks=45)
     say("case launch", grid, flags)
@@ -68,7 +76,8 @@ def test_parity_launch_shapes(grid, flags):
 
 
 @pytest.mark.parametrize("flags", [0, K.LAUNCH_LDS, K.LAUNCH_LDS | K.LAUNCH_NT_LOAD,
-                                   K.LAUNCH_LDS | K.LAUNCH_CHUNK_MAJOR, K.LAUNCH_CHUNK_MAJOR])
+                                   K.LAUNCH_LDS | K.LAUNCH_CHUNK_MAJOR, K.LAUNCH_CHUNK_MAJOR,
+                                   K.LAUNCH_LDS | K.LAUNCH_TILE | K.LAUNCH_UPLOAD, K.LAUNCH_TILE | K.LAUNCH_UPLOAD])
 def test_parity_token_major_lds(flags):
     wl = workloads.make(4, max_blocks=33, layout=1)
     say("case token-major", flags)

@@ -229,7 +229,7 @@ def test_transfers_rejected_without_device():
     assert _err(p.store, m, [0, 1], 2, ptrs, ptrs) == "INVALID"
     assert _err(p.set_timing, True) == "INVALID"
     assert _err(p.set_launch, 2, 0, 0, 0) == "INVALID"
-    assert _err(p.set_launch, 0, 0, 0, 256) == "INVALID"                                     # unknown flag
+    assert _err(p.set_launch, 0, 0, 0, 512) == "INVALID"                                     # unknown flag
     p.set_launch(0, 0, 64, K.LAUNCH_NT_LOAD)
     assert _err(p.set_launch, K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA) == "INVALID"   # nothing to copy with
     assert _err(p.set_launch, K.CLASS_STAGING, K.OP_STORE, 0, K.LAUNCH_SDMA) == "INVALID"  # host class only
