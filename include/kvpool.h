@@ -9,11 +9,14 @@
  * GPU's paged KV cache by looking the blocks up, grouping them by region and
  * reading all regions in parallel (Sec. 4.3, "KV Retrieval").
  *
- * Pool regions ("pool devices" in the paper) are either
+ * Pool regions ("pool devices" in the paper) are
  *   - KVP_REGION_HOST: pinned host memory bound to a NUMA node and mapped
  *     into the GPU's address space; GPU kernels read it directly over the
- *     host link (zero copy), or
- *   - KVP_REGION_STAGING: a buffer in HBM that stands in for an SSD.
+ *     host link (zero copy);
+ *   - KVP_REGION_STAGING: a buffer in HBM that stands in for an SSD; or
+ *   - KVP_REGION_FILE: a file or a block device, the storage tier, read and
+ *     written with O_DIRECT by one worker thread per region (see
+ *     kv_pool_create_files).
  *
  * Conventions for every function
  *   - Return 0 (KVP_OK) on success or a negative KVP_ERR_* code.  Nothing
@@ -61,23 +64,27 @@ extern "C" {
 #define KVP_ERR_NOTFOUND -4   /* unknown request */
 #define KVP_ERR_STALE    -5   /* map entry refers to a released or reused range */
 #define KVP_ERR_HIP      -6   /* a HIP runtime call failed */
+#define KVP_ERR_IO       -7   /* a read or write of a file region failed */
 
 /* ---- region types and flags ---- */
 #define KVP_REGION_HOST     0u  /* pinned, NUMA-bound, GPU-mapped host memory */
 #define KVP_REGION_STAGING  1u  /* HBM buffer standing in for an SSD */
+#define KVP_REGION_FILE     2u  /* a file or block device, read and written with O_DIRECT (storage tier) */
 
 #define KVP_HOST_DEFAULT      0u  /* library's choice of host-memory coherence */
 #define KVP_HOST_COHERENT     1u  /* fine-grained (coherent) pinned memory */
 #define KVP_HOST_NONCOHERENT  2u  /* coarse-grained (non-coherent) pinned memory */
 
+#define KVP_FILE_BUFFERED     1u  /* file regions: through the page cache (no O_DIRECT) */
+
 #define KVP_ABSENT 0xFFFFFFFFu    /* kvp_loc.region of a block that is not in the pool */
 
 /* One pool region ("pool device", Sec. 4.1.1: each gets a unique index). */
 typedef struct {
-    uint32_t type;            /* KVP_REGION_HOST or KVP_REGION_STAGING */
+    uint32_t type;            /* KVP_REGION_HOST, KVP_REGION_STAGING or KVP_REGION_FILE */
     int32_t  numa_node;       /* host: NUMA node whose memory backs it; -1 = no binding */
     uint64_t capacity_bytes;  /* usable bytes, rounded down to a multiple of 4096 */
-    uint32_t flags;           /* host: KVP_HOST_*; staging: 0 */
+    uint32_t flags;           /* host: KVP_HOST_*; staging: 0; file: 0 or KVP_FILE_BUFFERED */
     uint32_t reserved;        /* 0 */
 } kvp_region_desc;
 
@@ -125,6 +132,45 @@ typedef struct kvp_pool kvp_pool;   /* opaque */
 int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths,
                    uint32_t n_regions, const kvp_kv_spec *spec, int hip_device,
                    kvp_pool **out);
+
+/*
+ * Create a pool whose regions may include the storage tier (Sec. 4.2, the
+ * KV-passthrough to SSDs; Sec. 4.1.3, one worker per device).  Arguments as
+ * kv_pool_create, plus:
+ *   paths[n_regions]     for each KVP_REGION_FILE region, the file to create
+ *                        or the block device to use; ignored (may be NULL)
+ *                        for other regions; paths may be NULL if there is no
+ *                        file region.  A path that does not exist is created
+ *                        (mode 0600) and sized to the capacity, and removed
+ *                        by kv_pool_destroy.  An existing path must be a
+ *                        block device at least that large: it is read and
+ *                        written in place and kept.  An existing regular file
+ *                        is refused (KVP_ERR_INVALID), never overwritten.
+ * A file region's numa_node must be -1; its flags are 0 (O_DIRECT: reads and
+ * writes bypass the page cache) or KVP_FILE_BUFFERED (page cache, for file
+ * systems without O_DIRECT).  A pool with a file region needs 2 * C to be a
+ * multiple of 4096, so that every block, layer range and range of a request
+ * is sector aligned.  Its file regions share a ring of two pinned, GPU-mapped
+ * host buffers (min(256 MiB, the largest file region) each, at least one
+ * block; kv_pool_set_file_ring) between the files and the engine cache.
+ *
+ * Retrieve and store of file-region blocks: the call runs the file reads
+ * (retrieve) or writes (store) itself, by the regions' worker threads, batch
+ * by batch through the ring.  A retrieve returns once every read is done and
+ * the kernels moving the slots into the engine cache are enqueued on
+ * `stream`; a store returns once every write is done (it waits for its own
+ * kernels, and for work enqueued on `stream` before it).  Blocks of the
+ * other region types in the same call are moved as kv_pool_retrieve /
+ * kv_pool_store move them.  kv_pool_retrieve_noalloc refuses file-region
+ * entries (KVP_ERR_INVALID); the copy-engine transport, the small-call launch
+ * and kv_pool_set_timing do not cover them.  A failed file read or write
+ * returns KVP_ERR_IO; batches enqueued before it may have reached the engine
+ * cache (retrieve) or the file (store).
+ * Errors: as kv_pool_create, plus IO (creating or sizing a file).
+ */
+int kv_pool_create_files(const kvp_region_desc *regions, const uint64_t *bandwidths,
+                         uint32_t n_regions, const kvp_kv_spec *spec, int hip_device,
+                         const char *const *paths, kvp_pool **out);
 
 /*
  * Place the n_blocks blocks of one request (Algorithm 1 without the writes):
@@ -429,6 +475,12 @@ int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid,
  *   slot_bytes   multiple of 4096 in [64 KiB, 64 GiB].
  * Errors: INVALID (bad size, placement-only pool), NOMEM, HIP. */
 int kv_pool_set_copy_ring(kvp_pool *pool, uint64_t slot_bytes);
+
+/* Bytes per slot of the file regions' 2-slot pinned ring (a multiple of 4096
+ * in [64 KiB, 64 GiB]; raised to one block).  The ring is freed after the work
+ * on it and allocated again at the new size.  Errors: INVALID (bad size, or
+ * the pool has no file region), NOMEM, HIP. */
+int kv_pool_set_file_ring(kvp_pool *pool, uint64_t slot_bytes);
 
 typedef struct {
     float    host_ms;         /* duration of the host-class kernel, -1 if none ran; with

@@ -8,7 +8,8 @@
 #include "internal.hpp"
 
 namespace kvp {
-Pool *pool_create(const kvp_region_desc *, const uint64_t *, uint32_t, const kvp_kv_spec *, int);
+Pool *pool_create(const kvp_region_desc *, const uint64_t *, uint32_t, const kvp_kv_spec *, int,
+                  const char *const *);
 void pool_destroy(Pool *);
 void pool_place(Pool &, uint64_t, uint32_t, kvp_loc *);
 void pool_extend(Pool &, uint64_t, uint32_t, kvp_loc *);
@@ -21,6 +22,7 @@ void pool_region_info(const Pool &, uint32_t, kvp_region_info *);
 void pool_region_read(Pool &, uint32_t, uint64_t, uint64_t, void *);
 void pool_set_launch(Pool &, uint32_t, uint32_t, uint32_t, uint32_t);
 void pool_set_copy_ring(Pool &, uint64_t);
+void pool_set_file_ring(Pool &, uint64_t);
 void pool_set_timing(Pool &, int);
 void pool_last_timing(Pool &, kvp_timing *);
 void pool_timing_summary(Pool &, kvp_timing_summary *);
@@ -90,7 +92,23 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, u
     return guarded([&] {
         if (!out) kvp::fail(KVP_ERR_INVALID, "out is null");
         *out = nullptr;
-        kvp::Pool *p = kvp::pool_create(regions, bandwidths, n_regions, spec, hip_device);
+        kvp::Pool *p = kvp::pool_create(regions, bandwidths, n_regions, spec, hip_device, nullptr);
+        try {
+            *out = new kvp_pool{p};
+        } catch (...) {
+            kvp::pool_destroy(p);
+            throw;
+        }
+    });
+}
+
+int kv_pool_create_files(const kvp_region_desc *regions, const uint64_t *bandwidths, uint32_t n_regions,
+                         const kvp_kv_spec *spec, int hip_device, const char *const *paths, kvp_pool **out)
+{
+    return guarded([&] {
+        if (!out) kvp::fail(KVP_ERR_INVALID, "out is null");
+        *out = nullptr;
+        kvp::Pool *p = kvp::pool_create(regions, bandwidths, n_regions, spec, hip_device, paths);
         try {
             *out = new kvp_pool{p};
         } catch (...) {
@@ -231,6 +249,11 @@ int kv_pool_set_launch(kvp_pool *pool, uint32_t cls, uint32_t op, uint32_t grid,
 int kv_pool_set_copy_ring(kvp_pool *pool, uint64_t slot_bytes)
 {
     return guarded([&] { kvp::pool_set_copy_ring(impl(pool), slot_bytes); });
+}
+
+int kv_pool_set_file_ring(kvp_pool *pool, uint64_t slot_bytes)
+{
+    return guarded([&] { kvp::pool_set_file_ring(impl(pool), slot_bytes); });
 }
 
 int kv_pool_set_timing(kvp_pool *pool, int enable)

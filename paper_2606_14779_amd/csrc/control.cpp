@@ -31,6 +31,10 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
         uint32_t n_host = 0;
         for (size_t r = 0; r < p.regions.size(); ++r) {
             const Region &reg = p.regions[r];
+            if (reg.desc.type == KVP_REGION_FILE) {   // the file side: reads of the region's file
+                mbps[r] = measure_file_region(reg, probe_bytes);
+                continue;
+            }
             const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
             n_host += cls == KVP_CLASS_HOST;
             hipStream_t st = p.s_stage;   // one probe at a time
@@ -108,7 +112,9 @@ void pool_region_read(Pool &p, uint32_t region, uint64_t offset, uint64_t bytes,
     if (!dst && bytes) fail(KVP_ERR_INVALID, "null destination");
     if (offset > r.capacity || r.capacity - offset < bytes) fail(KVP_ERR_INVALID, "range outside region");
     if (!bytes) return;
-    if (r.host) {
+    if (r.desc.type == KVP_REGION_FILE) {
+        file_region_read(r, offset, bytes, dst);
+    } else if (r.host) {
         std::memcpy(dst, static_cast<const char *>(r.host) + offset, bytes);
     } else {
         DeviceScope dev(p.device);
@@ -148,6 +154,18 @@ void pool_set_copy_ring(Pool &p, uint64_t slot_bytes)
     if ((p.launch[KVP_CLASS_HOST][KVP_OP_RETRIEVE].flags | p.launch[KVP_CLASS_HOST][KVP_OP_STORE].flags) &
         KVP_LAUNCH_SDMA)
         ensure_bounce(p);
+}
+
+void pool_set_file_ring(Pool &p, uint64_t slot_bytes)
+{
+    if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool launches nothing");
+    if (slot_bytes % kSector || slot_bytes < (64u << 10) || slot_bytes > (1ull << 36))
+        fail(KVP_ERR_INVALID, "slot_bytes must be a multiple of 4096 in [64 KiB, 64 GiB]");
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (!p.workers) fail(KVP_ERR_INVALID, "the pool has no file region");
+    DeviceScope dev(p.device);
+    free_file_ring(p);
+    alloc_file_ring(p, slot_bytes);
 }
 
 void pool_set_timing(Pool &p, int enable)

@@ -3,12 +3,14 @@
 
 #include <hip/hip_runtime.h>
 
+#include <condition_variable>
 #include <cstdint>
 #include <map>
 #include <memory>
 #include <mutex>
 #include <deque>
 #include <string>
+#include <thread>
 #include <unordered_map>
 #include <vector>
 
@@ -148,7 +150,86 @@ struct Region {
     uint32_t flags_used = 0;
     RangeAllocator alloc;
     std::map<uint64_t, Allocation *> live;   // base -> allocation
+    // file regions: the open file or block device, and its worker thread
+    int fd = -1;
+    bool file_owned = false;                 // created by the pool: removed at destroy
+    std::string file_path;
+    uint32_t worker = 0;
 };
+
+// ---------------------------------------------------------------- file regions (fileio.cpp)
+
+struct IoGroup {                 // a set of reads or writes waited for together
+    std::mutex mu;
+    std::condition_variable cv;
+    uint32_t pending = 0;
+    int err = 0;                 // first failure's errno, with its message
+    std::string what;
+};
+
+struct IoJob {
+    int fd = -1;
+    bool write = false;
+    uint64_t off = 0;            // in the file, sector aligned
+    uint64_t len = 0;            // sector multiple
+    char *buf = nullptr;         // sector aligned
+    IoGroup *group = nullptr;
+};
+
+// One worker thread per file region (the per-device workers of Sec. 4.1.3):
+// each runs the reads and writes of its region in submission order.
+class FileWorkers {
+public:
+    explicit FileWorkers(size_t n);
+    ~FileWorkers();
+    void submit(size_t worker, const IoJob &job);
+
+private:
+    struct Worker {
+        std::thread th;
+        std::mutex mu;
+        std::condition_variable cv;
+        std::deque<IoJob> q;
+        bool stop = false;
+    };
+    static void run(Worker &w);
+    void shutdown();
+    std::vector<std::unique_ptr<Worker>> w_;
+};
+
+void io_wait(IoGroup &g);            // waits, then throws KVP_ERR_IO on a failure
+void io_drain(IoGroup &g) noexcept;  // waits, forgets any failure
+
+// One file read or write: `len` bytes at `file_off` of a region, to or from
+// offset `slot_off` of a ring slot.
+struct FileSpan {
+    uint32_t region;
+    uint64_t file_off;
+    uint64_t len;
+    uint64_t slot_off;
+};
+
+// The blocks moved through one ring slot: work items [first, first + n) and
+// spans [span0, span0 + spans).
+struct FileBatch {
+    uint32_t ring;
+    uint32_t first, n;
+    size_t span0, spans;
+};
+
+struct FileGeometry {
+    uint64_t base;         // device address of slot 0
+    uint64_t slot_bytes;
+    uint32_t slots;
+    uint32_t next;         // ring slot of the first batch
+    uint64_t block_bytes;
+    uint64_t chunk_bytes;
+};
+
+void open_file_region(Region &r, const char *path);   // creates (or opens a block device); sets fd
+void close_file_region(Region &r) noexcept;          // closes; removes a file the pool created
+void file_region_read(const Region &r, uint64_t offset, uint64_t bytes, void *dst);
+uint64_t measure_file_region(const Region &r, uint64_t probe_bytes);   // MB/s
 
 struct LaunchCfg {
     uint32_t grid;
@@ -201,6 +282,9 @@ ScratchDevice &scratch_device(int device);
 constexpr uint32_t kBounceSlots = 2;                 // copy-engine transport: ring slots
 constexpr uint64_t kBounceSlotMin = 1ull << 30;      //   default bytes per slot (one block at least)
 
+constexpr uint32_t kFileSlots = 2;                   // file regions: pinned ring slots
+constexpr uint64_t kFileSlotMax = 256ull << 20;      //   default bytes per slot (one block at least)
+
 struct Pool {
     int device = -1;
     bool placement_only = true;
@@ -239,6 +323,17 @@ struct Pool {
     bool bounce_free_rec[kBounceSlots] = {};
     uint32_t bounce_next = 0;
 
+    // file regions: a worker per region, and a ring of pinned, GPU-mapped
+    // slots between the files and the engine cache
+    std::unique_ptr<FileWorkers> workers;
+    char *file_ring = nullptr;         // host address of slot 0
+    uint64_t file_ring_dev = 0;        // its device address
+    uint64_t file_slot_bytes = 0;
+    hipEvent_t file_free[kFileSlots] = {};   // the last kernel reading or filling the slot is done
+    bool file_free_rec[kFileSlots] = {};
+    IoGroup file_io[kFileSlots];       // the slot's reads or writes
+    uint32_t file_next = 0;
+
     bool timing = false;
     std::vector<TimedCall> timed;      // calls recorded since timing was enabled or last summarised
     std::vector<hipEvent_t> spare;     // timing events ready for reuse
@@ -250,6 +345,8 @@ void free_slot(Slot &s);                                    // pool.cpp: one wor
 void release_bounce(Pool &p);                               // pool.cpp: copy-engine ring, after its work
 void ensure_bounce(Pool &p);                                // pool.cpp: copy-engine ring on first use
 void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps);   // control.cpp
+void alloc_file_ring(Pool &p, uint64_t slot_bytes);         // pool.cpp: the file regions' ring
+void free_file_ring(Pool &p);                               // pool.cpp: after the work on it
 void drain_timed(Pool &p, kvp_timing_summary *sum);        // transfer.cpp: wait, summarise, recycle
 
 // ---------------------------------------------------------------- kernels (kernels.hip)
@@ -334,10 +431,20 @@ struct RingGeometry {
 void plan_bounce(const RingGeometry &g, std::vector<HostBlock> &blocks, uint64_t width, uint32_t chunk0,
                  std::vector<CopyItem> &items, std::vector<LinkRun> &runs, std::vector<Batch> &batches);
 
+// Pack a call's file-class blocks into ring slots: grouped by region, in
+// offset order within a region; the moved part of each block (`width` bytes
+// from `skip` on) back to back in a slot, and neighbouring blocks of a region
+// merged into one span when whole blocks move.  Appends one work item per
+// block, addressing its part in the slot less chunk0 chunks.
+void plan_file(const FileGeometry &g, std::vector<HostBlock> &blocks, uint64_t skip, uint64_t width, uint32_t chunk0,
+               std::vector<CopyItem> &items, std::vector<FileSpan> &spans, std::vector<FileBatch> &batches);
+
+
 // cls: KVP_CLASS_HOST / KVP_CLASS_STAGING / kClassRing (selects the kernel
 // entry point: zero-copy host region, HBM staging region, copy-engine ring);
 // gather: pool -> cache (retrieve); !gather: cache -> pool (store)
 constexpr uint32_t kClassRing = 2;
+constexpr uint32_t kClassFile = 4;   // a file regions' ring slot (pinned host memory)
 hipError_t launch_chunk_copy(const CopyArgs &a, uint32_t cls, bool gather, uint32_t grid, uint32_t flags,
                              hipStream_t s);
 // One launch of both classes for a call whose table and items are already in

@@ -22,12 +22,14 @@
 // The work list and the engine pointer table are read with scalar loads, and
 // the next unit's entries are fetched while the current unit is copied.
 //
-// Four entry points share the body, so that traces and counters tell them
+// Five entry points share the body, so that traces and counters tell them
 // apart: host_region_copy (zero-copy reads or writes of pinned host regions
 // over the host link), staging_region_copy (HBM staging regions),
 // ring_slot_copy (a copy-engine ring slot in HBM, whose host-link leg is a
-// hipMemcpy), and small_call_copy (both region classes of a call whose work
-// list fits in the kernel arguments, in one launch with no upload).
+// hipMemcpy), file_slot_copy (a file regions' ring slot in pinned host
+// memory, filled or emptied by file reads and writes), and small_call_copy
+// (both region classes of a call whose work list fits in the kernel
+// arguments, in one launch with no upload).
 //
 // Three copy forms:
 //   - head-major pool chunks: the chunk is [H][bs][D] on both sides; a plain
@@ -358,6 +360,12 @@ __global__ __launch_bounds__(kThreads) void ring_slot_copy(CopyArgs a)
     class_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
 }
 
+template <bool GATHER, int FORM, int UNROLL, bool NTL, bool NTS>
+__global__ __launch_bounds__(kThreads) void file_slot_copy(CopyArgs a)
+{
+    class_body<GATHER, FORM, UNROLL, NTL, NTS>(a);
+}
+
 // Both classes of a small call in one launch, the table and the items read
 // from the kernel arguments (scalar loads, as from the work list).  The
 // class split is uniform per workgroup.
@@ -464,6 +472,8 @@ static void launch_one(const A &a, dim3 g, size_t lds, hipStream_t s)
         hipLaunchKernelGGL((host_region_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
     else if constexpr (CLS == KVP_CLASS_STAGING)
         hipLaunchKernelGGL((staging_region_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
+    else if constexpr (CLS == kClassFile)
+        hipLaunchKernelGGL((file_slot_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
     else
         hipLaunchKernelGGL((ring_slot_copy<GATHER, FORM, UNROLL, NTL, NTS>), g, dim3(kThreads), lds, s, a);
 }
@@ -531,6 +541,8 @@ hipError_t launch_chunk_copy(const CopyArgs &args, uint32_t cls, bool gather, ui
     if (cls == KVP_CLASS_STAGING)
         return gather ? launch_dir<KVP_CLASS_STAGING, true>(a, grid, flags, s)
                       : launch_dir<KVP_CLASS_STAGING, false>(a, grid, flags, s);
+    if (cls == kClassFile)
+        return gather ? launch_dir<kClassFile, true>(a, grid, flags, s) : launch_dir<kClassFile, false>(a, grid, flags, s);
     return gather ? launch_dir<kClassRing, true>(a, grid, flags, s) : launch_dir<kClassRing, false>(a, grid, flags, s);
 }
 

@@ -241,12 +241,58 @@ void ensure_bounce(Pool &p)
     }
 }
 
+// The file regions' ring: kFileSlots pinned, GPU-mapped host buffers of
+// slot_bytes each (raised to one block), and their events.  Caller holds the
+// device scope; on failure nothing stays allocated.
+void alloc_file_ring(Pool &p, uint64_t slot_bytes)
+{
+    const uint64_t slot = round_up(std::max(slot_bytes, p.block_bytes), kSector);
+    void *h = nullptr;
+    if (hipHostMalloc(&h, slot * kFileSlots, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess || !h) {
+        clear_hip_error();
+        fail(KVP_ERR_NOMEM, "file-region ring of " + std::to_string(slot * kFileSlots) + " bytes");
+    }
+    try {
+        void *d = nullptr;
+        check_hip(hipHostGetDevicePointer(&d, h, 0), "hipHostGetDevicePointer");
+        for (uint32_t j = 0; j < kFileSlots; ++j)
+            if (!p.file_free[j])
+                check_hip(hipEventCreateWithFlags(&p.file_free[j], hipEventDisableTiming), "hipEventCreate");
+        p.file_ring = static_cast<char *>(h);
+        p.file_ring_dev = reinterpret_cast<uint64_t>(d);
+        p.file_slot_bytes = slot;
+        p.file_next = 0;
+    } catch (...) {
+        (void)hipHostFree(h);
+        throw;
+    }
+}
+
+// The file regions' ring, after the kernels and the reads / writes on it.
+void free_file_ring(Pool &p)
+{
+    for (uint32_t j = 0; j < kFileSlots; ++j) {
+        io_drain(p.file_io[j]);
+        if (p.file_free_rec[j] && p.file_free[j]) (void)hipEventSynchronize(p.file_free[j]);
+        p.file_free_rec[j] = false;
+    }
+    if (p.file_ring) (void)hipHostFree(p.file_ring);
+    p.file_ring = nullptr;
+    p.file_ring_dev = 0;
+    p.file_slot_bytes = 0;
+}
+
 namespace {
 
 void release_gpu(Pool &p)
 {
     if (p.placement_only) return;
     release_bounce(p);
+    free_file_ring(p);
+    for (auto &e : p.file_free)
+        if (e) (void)hipEventDestroy(e), e = nullptr;
+    p.workers.reset();   // joins the file regions' worker threads
+    for (auto &r : p.regions) close_file_region(r);
     if (p.s_stage) (void)hipStreamSynchronize(p.s_stage);
     for (auto &s : p.ring) {
         if (s.pending && s.done) (void)hipEventSynchronize(s.done);
@@ -279,6 +325,13 @@ void release_gpu(Pool &p)
         else if (r.dev) (void)hipFree(r.dev);
         r.host = r.dev = nullptr;
     }
+}
+
+bool has_file_region(const Pool &p)
+{
+    for (const auto &r : p.regions)
+        if (r.desc.type == KVP_REGION_FILE) return true;
+    return false;
 }
 
 void check_spec(const kvp_kv_spec &s, uint64_t &chunk, uint64_t &block)
@@ -345,7 +398,7 @@ uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
 // ---------------------------------------------------------------- create / destroy
 
 Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, uint32_t n_regions,
-                  const kvp_kv_spec *spec, int hip_device)
+                  const kvp_kv_spec *spec, int hip_device, const char *const *paths)
 {
     if (!regions || !spec) fail(KVP_ERR_INVALID, "null argument");
     if (!bandwidths && hip_device < 0) fail(KVP_ERR_INVALID, "a placement-only pool needs bandwidths");
@@ -362,13 +415,22 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
     for (uint32_t i = 0; i < n_regions; ++i) {
         const kvp_region_desc &d = regions[i];
         const std::string who = "region " + std::to_string(i) + ": ";
-        if (d.type != KVP_REGION_HOST && d.type != KVP_REGION_STAGING) fail(KVP_ERR_INVALID, who + "bad type");
+        if (d.type != KVP_REGION_HOST && d.type != KVP_REGION_STAGING && d.type != KVP_REGION_FILE)
+            fail(KVP_ERR_INVALID, who + "bad type");
         if (p->bandwidth[i] == 0) fail(KVP_ERR_INVALID, who + "bandwidth must be positive");
         if (d.capacity_bytes < kSector) fail(KVP_ERR_INVALID, who + "capacity below one 4096-byte sector");
         if (d.numa_node < -1) fail(KVP_ERR_INVALID, who + "numa_node must be >= -1");
         if (d.type == KVP_REGION_HOST && d.flags > KVP_HOST_NONCOHERENT) fail(KVP_ERR_INVALID, who + "bad flags");
         if (d.type == KVP_REGION_STAGING && (d.flags != 0 || d.numa_node != -1))
             fail(KVP_ERR_INVALID, who + "staging regions take no flags and no NUMA node");
+        if (d.type == KVP_REGION_FILE) {
+            if (d.flags & ~KVP_FILE_BUFFERED) fail(KVP_ERR_INVALID, who + "bad flags");
+            if (d.numa_node != -1) fail(KVP_ERR_INVALID, who + "file regions take no NUMA node");
+            if ((2 * p->chunk_bytes) % kSector != 0)
+                fail(KVP_ERR_INVALID, who + "a file region needs 2 x chunk bytes to be a multiple of 4096");
+            if (hip_device >= 0 && (!paths || !paths[i] || !*paths[i]))
+                fail(KVP_ERR_INVALID, who + "file region without a path");
+        }
         if (d.reserved != 0) fail(KVP_ERR_INVALID, who + "reserved must be 0");
         Region &r = p->regions[i];
         r.desc = d;
@@ -389,7 +451,24 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
     if (hip_device >= n_dev) fail(KVP_ERR_INVALID, "hip_device " + std::to_string(hip_device) + " not present");
     DeviceScope dev(hip_device);
     try {
-        for (auto &r : p->regions) alloc_region(r);
+        for (uint32_t i = 0; i < n_regions; ++i) {
+            Region &r = p->regions[i];
+            if (r.desc.type == KVP_REGION_FILE)
+                open_file_region(r, paths[i]);
+            else
+                alloc_region(r);
+        }
+        if (has_file_region(*p)) {
+            size_t n_files = 0;
+            uint64_t largest = 0;
+            for (auto &r : p->regions)
+                if (r.desc.type == KVP_REGION_FILE) {
+                    r.worker = static_cast<uint32_t>(n_files++);
+                    largest = std::max(largest, r.capacity);
+                }
+            p->workers = std::make_unique<FileWorkers>(n_files);
+            alloc_file_ring(*p, std::min(kFileSlotMax, round_up(largest, kSector)));
+        }
         check_hip(hipStreamCreateWithFlags(&p->s_stage, hipStreamNonBlocking), "hipStreamCreate");
         check_hip(hipEventCreateWithFlags(&p->fork, hipEventDisableTiming), "hipEventCreate");
         check_hip(hipEventCreateWithFlags(&p->uploaded, hipEventDisableTiming), "hipEventCreate");

@@ -104,6 +104,56 @@ Slot &acquire_slot(Pool &p, size_t bytes)
     return s;
 }
 
+// The file regions' blocks of a call, batch by batch through the pinned ring
+// (see fileio.cpp): a retrieve reads a batch's spans by the regions' workers,
+// then moves the slot to the engine cache by a kernel on stream `sf`; a store
+// fills the slot by a kernel, waits for it, and has the workers write the
+// spans while the next batch's kernel runs.  A slot is refilled only after
+// its previous kernel and its previous reads or writes are done.  On return
+// every read or write is done; on a failure the workers are drained first.
+void run_file_batches(Pool &p, bool gather, const std::vector<FileBatch> &batches,
+                      const std::vector<FileSpan> &spans, const CopyArgs &a, const LaunchCfg &lc, hipStream_t sf)
+{
+    auto submit = [&](const FileBatch &bt, bool write) {
+        char *slot = p.file_ring + static_cast<uint64_t>(bt.ring) * p.file_slot_bytes;
+        for (size_t i = bt.span0; i < bt.span0 + bt.spans; ++i) {
+            const FileSpan &sp = spans[i];
+            const Region &r = p.regions[sp.region];
+            p.workers->submit(r.worker, IoJob{r.fd, write, sp.file_off, sp.len, slot + sp.slot_off, &p.file_io[bt.ring]});
+        }
+    };
+    auto kernel = [&](const FileBatch &bt) {
+        CopyArgs k = a;
+        k.items = a.items + bt.first;
+        k.n_items = bt.n;
+        check_hip(launch_chunk_copy(k, kClassFile, gather, lc.grid, lc.flags, sf), "kernel launch");
+        check_hip(hipEventRecord(p.file_free[bt.ring], sf), "hipEventRecord");
+        p.file_free_rec[bt.ring] = true;
+    };
+    try {
+        for (const FileBatch &bt : batches) {
+            io_wait(p.file_io[bt.ring]);
+            if (p.file_free_rec[bt.ring])
+                check_hip(hipEventSynchronize(p.file_free[bt.ring]), "hipEventSynchronize");
+            if (gather) {
+                submit(bt, false);
+                io_wait(p.file_io[bt.ring]);
+                kernel(bt);
+            } else {
+                kernel(bt);
+                check_hip(hipEventSynchronize(p.file_free[bt.ring]), "hipEventSynchronize");
+                submit(bt, true);
+            }
+        }
+        for (auto &g : p.file_io) io_wait(g);
+    } catch (...) {
+        for (auto &g : p.file_io) io_drain(g);
+        p.file_next = static_cast<uint32_t>((p.file_next + batches.size()) % kFileSlots);
+        throw;
+    }
+    p.file_next = static_cast<uint32_t>((p.file_next + batches.size()) % kFileSlots);
+}
+
 }  // namespace
 
 // Wait for every recorded call, optionally summarise it, and recycle its events.
@@ -170,6 +220,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     // GLT-resolved locations, grouped by region class (Sec. 4.3)
     std::vector<CopyItem> items[2];
     std::vector<HostBlock> host_blocks;   // copy-engine transport: placed in ring slots below
+    std::vector<HostBlock> file_blocks;   // file regions: placed in the file ring's slots below
     std::vector<RequestRec *> touched;
     const uint64_t epoch = ++p.call_epoch;
     // No two present entries may write the same place: a destination slot on
@@ -227,11 +278,18 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             touched.push_back(hint->owner);
         }
         const Region &r = p.regions[e.region];
-        const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
-        if (cls == KVP_CLASS_HOST && sdma)
-            host_blocks.push_back(HostBlock{e.region, e.offset, static_cast<uint32_t>(slot)});
-        else
-            items[cls].push_back(CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
+        if (r.desc.type == KVP_REGION_FILE) {
+            if (noalloc)
+                fail(KVP_ERR_INVALID, "map entry " + std::to_string(b) + ": the allocation-free call reads no file region");
+            file_blocks.push_back(HostBlock{e.region, e.offset, static_cast<uint32_t>(slot)});
+        } else {
+            const uint32_t cls = r.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
+            if (cls == KVP_CLASS_HOST && sdma)
+                host_blocks.push_back(HostBlock{e.region, e.offset, static_cast<uint32_t>(slot)});
+            else
+                items[cls].push_back(
+                    CopyItem{reinterpret_cast<uint64_t>(r.dev) + e.offset, static_cast<uint32_t>(slot), 0u});
+        }
     }
     if (!wide_slots.empty()) {
         std::sort(wide_slots.begin(), wide_slots.end());
@@ -254,7 +312,16 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         plan_bounce(g, host_blocks, width, 2 * layer_begin, items[KVP_CLASS_HOST], runs, batches);
     }
 
-    const size_t n_items = items[0].size() + items[1].size();
+    std::vector<CopyItem> file_items;
+    std::vector<FileSpan> spans;
+    std::vector<FileBatch> file_batches;
+    if (!file_blocks.empty()) {
+        const FileGeometry fg{p.file_ring_dev, p.file_slot_bytes, kFileSlots, p.file_next, p.block_bytes,
+                              p.chunk_bytes};
+        plan_file(fg, file_blocks, skip, width, 2 * layer_begin, file_items, spans, file_batches);
+    }
+
+    const size_t n_items = items[0].size() + items[1].size() + file_items.size();
     const size_t ptr_bytes = round_up(static_cast<size_t>(2 * (layer_end - layer_begin)) * sizeof(uint64_t), 16);
     const size_t list_bytes = ptr_bytes + n_items * sizeof(CopyItem);
     if (noalloc && list_bytes > kScratchBytes)
@@ -345,7 +412,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             check_hip(q, "hipEventQuery");
         }
     }
-    if (!noalloc && batches.empty() && !p.timing && !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
+    if (!noalloc && batches.empty() && file_batches.empty() && !p.timing &&
+        !((lh.flags | ls.flags) & KVP_LAUNCH_UPLOAD) &&
         chunks + 2 * n_items <= kInlineWords) {
         // Small call: table and items in the kernel arguments, both classes in
         // one launch in the host class's copy form (the link-bound part; the
@@ -365,7 +433,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         return;
     }
 
-    // work list: [chunks cache pointers][host items][staging items], in a
+    // work list: [chunks cache pointers][host items][staging items][file items], in a
     // ring slot of the pool, or in the device's static scratch (noalloc)
     const size_t bytes = list_bytes;
     Slot *slot = nullptr;
@@ -388,6 +456,7 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     auto *list = reinterpret_cast<CopyItem *>(static_cast<char *>(host_list) + ptr_bytes);
     std::copy(items[0].begin(), items[0].end(), list);
     std::copy(items[1].begin(), items[1].end(), list + items[0].size());
+    std::copy(file_items.begin(), file_items.end(), list + items[0].size() + items[1].size());
 
     // With earlier work still running on the caller's stream (calls issued
     // back to back, e.g. one per layer), the upload goes on the pool's stream:
@@ -423,7 +492,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
         check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
     }
-    if (fork_staging || !batches.empty()) check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
+    if (fork_staging || !batches.empty() || !file_batches.empty())
+        check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
 
     const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(dev_base) + ptr_bytes);
     // Staging class forked onto the internal stream first, then the host
@@ -529,6 +599,19 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
             check_hip(hipEventRecord(tc->t1[KVP_CLASS_HOST], s), "hipEventRecord");
             tc->ran[KVP_CLASS_HOST] = true;
         }
+    }
+    if (!file_batches.empty()) {
+        // file-region kernels on the pool's stream, beside the host-class
+        // kernel on the caller's, then joined back into the caller's stream
+        if (!fork_staging && batches.empty()) check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
+        CopyArgs fa = geo;
+        fa.items = dev_list + items[0].size() + items[1].size();
+        fa.cache = static_cast<const uint64_t *>(dev_base);
+        LaunchCfg lf = p.launch[KVP_CLASS_HOST][op];
+        lf.flags &= ~(KVP_LAUNCH_SDMA | KVP_LAUNCH_UPLOAD);
+        run_file_batches(p, gather, file_batches, spans, fa, lf, p.s_stage);
+        check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
+        check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     }
     if (noalloc) {
         check_hip(hipEventRecord(sd->free, s), "hipEventRecord");

@@ -21,9 +21,10 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libkvpool.so")
 
 KVP_OK = 0
-ERRORS = {-1: "INVALID", -2: "NOMEM", -3: "NOSPACE", -4: "NOTFOUND", -5: "STALE", -6: "HIP"}
-REGION_HOST, REGION_STAGING = 0, 1
+ERRORS = {-1: "INVALID", -2: "NOMEM", -3: "NOSPACE", -4: "NOTFOUND", -5: "STALE", -6: "HIP", -7: "IO"}
+REGION_HOST, REGION_STAGING, REGION_FILE = 0, 1, 2
 HOST_DEFAULT, HOST_COHERENT, HOST_NONCOHERENT = 0, 1, 2
+FILE_BUFFERED = 1            # file regions: through the page cache instead of O_DIRECT
 ABSENT = 0xFFFFFFFF
 CLASS_HOST, CLASS_STAGING = 0, 1
 OP_RETRIEVE, OP_STORE = 0, 1
@@ -107,6 +108,7 @@ atexit.register(_close_live_pools)
 _u32, _u64, _i32, _vp = ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, ctypes.c_void_p
 _SIGS = {
     "kv_pool_create": (_i32, [_vp, _vp, _u32, _vp, _i32, _vp]),
+    "kv_pool_create_files": (_i32, [_vp, _vp, _u32, _vp, _i32, _vp, _vp]),
     "kv_pool_place": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_extend": (_i32, [_vp, _u64, _u32, _vp]),
     "kv_pool_lookup": (_i32, [_vp, _u64, _u32, _vp]),
@@ -126,6 +128,7 @@ _SIGS = {
     "kv_pool_set_bandwidths": (_i32, [_vp, _vp]),
     "kv_pool_set_launch": (_i32, [_vp, _u32, _u32, _u32, _u32]),
     "kv_pool_set_copy_ring": (_i32, [_vp, _u64]),
+    "kv_pool_set_file_ring": (_i32, [_vp, _u64]),
     "kv_pool_set_timing": (_i32, [_vp, _i32]),
     "kv_pool_last_timing": (_i32, [_vp, _vp]),
     "kv_pool_timing_summary": (_i32, [_vp, _vp]),
@@ -219,10 +222,11 @@ def _loc_array(m) -> np.ndarray:
 
 @dataclass
 class Region:
-    kind: str                 # "host" or "staging"
+    kind: str                 # "host", "staging" or "file"
     capacity_bytes: int
     numa_node: int = -1
-    coherence: int = HOST_DEFAULT
+    coherence: int = HOST_DEFAULT   # the region's flags: host KVP_HOST_*, file 0 or FILE_BUFFERED
+    path: str | None = None         # file regions: the file to create, or a block device
 
 
 @dataclass
@@ -290,9 +294,11 @@ class KVPool:
     def __init__(self, regions, bandwidths, spec: KVSpec, device: int = 0):
         n = len(regions)
         descs = (_RegionDesc * n)()
+        paths = (ctypes.c_char_p * n)()
         for i, r in enumerate(regions):
-            kind = {"host": REGION_HOST, "staging": REGION_STAGING}[r.kind]
+            kind = {"host": REGION_HOST, "staging": REGION_STAGING, "file": REGION_FILE}[r.kind]
             descs[i] = _struct(_RegionDesc, kind, r.numa_node, r.capacity_bytes, r.coherence, 0)
+            paths[i] = os.fsencode(r.path) if r.path is not None else None
         bw = None if bandwidths is None else _int_array(bandwidths, np.uint64, "bandwidths")
         if bw is not None and len(bw) != n:
             raise ValueError("one bandwidth per region")
@@ -301,8 +307,8 @@ class KVPool:
         cs = _struct(_KVSpec, spec.num_layers, spec.num_kv_heads, spec.head_dim, spec.block_size,
                      spec.elem_bytes, spec.pool_layout)
         h = ctypes.c_void_p()
-        _check(_lib.kv_pool_create(ctypes.addressof(descs), None if bw is None else bw.ctypes.data, n,
-                                   ctypes.addressof(cs), device, ctypes.byref(h)))
+        _check(_lib.kv_pool_create_files(ctypes.addressof(descs), None if bw is None else bw.ctypes.data, n,
+                                         ctypes.addressof(cs), device, ctypes.addressof(paths), ctypes.byref(h)))
         self._h = h
         _live_pools.add(self)
 
@@ -418,6 +424,9 @@ class KVPool:
     # ---- launch configuration and timing
     def set_launch(self, cls: int, op: int, grid: int = 0, flags: int = 0) -> None:
         _check(_lib.kv_pool_set_launch(self._h, cls, op, grid, flags))
+
+    def set_file_ring(self, slot_bytes: int) -> None:
+        _check(_lib.kv_pool_set_file_ring(self._h, slot_bytes))
 
     def set_copy_ring(self, slot_bytes: int) -> None:
         _check(_lib.kv_pool_set_copy_ring(self._h, slot_bytes))

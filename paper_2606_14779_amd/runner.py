@@ -21,7 +21,10 @@ SENTINEL = 0x7FA5  # a bf16 NaN pattern that the generator never produces
 
 
 class WorkloadRun:
-    def __init__(self, wl: Workload, device: int = 0, coherence: int = K.HOST_DEFAULT, numa_nodes=None):
+    def __init__(self, wl: Workload, device: int = 0, coherence: int = K.HOST_DEFAULT, numa_nodes=None,
+                 file_dir=None, file_flags: int = 0):
+        import os
+        import tempfile
         import torch
         self.torch = torch
         self.wl = wl
@@ -29,10 +32,16 @@ class WorkloadRun:
         sh = wl.shape
         nodes = list(numa_nodes) if numa_nodes else K.allowed_numa_nodes()
         self.regions = []
-        for r in wl.regions:
+        self.file_paths = []
+        for i, r in enumerate(wl.regions):
             if r.kind == "host":
                 node = nodes[r.numa % len(nodes)] if r.numa >= 0 else -1
                 self.regions.append(K.Region("host", r.capacity_bytes, node, coherence))
+            elif r.kind == "file":     # a new file per region, created and removed by the pool
+                path = os.path.join(file_dir or tempfile.gettempdir(),
+                                    "kvpool-%d-%x-region%d.bin" % (os.getpid(), id(self), i))
+                self.file_paths.append(path)
+                self.regions.append(K.Region("file", r.capacity_bytes, -1, file_flags, path))
             else:
                 self.regions.append(K.Region("staging", r.capacity_bytes))
         self.weights = [r.weight for r in wl.regions]

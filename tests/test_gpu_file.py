@@ -1,0 +1,236 @@
+"""GPU parity of the storage tier: pool regions backed by files (KVP_REGION_FILE).
+
+The files are created by the pool with O_DIRECT in a temporary directory and
+read and written by one worker thread per region; the bytes pass through a
+ring of pinned slots that a kernel moves to or from the engine cache.  Every
+case is compared with the CPU oracle bit for bit: the placement, the pool
+bytes -- read back through the library and, separately, straight from the
+file on disk -- and the destination cache.  The file regions here live on the
+machine's ordinary disk; nothing in these tests measures a storage device.
+"""
+import dataclasses
+import os
+import tempfile
+
+import numpy as np
+import pytest
+
+from kvgen import workloads
+from paper_2606_14779_amd import kvpool as K
+from paper_2606_14779_amd.runner import SENTINEL, WorkloadRun
+
+from gpu_util import check_full, oracle_expectation, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _with_files(wl, kinds=None):
+    """The workload with its staging regions (or the regions named in kinds) turned into file regions."""
+    regions = []
+    for i, r in enumerate(wl.regions):
+        kind = kinds[i] if kinds else ("file" if r.kind == "staging" else r.kind)
+        regions.append(dataclasses.replace(r, kind=kind))
+    return dataclasses.replace(wl, regions=regions)
+
+
+def _check_files_on_disk(wl, run, host):
+    """The pool bytes of every file region, read from the file itself, equal the oracle's store."""
+    maps, regions, _ = oracle_expectation(wl, run, host)
+    bb = wl.shape.block_bytes
+    paths = iter(run.file_paths)
+    for r, spec in enumerate(wl.regions):
+        if spec.kind != "file":
+            continue
+        path = next(paths)
+        assert os.path.exists(path)
+        for q in wl.requests:
+            m = maps[q.request_id]
+            offs = m["offset"][m["region"] == r]
+            if len(offs) == 0:
+                continue
+            lo, hi = int(offs.min()), int(offs.max()) + bb
+            got = np.fromfile(path, dtype=np.uint8, count=hi - lo, offset=lo)
+            assert np.array_equal(got, regions[r][lo:hi]), "file %s differs from the oracle's store" % path
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_file_regions_beside_host_and_staging(layout):
+    """LLaMA-shaped request over a host, two file and a staging region (weights 4:2:1:1): store, then
+    retrieve into a fragmented table; maps, pool bytes (through the library and from the files on
+    disk) and destination against the oracle."""
+    base = workloads.make(3, max_blocks=61, layout=layout)
+    regions = [workloads.RegionSpec("host", 4, 0), workloads.RegionSpec("file", 2),
+               workloads.RegionSpec("staging", 1), workloads.RegionSpec("file", 1)]
+    workloads._size_regions(regions, [q.n_present for q in base.requests], base.shape.block_bytes)
+    wl = dataclasses.replace(base, regions=regions)
+    say("case file regions, layout", layout)
+    with tempfile.TemporaryDirectory() as d:
+        run = WorkloadRun(wl, device=0, file_dir=d)
+        try:
+            host = run.setup(keep_host=True)
+            run.retrieve_all()
+            torch.cuda.synchronize()
+            check_full(wl, run, host)
+            _check_files_on_disk(wl, run, host)
+        finally:
+            run.close()
+        assert os.listdir(d) == [], "the pool leaves its files behind"
+
+
+@pytest.mark.parametrize("cfg", [2, 4, 5])
+def test_workloads_with_file_regions(cfg):
+    """Workloads 2, 4 and 5 (several requests on four streams, absent tails) with their staging
+    regions as file regions."""
+    wl = _with_files(workloads.make(cfg, max_blocks=61))
+    say("case file workload", cfg)
+    with tempfile.TemporaryDirectory() as d:
+        run = WorkloadRun(wl, device=0, file_dir=d)
+        try:
+            host = run.setup(keep_host=True)
+            run.retrieve_all()
+            torch.cuda.synchronize()
+            check_full(wl, run, host)
+        finally:
+            run.close()
+
+
+@pytest.mark.parametrize("buffered", [False, True])
+def test_small_ring_many_batches(buffered):
+    """A ring of one-block slots: every block is a batch of its own and the two slots alternate many
+    times, in both directions; through O_DIRECT and through the page cache."""
+    wl = _with_files(workloads.make(2, max_blocks=40))
+    say("case file ring of one block", buffered)
+    with tempfile.TemporaryDirectory() as d:
+        run = WorkloadRun(wl, device=0, file_dir=d, file_flags=K.FILE_BUFFERED if buffered else 0)
+        try:
+            run.pool.set_file_ring(64 << 10)                 # raised to one block
+            host = run.setup(keep_host=True)
+            run.retrieve_all()
+            torch.cuda.synchronize()
+            check_full(wl, run, host)
+            _check_files_on_disk(wl, run, host)
+        finally:
+            run.close()
+
+
+def test_layer_ranges_through_files():
+    """Store in three layer groups, retrieve one layer per call, and a sub-range that leaves the
+    other layers untouched: each file span then covers a layer range of a block."""
+    wl = _with_files(workloads.make(4, max_blocks=29))
+    say("case file layer ranges")
+    with tempfile.TemporaryDirectory() as d:
+        run = WorkloadRun(wl, device=0, file_dir=d)
+        try:
+            host = run.fill_source(keep_host=True)
+            run.fill_dst()
+            run.place_all()
+            q = wl.requests[0]
+            s = torch.cuda.current_stream().cuda_stream
+            L = wl.shape.layers
+            kp, vp = run.layer_ptrs(run.src)
+            for lo, hi in [(0, 5), (5, 6), (6, L)]:
+                run.pool.store_layers(run.maps[q.request_id], q.src_slots, wl.src_num_slots, lo, hi, kp, vp, s)
+            kd, vd = run.layer_ptrs(run.dst)
+            m = run.retrieve_maps[q.request_id]
+            for l in range(L):
+                run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, l, l + 1, kd, vd, s)
+            torch.cuda.synchronize()
+            check_full(wl, run, host)
+            run.fill_dst()
+            run.pool.retrieve_layers(m, q.dst_slots, wl.dst_num_slots, 3, 7, kd, vd, s)
+            torch.cuda.synchronize()
+            _, _, expect = oracle_expectation(wl, run, host)
+            got = run.dst.cpu().numpy().view(np.uint16)
+            assert np.array_equal(got[3:7], expect[3:7])
+            assert np.all(got[:3] == SENTINEL) and np.all(got[7:] == SENTINEL)
+        finally:
+            run.close()
+
+
+def test_extend_release_and_reuse_with_files():
+    """A request grown by two offload sets (each stored as it arrives), retrieved whole; then
+    released, and a new request placed over the same ranges and stored with other values."""
+    wl = _with_files(workloads.make(2, max_blocks=30))
+    regions = [dataclasses.replace(r) for r in wl.regions]
+    workloads._size_regions(regions, [30, 30, 30], wl.shape.block_bytes)
+    wl = dataclasses.replace(wl, regions=regions)
+    say("case file extend / reuse")
+    with tempfile.TemporaryDirectory() as d:
+        run = WorkloadRun(wl, device=0, file_dir=d)
+        try:
+            host = run.fill_source(keep_host=True)
+            run.fill_dst()
+            q = wl.requests[0]
+            s = torch.cuda.current_stream().cuda_stream
+            kp, vp = run.layer_ptrs(run.src)
+            parts = [run.pool.place(q.request_id, 12), run.pool.extend(q.request_id, 11),
+                     run.pool.extend(q.request_id, q.n_present - 23)]
+            at = 0
+            for m in parts:
+                run.pool.store(m, q.src_slots[at:at + len(m)], wl.src_num_slots, kp, vp, s)
+                at += len(m)
+            kd, vd = run.layer_ptrs(run.dst)
+            run.pool.retrieve_request(q.request_id, q.dst_slots, wl.dst_num_slots, kd, vd, s)
+            torch.cuda.synchronize()
+            got = run.dst.cpu().numpy().view(np.uint16)
+            src = host
+            for b in range(q.n_present):
+                assert np.array_equal(got[:, :, q.dst_slots[b]], src[:, :, q.src_slots[b]]), "block %d" % b
+            run.pool.release(q.request_id)
+            new = run.pool.place(99, q.n_present)                 # first fit: over the released ranges
+            assert int(new["offset"].min()) == 0
+            run.src.bitwise_not_()
+            run.pool.store(new, q.src_slots, wl.src_num_slots, kp, vp, s)
+            run.fill_dst()
+            run.pool.retrieve(new, q.dst_slots[:q.n_present], wl.dst_num_slots, kd, vd, s)
+            torch.cuda.synchronize()
+            got = run.dst.cpu().numpy().view(np.uint16)
+            for b in range(q.n_present):
+                assert np.array_equal(got[:, :, q.dst_slots[b]], ~src[:, :, q.src_slots[b]]), "reused block %d" % b
+        finally:
+            run.close()
+
+
+def test_file_region_rules():
+    """A path that exists as a regular file is refused (not overwritten); a shape whose chunks are not
+    sector multiples is refused; the allocation-free retrieve refuses file entries; a placement-only
+    pool with file regions places without paths; measured file bandwidth is positive."""
+    spec = K.KVSpec(2, 2, 64)                                  # chunk 4 KiB
+    with tempfile.TemporaryDirectory() as d:
+        taken = os.path.join(d, "taken.bin")
+        with open(taken, "wb") as f:
+            f.write(b"keep me")
+        with pytest.raises(K.KVPoolError) as ei:
+            K.KVPool([K.Region("file", 1 << 20, path=taken)], [1], spec, 0)
+        assert ei.value.name == "INVALID"
+        assert open(taken, "rb").read() == b"keep me"
+        with pytest.raises(K.KVPoolError) as ei:               # chunk 2304 B: 2 x chunk not a sector multiple
+            K.KVPool([K.Region("file", 1 << 20, path=os.path.join(d, "r.bin"))], [1], K.KVSpec(3, 3, 24), 0)
+        assert ei.value.name == "INVALID" and not os.path.exists(os.path.join(d, "r.bin"))
+        with K.KVPool([K.Region("file", 1 << 20)], [1], spec, -1) as p:   # placement only: no file
+            assert len(p.place(1, 5)) == 5
+        path = os.path.join(d, "f.bin")
+        with K.KVPool([K.Region("file", 8 << 20, path=path), K.Region("staging", 8 << 20)], [1, 1], spec, 0) as p:
+            assert os.path.getsize(path) == 8 << 20
+            m = p.place(1, 6)
+            cache = torch.zeros(2, 2, 8, 2, 16, 64, dtype=torch.int16, device="cuda")
+            ks = [cache[l, 0].data_ptr() for l in range(2)]
+            vs = [cache[l, 1].data_ptr() for l in range(2)]
+            with pytest.raises(K.KVPoolError) as ei:
+                p.retrieve_noalloc(m, list(range(6)), 8, ks, vs, torch.cuda.current_stream().cuda_stream)
+            assert ei.value.name == "INVALID"
+            bw = p.measure_bandwidth(4 << 20)
+            say("file / staging MB/s", bw.tolist())
+            assert bw[0] > 0 and bw[1] > 0
+            assert p.region_info(0)["type"] == K.REGION_FILE and p.region_info(0)["host_ptr"] is None
+        assert not os.path.exists(path), "the pool removes the file it created"

@@ -1,6 +1,7 @@
 """The library's host code under AddressSanitizer and UndefinedBehaviorSanitizer
 (CPU only): tests/native/host_structures_fuzz.cpp built with placement.cpp,
-glt.cpp and bounce.cpp; tests/native/placement_fuzz.cpp driving
+glt.cpp and bounce.cpp; tests/native/file_io_test.cpp built with fileio.cpp
+(the storage tier's plan, worker threads and files); tests/native/placement_fuzz.cpp driving
 placement-only pools through the C ABI of the host-sanitized library;
 tests/native/alloc_failure.cpp failing host allocations inside place, extend
 and release; and the oracle itself (tests/native/oracle_fuzz.c)."""
@@ -24,6 +25,23 @@ def test_host_structures_under_asan_ubsan(tmp_path):
            os.path.join(ROOT, "tests", "native", "host_structures_fuzz.cpp"),
            os.path.join(CSRC, "placement.cpp"), os.path.join(CSRC, "glt.cpp"), os.path.join(CSRC, "bounce.cpp"),
            "-o", exe]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all checks passed" in r.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_file_tier_host_side_under_asan_ubsan(tmp_path):
+    """plan_file's batches on random inputs, the per-region worker threads on O_DIRECT files, and the
+    file-region life cycle (tests/native/file_io_test.cpp)."""
+    exe = str(tmp_path / "file_io_test")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-pthread", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-D__HIP_PLATFORM_AMD__", "-isystem", os.path.join(ROCM, "include"),
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           os.path.join(ROOT, "tests", "native", "file_io_test.cpp"), os.path.join(CSRC, "fileio.cpp"),
+           os.path.join(CSRC, "placement.cpp"), "-o", exe]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
