@@ -310,17 +310,24 @@ def traffic_detail(tr, alg_read, alg_write):
     return out
 
 
-def measure_weights(torch, K, wl):
+def measure_weights(torch, K, wl, file_dir=None):
     """Eq. 1 weights measured by the pool organizer: a pool of the workload's region kinds (1 GiB
-    each) reads 256 MiB of every region into HBM with its class's kernel; host regions share one
-    host link, so their figure is divided by their count (KVP_MEASURE_SHARED_LINK).  MB/s."""
+    each) reads 256 MiB of every region into HBM with its class's kernel (a file region: 256 MiB
+    written to a probe file beside it and read back); host regions share one host link, so their
+    figure is divided by their count (KVP_MEASURE_SHARED_LINK), and file regions are read all at
+    once, as a retrieve reads them (KVP_MEASURE_FILES_TOGETHER).  MB/s."""
+    import tempfile
     regions = []
-    for r in wl.regions:
-        regions.append(K.Region("host", 1 << 30, -1) if r.kind == "host" else K.Region("staging", 1 << 30))
+    for i, r in enumerate(wl.regions):
+        if r.kind == "file":
+            path = os.path.join(file_dir or tempfile.gettempdir(), "kvpool-measure-%d-%d.bin" % (os.getpid(), i))
+            regions.append(K.Region("file", 1 << 30, -1, 0, path))
+        else:
+            regions.append(K.Region("host", 1 << 30, -1) if r.kind == "host" else K.Region("staging", 1 << 30))
     sh = wl.shape
     spec = K.KVSpec(sh.layers, sh.kv_heads, sh.head_dim, sh.block_size, sh.elem_bytes, wl.layout)
     with K.KVPool(regions, [1] * len(regions), spec, 0) as p:
-        w = p.measure_bandwidth(256 << 20, K.MEASURE_SHARED_LINK)
+        w = p.measure_bandwidth(256 << 20, K.MEASURE_SHARED_LINK | K.MEASURE_FILES_TOGETHER)
     torch.cuda.synchronize()
     return [int(x) for x in w]
 
@@ -832,6 +839,9 @@ def main():
     ap.add_argument("--weights", default=None,
                     help="with --measured-weights: comma-separated weights measured by an earlier run (MB/s), used "
                          "instead of measuring again, so that repeated runs (profiler passes) place identically")
+    ap.add_argument("--file-regions", action="store_true",
+                    help="the workload's staging regions as file regions (O_DIRECT files, one worker per region)")
+    ap.add_argument("--file-dir", default=None, help="with --file-regions: directory of the region files")
     ap.add_argument("--layerwise", action="store_true",
                     help="also time the request retrieved one layer per call (kv_pool_retrieve_layers)")
     ap.add_argument("--summarize-pmc", metavar="DIR", default=None,
@@ -879,6 +889,10 @@ def main():
     torch.cuda.set_device(0)
     wl = workloads.make(args.config, layout=args.layout, context_tokens=args.context)
     sh = wl.shape
+    if args.file_regions:     # the staging regions become file regions: the storage tier
+        import dataclasses
+        wl.regions = [dataclasses.replace(r, kind="file") if r.kind == "staging" else r for r in wl.regions]
+        wl.name += "-file"
     measured = None
     if args.weights and not args.measured_weights:
         raise SystemExit("--weights gives measured weights: use it with --measured-weights")
@@ -888,7 +902,7 @@ def main():
             if len(measured) != len(wl.regions) or min(measured) <= 0:
                 raise SystemExit("--weights needs one positive integer per region (%d)" % len(wl.regions))
         else:
-            measured = measure_weights(torch, K, wl)
+            measured = measure_weights(torch, K, wl, args.file_dir)
         import dataclasses
         wl.regions = [dataclasses.replace(r, weight=int(w)) for r, w in zip(wl.regions, measured)]
         workloads._size_regions(wl.regions, [q.n_present for q in wl.requests], sh.block_bytes)
@@ -896,7 +910,7 @@ def main():
         log("measured weights (MB/s, host regions sharing one link):", measured)
     log("workload", wl.name, "retrieved bytes", wl.retrieved_bytes)
     t = time.perf_counter()
-    run = WorkloadRun(wl, device=0, coherence=args.coherence)
+    run = WorkloadRun(wl, device=0, coherence=args.coherence, file_dir=args.file_dir)
     t_create = time.perf_counter() - t
     if args.host_grid or args.host_flags:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
@@ -927,11 +941,21 @@ def main():
     store_t = run.pool.last_timing() if len(wl.requests) == 1 else None
     log("placed in %.3f ms, stored in %.1f ms" % (t_place * 1e3, store_wall * 1e3))
 
-    host_blocks = sum(int(np.isin(run.maps[q.request_id]["region"],
-                                  [i for i, r in enumerate(wl.regions) if r.kind == "host"]).sum())
-                      for q in wl.requests)
-    stage_blocks = wl.present_blocks - host_blocks
+    def kind_idx(kind):
+        return [i for i, r in enumerate(wl.regions) if r.kind == kind]
+
+    def blocks_of(kind):
+        return sum(int(np.isin(run.maps[q.request_id]["region"], kind_idx(kind)).sum()) for q in wl.requests)
+
+    host_blocks, stage_blocks, file_blocks = blocks_of("host"), blocks_of("staging"), blocks_of("file")
     host_bytes, stage_bytes = host_blocks * sh.block_bytes, stage_blocks * sh.block_bytes
+    file_bytes = file_blocks * sh.block_bytes
+
+    def only(q, kind):
+        """The request's map with every block outside regions of this kind marked absent."""
+        m = run.retrieve_maps[q.request_id].copy()
+        m["region"][~np.isin(m["region"], kind_idx(kind))] = K.ABSENT
+        return m
 
     cur = torch.cuda.current_stream()
     run.pool.set_timing(False)
@@ -977,9 +1001,7 @@ def main():
     stage_only = None
     if stage_blocks and len(wl.requests) == 1:
         q = wl.requests[0]
-        m = run.retrieve_maps[q.request_id].copy()
-        host_idx = [i for i, r in enumerate(wl.regions) if r.kind == "host"]
-        m["region"][np.isin(m["region"], host_idx)] = K.ABSENT
+        m = only(q, "staging")
         kp, vp = run.layer_ptrs(run.dst)
         for _ in range(args.warmup):
             run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
@@ -995,11 +1017,9 @@ def main():
 
     # zero-copy gather alone, from a map without the staging blocks (the link with nothing beside it)
     host_only = None
-    if host_blocks and stage_blocks and len(wl.requests) == 1 and not args.sdma:
+    if host_blocks and (stage_blocks or file_blocks) and len(wl.requests) == 1 and not args.sdma:
         q = wl.requests[0]
-        m = run.retrieve_maps[q.request_id].copy()
-        stage_idx = [i for i, r in enumerate(wl.regions) if r.kind != "host"]
-        m["region"][np.isin(m["region"], stage_idx)] = K.ABSENT
+        m = only(q, "host")
         kp, vp = run.layer_ptrs(run.dst)
         for _ in range(args.warmup):
             run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream)
@@ -1014,6 +1034,34 @@ def main():
                      "gbps": round(host_bytes / (avg / 1e3) / 1e9, 2)}
 
     log("timed region done: %.3f ms per retrieve" % ms_per_step)
+    # the storage tier alone: the file regions' blocks retrieved and stored by themselves, call to
+    # completion (the file reads and writes run inside the calls)
+    file_tier = None
+    if file_blocks and len(wl.requests) == 1:
+        q = wl.requests[0]
+        m = only(q, "file")
+        kp, vp = run.layer_ptrs(run.dst)
+        ks, vs = run.layer_ptrs(run.src)
+
+        def wall(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for _ in range(reps):
+                fn()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t) / reps * 1e3
+        rt = wall(lambda: run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream), args.steps)
+        st = wall(lambda: run.pool.store(m[:q.n_present], q.src_slots, wl.src_num_slots, ks, vs, cur.cuda_stream),
+                  max(1, args.steps // 2))
+        probe = [int(x) for i, x in enumerate(run.pool.measure_bandwidth(256 << 20)) if wl.regions[i].kind == "file"]
+        file_tier = {"bytes": file_bytes, "blocks": file_blocks,
+                     "retrieve_alone_ms": round(rt, 2), "retrieve_alone_gbps": round(file_bytes / rt / 1e6, 3),
+                     "store_alone_ms": round(st, 2), "store_alone_gbps": round(file_bytes / st / 1e6, 3),
+                     "read_probe_mbps_per_region": probe,
+                     "files": "O_DIRECT files, one worker thread per region",
+                     "device": "the machine's virtio block device (a VM disk, not an NVMe drive)"}
+        log("file tier: retrieve %.1f ms, store %.1f ms" % (rt, st))
     # the timed steps' result: every present block of every request equals its source slot (round
     # trip, compared on the GPU layer by layer), every other slot still holds the fill value
     verified = round_trip_ok(torch, run, wl)
@@ -1038,12 +1086,10 @@ def main():
                  "staging_kernel_ms_avg":
                      round(sm["staging_ms_sum"] / sm["staging_calls"], 3) if sm["staging_calls"] else None}
         log("store timed: %.3f ms" % st_ms)
-        # the staging-class store alone (HBM -> HBM), from a map without the host blocks
+        # the staging-class store alone (HBM -> HBM), from a map with only the staging blocks
         if stage_blocks:
             q = wl.requests[0]
-            m = run.maps[q.request_id].copy()
-            host_idx = [i for i, r in enumerate(wl.regions) if r.kind == "host"]
-            m["region"][np.isin(m["region"], host_idx)] = K.ABSENT
+            m = only(q, "staging")[:q.n_present]
             kp, vp = run.layer_ptrs(run.src)
             for _ in range(args.warmup):
                 run.pool.store(m, q.src_slots, wl.src_num_slots, kp, vp, cur.cuda_stream)
@@ -1217,6 +1263,7 @@ def main():
         "store": store,
         "roofline_store": store_roof,
         "roofline_store_staging": store_staging_roof,
+        "file_tier": file_tier,
         "layerwise": layerwise,
         "copy_engine_retrieve": copy_engine,
         "place_ms": round(t_place * 1e3, 3),

@@ -368,6 +368,7 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
 /* ---- measured bandwidths (pool organizer, Sec. 4.1.2) ---- */
 
 #define KVP_MEASURE_SHARED_LINK 1u  /* divide host regions' rate by their count */
+#define KVP_MEASURE_FILES_TOGETHER 2u /* read all file regions at once, as a retrieve does */
 
 /*
  * Measure each region's read rate into HBM, the b_i of Eq. 1: the region's
@@ -375,8 +376,15 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
  * into a scratch buffer (allocated for the call); best of 3 timed runs after
  * a warm-up, in MB/s (>= 1).  Host regions are measured one at a time; all of
  * them reach the GPU over the same host link, so KVP_MEASURE_SHARED_LINK
- * divides their figure by the number of host regions.  Region contents are
- * read, not changed.  Waits for the probes.
+ * divides their figure by the number of host regions.  A file region is read
+ * the way a retrieve reads it: its worker thread reads its file into the
+ * pool's pinned ring (min(probe_bytes, its share of the ring) bytes, best of 3
+ * after a warm-up; a file the pool created is measured on a probe file
+ * written beside it first, a block device is read in place from its start).
+ * Without KVP_MEASURE_FILES_TOGETHER one region at a time, with it all file
+ * regions at once, so that regions sharing one device each get the rate they
+ * sustain beside the others.  Region contents are read, not
+ * changed.  Waits for the probes.
  *   probe_bytes   in [64 KiB, 64 GiB].
  *   mbps_out[n_regions]   caller-owned.
  * Errors: INVALID (placement-only pool, bad flags or size), NOMEM, HIP.

@@ -3,7 +3,11 @@
 // reads, launch settings of the two kernel classes, the copy-engine ring, and
 // the HIP-event timing of store / retrieve calls.
 
+#include <fcntl.h>
+#include <unistd.h>
+
 #include <algorithm>
+#include <cerrno>
 #include <cstring>
 
 #include "internal.hpp"
@@ -11,6 +15,94 @@
 namespace kvp {
 
 // ---------------------------------------------------------------- measured bandwidths (Sec. 4.1.2)
+
+// Read rates of file regions, MB/s, through the path a retrieve takes: the
+// region's worker thread reads its file into the pool's pinned ring (through
+// its own aligned buffer).  A created file is measured on a probe file of its
+// own beside it, written first by the same worker, since a range that was
+// never written reads without touching the device; a block device is read in
+// place from its start.  Each region reads n bytes per pass (its share of the
+// ring, at most probe_bytes), one pass to warm up and the best of 3 after it.
+// Alone: one region at a time.  Together: every region at once, as a retrieve
+// reads them, so that regions sharing a device each get the rate they sustain
+// beside the others.  The GPU's move out of the ring is not timed; it runs
+// far faster.  Caller holds the pool lock; nothing else uses the ring.
+void measure_file_regions(Pool &p, uint64_t probe_bytes, bool together, uint64_t *mbps)
+{
+    std::vector<size_t> idx;
+    for (size_t r = 0; r < p.regions.size(); ++r)
+        if (p.regions[r].desc.type == KVP_REGION_FILE) idx.push_back(r);
+    if (idx.empty()) return;
+    for (uint32_t j = 0; j < kFileSlots; ++j) {   // the ring is idle
+        io_drain(p.file_io[j]);
+        if (p.file_free_rec[j]) check_hip(hipEventSynchronize(p.file_free[j]), "hipEventSynchronize");
+    }
+    const uint64_t share = kFileSlots * p.file_slot_bytes / idx.size() / kSector * kSector;
+    struct Probe {
+        const Region *r = nullptr;
+        uint64_t n = 0;
+        char *buf = nullptr;      // its part of the ring
+        int fd = -1;
+        std::string path;         // own probe file, removed afterwards
+        IoGroup g;
+        double best = 0.0;
+        ~Probe()
+        {
+            io_drain(g);
+            if (!path.empty()) {
+                if (fd >= 0) ::close(fd);
+                ::unlink(path.c_str());
+            }
+        }
+    };
+    std::vector<std::unique_ptr<Probe>> ps;
+    for (size_t i = 0; i < idx.size(); ++i) {
+        ps.push_back(std::make_unique<Probe>());
+        Probe &q = *ps.back();
+        q.r = &p.regions[idx[i]];
+        q.n = std::max<uint64_t>(kSector, std::min({probe_bytes, q.r->capacity, share}) / kSector * kSector);
+        q.buf = p.file_ring + i * share;
+        q.fd = q.r->fd;
+        if (q.r->file_owned) {
+            const std::string path = q.r->file_path + ".probe";
+            const int oflags =
+                O_RDWR | O_CLOEXEC | O_CREAT | O_EXCL | ((q.r->flags_used & KVP_FILE_BUFFERED) ? 0 : O_DIRECT);
+            q.fd = ::open(path.c_str(), oflags, 0600);
+            if (q.fd < 0) fail(KVP_ERR_IO, "cannot create probe file " + path + ": " + std::strerror(errno));
+            q.path = path;
+            std::memset(q.buf, 0x5a, static_cast<size_t>(q.n));
+            p.workers->submit(q.r->worker, IoJob{q.fd, true, 0, q.n, q.buf, &q.g});
+            io_wait(q.g);
+            if (::fsync(q.fd) != 0) fail(KVP_ERR_IO, "probe file " + path + ": " + std::strerror(errno));
+        }
+    }
+    auto start = [&](Probe &q) {
+        p.workers->submit(q.r->worker, IoJob{q.fd, false, 0, q.n, q.buf, &q.g});
+    };
+    auto finish = [&](Probe &q, std::chrono::steady_clock::time_point t0, bool timed) {
+        io_wait(q.g);
+        const double s = std::chrono::duration<double>(q.g.done_at - t0).count();
+        if (timed && s > 0.0 && (q.best == 0.0 || s < q.best)) q.best = s;
+    };
+    for (int it = 0; it < 4; ++it) {
+        if (together) {
+            const auto t0 = std::chrono::steady_clock::now();
+            for (auto &q : ps) start(*q);
+            for (auto &q : ps) finish(*q, t0, it > 0);
+        } else {
+            for (auto &q : ps) {
+                const auto t0 = std::chrono::steady_clock::now();
+                start(*q);
+                finish(*q, t0, it > 0);
+            }
+        }
+    }
+    for (size_t i = 0; i < idx.size(); ++i) {
+        const double rate = ps[i]->best > 0.0 ? static_cast<double>(ps[i]->n) / ps[i]->best / 1e6 : 1.0;
+        mbps[idx[i]] = std::max<uint64_t>(1, static_cast<uint64_t>(rate + 0.5));
+    }
+}
+
 
 // Read rate of every region (bytes from the region into HBM per second, in
 // MB/s): the region-class kernel's launch shape streams min(probe_bytes,
@@ -31,10 +123,7 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
         uint32_t n_host = 0;
         for (size_t r = 0; r < p.regions.size(); ++r) {
             const Region &reg = p.regions[r];
-            if (reg.desc.type == KVP_REGION_FILE) {   // the file side: reads of the region's file
-                mbps[r] = measure_file_region(reg, probe_bytes);
-                continue;
-            }
+            if (reg.desc.type == KVP_REGION_FILE) continue;   // below, all file regions together or one by one
             const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
             n_host += cls == KVP_CLASS_HOST;
             hipStream_t st = p.s_stage;   // one probe at a time
@@ -54,6 +143,8 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
             const double rate = best > 0.f ? static_cast<double>(n) / (best * 1e3) : 1.0;   // MB/s
             mbps[r] = std::max<uint64_t>(1, static_cast<uint64_t>(rate + 0.5));
         }
+        // file regions: their files read into the pinned ring by their workers
+        measure_file_regions(p, probe_bytes, (flags & KVP_MEASURE_FILES_TOGETHER) != 0, mbps);
         // host regions reach the GPU over one shared link: split what one measured alone
         if ((flags & KVP_MEASURE_SHARED_LINK) && n_host > 1)
             for (size_t r = 0; r < p.regions.size(); ++r)
@@ -73,7 +164,7 @@ void pool_measure(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_
 {
     if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to measure");
     if (!mbps_out) fail(KVP_ERR_INVALID, "null output");
-    if (flags & ~KVP_MEASURE_SHARED_LINK) fail(KVP_ERR_INVALID, "unknown flags");
+    if (flags & ~(KVP_MEASURE_SHARED_LINK | KVP_MEASURE_FILES_TOGETHER)) fail(KVP_ERR_INVALID, "unknown flags");
     if (probe_bytes < (1u << 16) || probe_bytes > (1ull << 36)) fail(KVP_ERR_INVALID, "probe_bytes outside [64 KiB, 64 GiB]");
     std::lock_guard<std::mutex> lock(p.mu);
     DeviceScope dev(p.device);

@@ -205,7 +205,7 @@ void FileWorkers::run(Worker &w)
                 } catch (...) {
                 }
             }
-            --j.group->pending;
+            if (--j.group->pending == 0) j.group->done_at = std::chrono::steady_clock::now();
         }
         j.group->cv.notify_all();
     }
@@ -308,57 +308,6 @@ void file_region_read(const Region &r, uint64_t offset, uint64_t bytes, void *ds
         throw;
     }
     std::free(buf);
-}
-
-// Read rate of a file region, MB/s.  A created file is measured on a probe
-// file of its own beside it (written, synced, then read back best of 3 after
-// one pass), since a range that was never written reads without touching the
-// device; a block device is read in place from its start.  Only the file side
-// is timed: the copy into the pinned slot and the GPU's move from it run far
-// faster.
-uint64_t measure_file_region(const Region &r, uint64_t probe_bytes)
-{
-    const uint64_t n = std::max<uint64_t>(kSector, std::min(probe_bytes, r.capacity) / kSector * kSector);
-    void *mem = nullptr;
-    if (::posix_memalign(&mem, kSector, static_cast<size_t>(n)) != 0 || !mem) fail(KVP_ERR_NOMEM, "probe buffer");
-    struct Free {
-        void *m;
-        ~Free() { std::free(m); }
-    } release{mem};
-    char *buf = static_cast<char *>(mem);
-    std::memset(buf, 0x5a, static_cast<size_t>(n));
-    int fd = r.fd;
-    std::string probe;
-    if (r.file_owned) {
-        probe = r.file_path + ".probe";
-        const int oflags = O_RDWR | O_CLOEXEC | O_CREAT | O_EXCL | ((r.flags_used & KVP_FILE_BUFFERED) ? 0 : O_DIRECT);
-        fd = ::open(probe.c_str(), oflags, 0600);
-        if (fd < 0) fail(KVP_ERR_IO, "cannot create probe file " + probe + ": " + std::strerror(errno));
-        IoJob w{fd, true, 0, n, buf, nullptr};
-        std::string what;
-        if (transfer(w, what) || ::fsync(fd) != 0) {
-            ::close(fd);
-            ::unlink(probe.c_str());
-            fail(KVP_ERR_IO, "probe file " + probe + ": " + (what.empty() ? std::strerror(errno) : what));
-        }
-    }
-    double best = 0.0;
-    std::string what;
-    int err = 0;
-    for (int it = 0; it < 4 && !err; ++it) {
-        const auto t0 = std::chrono::steady_clock::now();
-        IoJob j{fd, false, 0, n, buf, nullptr};
-        err = transfer(j, what);
-        const double s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-        if (it > 0 && s > 0.0 && (best == 0.0 || s < best)) best = s;
-    }
-    if (r.file_owned) {
-        ::close(fd);
-        ::unlink(probe.c_str());
-    }
-    if (err) fail(KVP_ERR_IO, "file region " + what);
-    const double rate = best > 0.0 ? static_cast<double>(n) / best / 1e6 : 1.0;
-    return std::max<uint64_t>(1, static_cast<uint64_t>(rate + 0.5));
 }
 
 }  // namespace kvp

@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <chrono>
 #include <condition_variable>
 #include <cstdint>
 #include <map>
@@ -165,6 +166,7 @@ struct IoGroup {                 // a set of reads or writes waited for together
     uint32_t pending = 0;
     int err = 0;                 // first failure's errno, with its message
     std::string what;
+    std::chrono::steady_clock::time_point done_at;   // when pending last fell to 0
 };
 
 struct IoJob {
@@ -229,7 +231,11 @@ struct FileGeometry {
 void open_file_region(Region &r, const char *path);   // creates (or opens a block device); sets fd
 void close_file_region(Region &r) noexcept;          // closes; removes a file the pool created
 void file_region_read(const Region &r, uint64_t offset, uint64_t bytes, void *dst);
-uint64_t measure_file_region(const Region &r, uint64_t probe_bytes);   // MB/s
+struct Pool;
+// MB/s of each file region through the retrieve's own path (the region's
+// worker, into the pool's pinned ring), one region at a time or all at once
+// (together); entries of other regions are left as they are.
+void measure_file_regions(Pool &p, uint64_t probe_bytes, bool together, uint64_t *mbps);
 
 struct LaunchCfg {
     uint32_t grid;

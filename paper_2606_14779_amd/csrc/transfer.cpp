@@ -130,16 +130,31 @@ void run_file_batches(Pool &p, bool gather, const std::vector<FileBatch> &batche
         check_hip(hipEventRecord(p.file_free[bt.ring], sf), "hipEventRecord");
         p.file_free_rec[bt.ring] = true;
     };
+    // the slot is free: its reads or writes and its kernel are done
+    auto slot_free = [&](const FileBatch &bt) {
+        io_wait(p.file_io[bt.ring]);
+        if (p.file_free_rec[bt.ring]) check_hip(hipEventSynchronize(p.file_free[bt.ring]), "hipEventSynchronize");
+    };
     try {
-        for (const FileBatch &bt : batches) {
-            io_wait(p.file_io[bt.ring]);
-            if (p.file_free_rec[bt.ring])
-                check_hip(hipEventSynchronize(p.file_free[bt.ring]), "hipEventSynchronize");
-            if (gather) {
-                submit(bt, false);
-                io_wait(p.file_io[bt.ring]);
-                kernel(bt);
-            } else {
+        if (gather) {
+            // read ahead: the next batch's reads are queued behind this one's (into the
+            // other slot) before this one is waited for, so each worker moves on as soon
+            // as its own part of a batch is read
+            if (!batches.empty()) {
+                slot_free(batches[0]);
+                submit(batches[0], false);
+            }
+            for (size_t i = 0; i < batches.size(); ++i) {
+                if (i + 1 < batches.size()) {
+                    slot_free(batches[i + 1]);
+                    submit(batches[i + 1], false);
+                }
+                io_wait(p.file_io[batches[i].ring]);
+                kernel(batches[i]);
+            }
+        } else {
+            for (const FileBatch &bt : batches) {
+                slot_free(bt);
                 kernel(bt);
                 check_hip(hipEventSynchronize(p.file_free[bt.ring]), "hipEventSynchronize");
                 submit(bt, true);
