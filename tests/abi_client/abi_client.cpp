@@ -3,16 +3,22 @@
 // cache filled with a per-element tag, retrieves it into a destination cache
 // under a permuted block table, and checks every element on the host.  Then
 // it retrieves again through the copy-engine transport with one-block ring
-// slots, in two layer ranges, and checks again.
+// slots, in two layer ranges, and checks again.  Last, a second pool made by
+// kv_pool_create_files with a host and a file region (a file created in a
+// temporary directory) stores and retrieves the request through the storage
+// tier and is checked the same way; destroying it removes the file.
 // With the argument "exit-open" it instead leaves the pool open with a
 // retrieve still enqueued and returns from main: the process must end
 // cleanly (the library registers nothing that runs at exit).
 // Built by the package build step; run by tests/test_abi_client.py (GPU).
 #include <hip/hip_runtime.h>
+#include <sys/stat.h>
+#include <unistd.h>
 
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <string>
 #include <vector>
 
 #include "kvpool.h"
@@ -150,6 +156,34 @@ int main(int argc, char **argv)
     if (kv_pool_extend(pool, 78, 1, b.data()) != KVP_ERR_NOTFOUND) ++bad;
     TRY(kv_pool_release(pool, 77));
     kv_pool_destroy(pool);
+
+    // the storage tier: a host region and a file region, weights 1:2, ring slots of four blocks
+    char dir_tmpl[] = "/tmp/kvpool-abi-XXXXXX";
+    if (!::mkdtemp(dir_tmpl)) {
+        std::fprintf(stderr, "mkdtemp failed\n");
+        return 1;
+    }
+    const std::string file_path = std::string(dir_tmpl) + "/region1.bin";
+    kvp_region_desc fregions[2] = {{KVP_REGION_HOST, -1, 64 * block_bytes, KVP_HOST_DEFAULT, 0},
+                                   {KVP_REGION_FILE, -1, 64 * block_bytes, 0, 0}};
+    const char *paths[2] = {nullptr, file_path.c_str()};
+    uint64_t fbw[2] = {1, 2};
+    kvp_pool *fpool = nullptr;
+    TRY(kv_pool_create_files(fregions, fbw, 2, &spec, 0, paths, &fpool));
+    TRY(kv_pool_set_file_ring(fpool, 4 * block_bytes));
+    TRY(kv_pool_place(fpool, 5, n, map.data()));
+    uint32_t on_file = 0;
+    for (uint32_t b = 0; b < n; ++b) on_file += map[b].region == 1;
+    for (uint32_t i = 0; i < 2 * L; ++i) HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
+    TRY(kv_pool_store(fpool, map.data(), n, src_table.data(), slots, k_src.data(), v_src.data(), stream));
+    TRY(kv_pool_retrieve_request(fpool, 5, n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
+    HIPTRY(hipStreamSynchronize(stream));
+    if (check()) return 1;
+    struct stat st;
+    if (on_file == 0 || ::stat(file_path.c_str(), &st) != 0 || uint64_t(st.st_size) != 64 * block_bytes) ++bad;
+    kv_pool_destroy(fpool);
+    if (::stat(file_path.c_str(), &st) == 0) ++bad;     // the pool removes the file it created
+    ::rmdir(dir_tmpl);
     HIPTRY(hipStreamDestroy(stream));
     for (void *p : src) HIPTRY(hipFree(p));
     for (void *p : dst) HIPTRY(hipFree(p));
@@ -157,7 +191,7 @@ int main(int argc, char **argv)
         std::fprintf(stderr, "abi client: %llu mismatching chunks or elements\n", (unsigned long long)bad);
         return 1;
     }
-    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, allocation-free call, copy engines both ways)\n",
+    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, allocation-free call, copy engines both ways, file region)\n",
                 n);
     return 0;
 }

@@ -52,19 +52,24 @@ def _need_gpu():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("tier", ["memory", "file"])
 @pytest.mark.parametrize("seed", SEEDS)
 @pytest.mark.parametrize("layout", [0, 1])
-def test_random_lifecycle(layout, seed):
+def test_random_lifecycle(layout, seed, tier, tmp_path):
+    """tier "file": the last region is a file region (the storage tier) instead of HBM staging."""
     rng = np.random.default_rng(seed + layout)
     path_rng = np.random.default_rng(seed + 17 + layout)   # upload bit: apart, so rng's sequence is unchanged
     ext_rng = np.random.default_rng(seed + 29 + layout)    # extensions: apart as well
     shape = workloads.KVShape("lifecycle", L, H, D)
     bb = shape.block_bytes
     weights = [3, 1, 2, 2]
-    kinds = ["host", "staging", "host", "staging"]
+    kinds = ["host", "staging", "host", "staging" if tier == "memory" else "file"]
     caps = [150 * bb, 60 * bb, 110 * bb, 110 * bb]   # small enough to fill: NOSPACE and fragmentation
-    pool = K.KVPool([K.Region(k, c) for k, c in zip(kinds, caps)], weights,
+    path = str(tmp_path / "region3.bin")
+    pool = K.KVPool([K.Region(k, c, path=path if k == "file" else None) for k, c in zip(kinds, caps)], weights,
                     K.KVSpec(L, H, D, BS, 2, layout), 0)
+    if tier == "file":
+        pool.set_file_ring(16 * bb)     # several batches per call, the ring wrapping
     ora = oracle.Pool(weights, caps, bb)
     dev = torch.device("cuda", 0)
     src = torch.empty((L, 2, SRC_SLOTS, H, BS, D), dtype=torch.int16, device=dev)
