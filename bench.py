@@ -1051,7 +1051,13 @@ def main():
                 fn()
             torch.cuda.synchronize()
             return (time.perf_counter() - t) / reps * 1e3
+        def together():   # the file regions read all at once by their workers, MB/s summed
+            w = run.pool.measure_bandwidth(256 << 20, K.MEASURE_FILES_TOGETHER)
+            return int(sum(int(x) for i, x in enumerate(w) if wl.regions[i].kind == "file"))
+        # the disk's rate drifts within a run: probe it on both sides of the timed retrieves
+        before = together()
         rt = wall(lambda: run.pool.retrieve(m, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream), args.steps)
+        after = together()
         st = wall(lambda: run.pool.store(m[:q.n_present], q.src_slots, wl.src_num_slots, ks, vs, cur.cuda_stream),
                   max(1, args.steps // 2))
         probe = [int(x) for i, x in enumerate(run.pool.measure_bandwidth(256 << 20)) if wl.regions[i].kind == "file"]
@@ -1059,6 +1065,8 @@ def main():
                      "retrieve_alone_ms": round(rt, 2), "retrieve_alone_gbps": round(file_bytes / rt / 1e6, 3),
                      "store_alone_ms": round(st, 2), "store_alone_gbps": round(file_bytes / st / 1e6, 3),
                      "read_probe_mbps_per_region": probe,
+                     "read_probe_together_mbps": [before, after],
+                     "retrieve_vs_probe_together": round(file_bytes / rt / 1e3 / ((before + after) / 2), 3),
                      "files": "O_DIRECT files, one worker thread per region",
                      "device": "the machine's virtio block device (a VM disk, not an NVMe drive)"}
         log("file tier: retrieve %.1f ms, store %.1f ms" % (rt, st))

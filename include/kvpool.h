@@ -382,8 +382,9 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
  * after a warm-up; a file the pool created is measured on a probe file
  * written beside it first, a block device is read in place from its start).
  * Without KVP_MEASURE_FILES_TOGETHER one region at a time, with it all file
- * regions at once, so that regions sharing one device each get the rate they
- * sustain beside the others.  Region contents are read, not
+ * regions at once, each credited with its probe bytes over the time until the
+ * last of them finished (best of 3), so that regions sharing one device get
+ * rates that add up to what they deliver together.  Region contents are read, not
  * changed.  Waits for the probes.
  *   probe_bytes   in [64 KiB, 64 GiB].
  *   mbps_out[n_regions]   caller-owned.

@@ -84,11 +84,17 @@ void measure_file_regions(Pool &p, uint64_t probe_bytes, bool together, uint64_t
         const double s = std::chrono::duration<double>(q.g.done_at - t0).count();
         if (timed && s > 0.0 && (q.best == 0.0 || s < q.best)) q.best = s;
     };
+    double group_best = 0.0;   // together: the time until the last region finished
     for (int it = 0; it < 4; ++it) {
         if (together) {
             const auto t0 = std::chrono::steady_clock::now();
             for (auto &q : ps) start(*q);
-            for (auto &q : ps) finish(*q, t0, it > 0);
+            double last = 0.0;
+            for (auto &q : ps) {
+                finish(*q, t0, false);
+                last = std::max(last, std::chrono::duration<double>(q->g.done_at - t0).count());
+            }
+            if (it > 0 && last > 0.0 && (group_best == 0.0 || last < group_best)) group_best = last;
         } else {
             for (auto &q : ps) {
                 const auto t0 = std::chrono::steady_clock::now();
@@ -97,8 +103,11 @@ void measure_file_regions(Pool &p, uint64_t probe_bytes, bool together, uint64_t
             }
         }
     }
+    // together, each region is credited with its bytes over the whole group's time, so the
+    // rates add up to what the regions deliver at once (a retrieve waits for the last one)
     for (size_t i = 0; i < idx.size(); ++i) {
-        const double rate = ps[i]->best > 0.0 ? static_cast<double>(ps[i]->n) / ps[i]->best / 1e6 : 1.0;
+        const double t = together ? group_best : ps[i]->best;
+        const double rate = t > 0.0 ? static_cast<double>(ps[i]->n) / t / 1e6 : 1.0;
         mbps[idx[i]] = std::max<uint64_t>(1, static_cast<uint64_t>(rate + 0.5));
     }
 }

@@ -48,6 +48,37 @@ void plan_file(const FileGeometry &g, std::vector<HostBlock> &blocks, uint64_t s
     std::stable_sort(blocks.begin(), blocks.end(), [](const HostBlock &a, const HostBlock &b) {
         return a.region != b.region ? a.region < b.region : a.offset < b.offset;
     });
+    // Every batch takes each region's blocks in proportion to the region's share of the
+    // call, so all of the regions' workers read (or write) during every batch.  The
+    // regions are merged by each block's place in its own region, (2i + 1) / (2 n_r) for
+    // the i-th of n_r blocks (ties by region); a batch is the next `per` blocks of that
+    // order, grouped by region again, where each region's blocks stay in offset order.
+    const uint64_t per = std::max<uint64_t>(1, g.slot_bytes / width);
+    if (blocks.size() > per) {
+        struct Ranked {
+            HostBlock b;
+            uint64_t i, n;   // place in its region, blocks of its region
+        };
+        std::vector<Ranked> order;
+        order.reserve(blocks.size());
+        for (size_t s = 0; s < blocks.size();) {
+            size_t e = s;
+            while (e < blocks.size() && blocks[e].region == blocks[s].region) ++e;
+            for (size_t k = s; k < e; ++k) order.push_back(Ranked{blocks[k], k - s, e - s});
+            s = e;
+        }
+        std::stable_sort(order.begin(), order.end(), [](const Ranked &a, const Ranked &b) {
+            const unsigned __int128 x = static_cast<unsigned __int128>(2 * a.i + 1) * b.n;
+            const unsigned __int128 y = static_cast<unsigned __int128>(2 * b.i + 1) * a.n;
+            return x != y ? x < y : a.b.region < b.b.region;
+        });
+        for (size_t s = 0; s < order.size(); s += per) {
+            const auto e = order.begin() + static_cast<std::ptrdiff_t>(std::min<uint64_t>(order.size(), s + per));
+            std::stable_sort(order.begin() + static_cast<std::ptrdiff_t>(s), e,
+                             [](const Ranked &a, const Ranked &b) { return a.b.region < b.b.region; });
+        }
+        for (size_t k = 0; k < order.size(); ++k) blocks[k] = order[k].b;
+    }
     const uint64_t back = static_cast<uint64_t>(chunk0) * g.chunk_bytes;   // the kernel adds (chunk0 + k) chunks
     uint32_t ring = g.next;
     uint64_t used = g.slot_bytes;   // forces a new batch for the first block

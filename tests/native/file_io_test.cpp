@@ -6,7 +6,10 @@
 //                 span of its own region, at the span's matching place in the
 //                 batch's slot; spans of a batch do not overlap in the slot and
 //                 fit it; batches take the ring's slots in turn; whole blocks
-//                 at consecutive offsets of a region share a span
+//                 at consecutive offsets of a region share a span; every batch
+//                 but the last is full, and after every batch each region has
+//                 sent its proportional share of the blocks, to within the
+//                 merge's bound (all regions busy in every batch)
 //   FileWorkers   one worker per file, O_DIRECT files in a temporary
 //                 directory: spans written from an aligned buffer by the
 //                 workers and read back by them equal the bytes written; a
@@ -119,6 +122,19 @@ static void plan_properties(std::mt19937_64 &rng)
         }
         CHECK(items_seen == items.size() && spans_seen == spans.size());
         for (int h : hits) CHECK(h == 1);
+        // full batches, and each region's share of the first m blocks: |c_r - m n_r / n| <= 1/2 + R n_r / (2 n)
+        const uint64_t per = slot_bytes / width;
+        std::vector<int64_t> n_r(n_regions, 0), c_r(n_regions, 0);
+        for (const HostBlock &b : orig) ++n_r[b.region];
+        int64_t m = 0;
+        const int64_t nn = static_cast<int64_t>(orig.size());
+        for (size_t bi = 0; bi < batches.size(); ++bi) {
+            if (bi + 1 < batches.size()) CHECK(batches[bi].n == per);
+            for (uint32_t i = batches[bi].first; i < batches[bi].first + batches[bi].n; ++i) ++c_r[orig[items[i].slot].region];
+            m += batches[bi].n;
+            for (uint32_t r = 0; r < n_regions; ++r)
+                CHECK(2 * std::llabs(c_r[r] * nn - m * n_r[r]) <= nn + static_cast<int64_t>(n_regions) * n_r[r]);
+        }
         // whole blocks of one region at consecutive offsets in one slot: one span
         if (width == bb)
             for (size_t s = 1; s < spans.size(); ++s)
