@@ -47,8 +47,9 @@ def _events_ms(torch, fn, iters=3):
     return out
 
 
-HBM_PROBE_GRIDS = (2048, 8192, 32768, 65536)   # grids of the 4 GiB HBM copy sweep
-SAME_BYTES_GRIDS = (16384, 131072)   # grids of the same-bytes copy probe: none of the 4 GiB sweep's
+HBM_PROBE_GRIDS = (2048, 8192, 32768, 65536, 262144)   # grids of the 4 GiB HBM copy sweep (262144: one
+                                                       # 16 KiB tile per workgroup)
+SAME_BYTES_GRIDS = (16384, 131072, 1048576)   # grids of the same-bytes copy probe: none of the 4 GiB sweep's
 
 
 def probes(torch, K, run, nbytes, same_bytes=0):
@@ -66,7 +67,8 @@ def probes(torch, K, run, nbytes, same_bytes=0):
         a.fill_(1)
         best, bgrid, bflags = 0.0, 0, 0
         for grid in SAME_BYTES_GRIDS:
-            for fl in (K.LAUNCH_SPLIT2, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD):
+            for fl in (K.LAUNCH_SPLIT2, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD,
+                       K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE):
                 ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(b.data_ptr(), a.data_ptr(), n, grid, fl,
                                                                        cur.cuda_stream)))
                 if n / ms / 1e6 > best:
@@ -79,7 +81,8 @@ def probes(torch, K, run, nbytes, same_bytes=0):
     a.fill_(1)
     best_k, best_grid, best_flags = 0.0, 0, 0
     for grid in HBM_PROBE_GRIDS:
-        for fl in (0, K.LAUNCH_NT_LOAD, K.LAUNCH_SPLIT2, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD):
+        for fl in (0, K.LAUNCH_NT_LOAD, K.LAUNCH_SPLIT2, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD,
+                   K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE):
             ms = min(_events_ms(torch, lambda: K.probe_copy_kernel(b.data_ptr(), a.data_ptr(), nbytes, grid, fl,
                                                                    cur.cuda_stream)))
             gbps = nbytes / ms / 1e6

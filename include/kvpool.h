@@ -425,9 +425,11 @@ int kv_pool_set_bandwidths(kvp_pool *pool, const uint64_t *bandwidths);
 
 /* Set the grid (workgroups of 256 threads; 0 = library default) and flags
  * of one (class, op) kernel; flags replace the current ones.  Defaults: host
- * class 12 workgroups (token-major pool: 16, 20 for the store); staging class 65536
- * for the pool_layout 0 retrieve, else 8192, with KVP_LAUNCH_TILE for every retrieve;
- * KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
+ * class 12 workgroups (token-major pool: 16, 20 for the store); staging class
+ * 2^20, i.e. one unit per workgroup up to that many (the launch caps a grid at
+ * the call's unit count), with KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE, plus
+ * KVP_LAUNCH_SPLIT2 for pool_layout 0 and KVP_LAUNCH_CHUNK_MAJOR for its
+ * retrieve; KVP_LAUNCH_NT_STORE for the host-class store; KVP_LAUNCH_LDS for
  * pool_layout 1 except the host-class store.  With the default host-class
  * retrieve grid, a retrieve enqueued while a host-class store kernel of this
  * pool has not finished takes 48 workgroups: with traffic both ways the

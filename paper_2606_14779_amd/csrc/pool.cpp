@@ -364,11 +364,10 @@ uint32_t default_grid(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
     // ms at 16, 201.7 at 12, 206 at 20, 216 at 24), and its store writes the
     // host side in runs of whole chunks while reading HBM by rows (205.3 ms
     // at 20 or 24, 207.4-208.7 at 16, 211.2 at 12).
-    // Staging class: many workgroups so the HBM kernel keeps its share of
-    // the memory queues while the host kernel runs -- for the plain retrieve
-    // up to 65536 workgroup-owned tiles (one per workgroup), 8192 otherwise.
+    // Staging class: one unit per workgroup, with no grid-stride loop (the
+    // launch caps the grid at the call's unit count), up to 2^20 workgroups.
     if (cls == KVP_CLASS_HOST) return spec.pool_layout == 1 ? (op == KVP_OP_STORE ? 20u : 16u) : 12u;
-    return (op == KVP_OP_RETRIEVE && spec.pool_layout == 0) ? 65536u : 8192u;
+    return 1u << 20;
 }
 
 uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
@@ -382,16 +381,23 @@ uint32_t default_flags(uint32_t cls, uint32_t op, const kvp_kv_spec &spec)
     // the host-link side contiguous and measured faster (16 workgroups:
     // 207.4-208.7 ms against 210.6-211.9 through LDS)
     if (spec.pool_layout == 1 && !(cls == KVP_CLASS_HOST && op == KVP_OP_STORE)) f |= KVP_LAUNCH_LDS;
-    // plain HBM retrieve: workgroup-owned tiles of whole chunks (8 blocks x 1
-    // chunk each).  A 128K-token LLaMA-shaped request placed on measured
-    // weights (8145 staging blocks, 17 GB) gathers at 2588 GB/s copied this way
-    // against 2536-2540 with grid-stride half-chunk units, the previous form:
-    // each workgroup then reads one chunk of neighbouring pool blocks and
-    // writes neighbouring slots of one per-layer buffer instead of a new
-    // page on both sides for every 16 KiB unit.
-    // The same tiles for the token-major retrieve through LDS: 2554 against
-    // 2527 GB/s copied on that request.
-    if (cls == KVP_CLASS_STAGING && op == KVP_OP_RETRIEVE) f |= KVP_LAUNCH_TILE;
+    // Staging class: non-temporal loads and stores, one unit per workgroup
+    // (default_grid); head-major pools in half-chunk units, the retrieve in
+    // chunk-major unit order.  Measured on a 128K-token LLaMA-shaped request
+    // placed on measured weights (8145 staging blocks, 17 GB), HBM traffic of
+    // the kernel alone: gather 5608 GB/s this way, 5526 in block order, 4907
+    // with the XCD renumbering, 5166 in workgroup-owned tiles of 8 blocks;
+    // store 5517 against 5418 in chunk-major order and 5103 for 8192
+    // grid-stride workgroups; token-major through LDS, gather 5519 and store
+    // 5353 against 5112 and 5111 in the earlier forms.  A plain copy on this
+    // GPU peaks in the same form (16 KiB per workgroup, non-temporal both
+    // ways) at 5.7 TB/s of traffic, where reads alone reach 7.2 and writes
+    // alone 5.9.  Beside the host-class kernel of the same request the link
+    // rate is unchanged.
+    if (cls == KVP_CLASS_STAGING) {
+        f |= KVP_LAUNCH_NT_LOAD | KVP_LAUNCH_NT_STORE;
+        if (spec.pool_layout == 0) f |= KVP_LAUNCH_SPLIT2 | (op == KVP_OP_RETRIEVE ? KVP_LAUNCH_CHUNK_MAJOR : 0u);
+    }
     return f;
 }
 
