@@ -373,8 +373,10 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
 /*
  * Measure each region's read rate into HBM, the b_i of Eq. 1: the region's
  * class kernel shape streams min(probe_bytes, capacity) bytes of the region
- * into a scratch buffer (allocated for the call); best of 3 timed runs after
- * a warm-up, in MB/s (>= 1).  Host regions are measured one at a time; all of
+ * into a scratch buffer (allocated for the call); an HBM staging region
+ * min(max(probe_bytes, 1 GiB), capacity), since the GPU's last-level cache
+ * holds the writes of a shorter copy and it would measure above the sustained
+ * rate.  Best of 3 timed runs after a warm-up, in MB/s (>= 1).  Host regions are measured one at a time; all of
  * them reach the GPU over the same host link, so KVP_MEASURE_SHARED_LINK
  * divides their figure by the number of host regions.  A file region is read
  * the way a retrieve reads it: its worker thread reads its file into the

@@ -113,17 +113,34 @@ void measure_file_regions(Pool &p, uint64_t probe_bytes, bool together, uint64_t
 }
 
 
+// An HBM region is read over at least this many bytes: a shorter copy leaves
+// much of its writes in the GPU's 256 MB last-level cache when the kernel
+// ends, and measures above the sustained rate (3.0-3.4 TB/s copied at 128-256
+// MiB with non-temporal loads, 2.6-2.8 from 512 MiB on, against about 2.8 for
+// a 17 GB gather).
+constexpr uint64_t kHbmProbeMin = 1ull << 30;
+
+// Bytes the probe of region r streams.
+static uint64_t probe_span(const Region &r, uint64_t probe_bytes)
+{
+    const uint64_t want = r.desc.type == KVP_REGION_STAGING ? std::max(probe_bytes, kHbmProbeMin) : probe_bytes;
+    return std::min<uint64_t>(want, r.capacity) & ~15ull;
+}
+
 // Read rate of every region (bytes from the region into HBM per second, in
-// MB/s): the region-class kernel's launch shape streams min(probe_bytes,
-// capacity) bytes from the region into a scratch buffer; best of 3 after one
-// warm-up.  Caller holds the pool lock and the device scope.
+// MB/s): the region-class kernel's launch shape streams probe_span bytes from
+// the region into a scratch buffer; best of 3 after one warm-up.  Caller
+// holds the pool lock and the device scope.
 void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps)
 {
     probe_bytes &= ~15ull;
+    uint64_t scratch_bytes = 16;
+    for (const Region &r : p.regions)
+        if (r.desc.type != KVP_REGION_FILE) scratch_bytes = std::max(scratch_bytes, probe_span(r, probe_bytes));
     void *scratch = nullptr;
-    if (hipMalloc(&scratch, probe_bytes) != hipSuccess || !scratch) {
+    if (hipMalloc(&scratch, scratch_bytes) != hipSuccess || !scratch) {
         clear_hip_error();
-        fail(KVP_ERR_NOMEM, "probe scratch of " + std::to_string(probe_bytes) + " bytes");
+        fail(KVP_ERR_NOMEM, "probe scratch of " + std::to_string(scratch_bytes) + " bytes");
     }
     hipEvent_t e0 = nullptr, e1 = nullptr;
     try {
@@ -136,7 +153,7 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
             const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
             n_host += cls == KVP_CLASS_HOST;
             hipStream_t st = p.s_stage;   // one probe at a time
-            const uint64_t n = std::min<uint64_t>(probe_bytes, reg.capacity) & ~15ull;
+            const uint64_t n = probe_span(reg, probe_bytes);
             const LaunchCfg &lc = p.launch[cls][KVP_OP_RETRIEVE];
             float best = 0.f;
             for (int it = 0; it < 4; ++it) {
