@@ -237,8 +237,10 @@ void FileWorkers::run(Worker &w)
                 }
             }
             if (--j.group->pending == 0) j.group->done_at = std::chrono::steady_clock::now();
+            // notified under the lock: a waiter that sees pending == 0 may destroy the
+            // group at once, so the group is not touched after the lock is released
+            j.group->cv.notify_all();
         }
-        j.group->cv.notify_all();
     }
 }
 

@@ -14,7 +14,9 @@
 //                 directory: spans written from an aligned buffer by the
 //                 workers and read back by them equal the bytes written; a
 //                 read past the end of a file is reported by io_wait as
-//                 KVP_ERR_IO with its message, and the group is usable again
+//                 KVP_ERR_IO with its message, and the group is usable again;
+//                 two host threads submitting to the same workers at once,
+//                 each with its own group, get their own spans back
 //   file regions  open_file_region creates and sizes a file, refuses an
 //                 existing regular file, and close_file_region removes what
 //                 it created; file_region_read returns unaligned ranges
@@ -32,6 +34,7 @@
 #include <random>
 #include <set>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "internal.hpp"
@@ -214,6 +217,31 @@ static void workers_round_trip(std::mt19937_64 &rng, const std::string &dir)
         bool zero = true;
         for (uint64_t i = 0; i < kSector; ++i) zero &= in[i] == 0;
         CHECK(zero || std::memcmp(in, out + file_bytes, kSector) == 0);
+
+        // two submitters at once: each writes its own half of every file, then reads it back
+        const uint64_t half = file_bytes / 2;
+        std::vector<char> ok(2, 0);
+        auto submitter = [&](int t) {
+            IoGroup mine;
+            char *src = out + t * half, *dst = in + t * half;   // [t*half, t*half + half) of each file's slice
+            for (int round = 0; round < 10; ++round) {
+                for (int f = 0; f < n_files; ++f)
+                    w.submit(f, IoJob{fds[f], true, t * half, half, src + f * file_bytes, &mine});
+                io_wait(mine);
+                for (int f = 0; f < n_files; ++f)
+                    w.submit(f, IoJob{fds[f], false, t * half, half, dst + f * file_bytes, &mine});
+                io_wait(mine);
+            }
+            bool same = true;
+            for (int f = 0; f < n_files; ++f)
+                same &= std::memcmp(dst + f * file_bytes, src + f * file_bytes, half) == 0;
+            ok[t] = same;
+        };
+        std::memset(in, 0, buf_bytes);
+        std::thread t0(submitter, 0), t1(submitter, 1);
+        t0.join();
+        t1.join();
+        CHECK(ok[0] && ok[1]);
     }
     for (int f = 0; f < n_files; ++f) {
         ::close(fds[f]);

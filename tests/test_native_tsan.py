@@ -1,6 +1,8 @@
 """The library's host code under ThreadSanitizer (CPU only): several threads
 place, extend, look up and release requests on one placement-only pool at
-once through the C ABI while others read it (tests/native/placement_threads.cpp).
+once through the C ABI while others read it (tests/native/placement_threads.cpp);
+and the storage tier's worker threads, fed by one and by two submitting
+threads (tests/native/file_io_test.cpp with fileio.cpp).
 
 The library's C++ sources are compiled here with g++ -fsanitize=thread and
 linked with the kernels object of the package build (GPU code, never called
@@ -38,6 +40,18 @@ def test_placement_from_many_threads_under_tsan(tmp_path):
     exe = str(tmp_path / "placement_threads")
     _run(["g++", "-fsanitize=thread", "-o", exe] + objs + [KERNELS_OBJ, "-L" + os.path.join(ROCM, "lib"),
          "-lamdhip64", "-Wl,-rpath," + os.path.join(ROCM, "lib"), "-pthread"])
+    env = dict(os.environ, TSAN_OPTIONS="halt_on_error=1 second_deadlock_stack=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "all checks passed" in r.stdout
+    assert "ThreadSanitizer" not in r.stderr, r.stderr
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_file_workers_under_tsan(tmp_path):
+    exe = str(tmp_path / "file_io_test")
+    _run(["g++"] + FLAGS + ["-pthread", os.path.join(ROOT, "tests", "native", "file_io_test.cpp"),
+                            os.path.join(CSRC, "fileio.cpp"), os.path.join(CSRC, "placement.cpp"), "-o", exe])
     env = dict(os.environ, TSAN_OPTIONS="halt_on_error=1 second_deadlock_stack=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
