@@ -234,3 +234,39 @@ def test_file_region_rules():
             assert bw[0] > 0 and bw[1] > 0
             assert p.region_info(0)["type"] == K.REGION_FILE and p.region_info(0)["host_ptr"] is None
         assert not os.path.exists(path), "the pool removes the file it created"
+
+
+def test_retrieves_from_threads_with_files():
+    """Four host threads retrieve their requests on four streams at once, three times each, with the
+    staging regions as file regions: the calls share the pool's ring and worker threads."""
+    import threading
+    wl = _with_files(workloads.make(5, max_blocks=80))
+    say("case file regions from threads")
+    with tempfile.TemporaryDirectory() as d:
+        run = WorkloadRun(wl, device=0, file_dir=d)
+        try:
+            run.pool.set_file_ring(4 << 20)                  # a few blocks a slot: many batches per call
+            host = run.setup(keep_host=True)
+            streams = [torch.cuda.Stream() for _ in wl.requests]
+            cur = torch.cuda.current_stream()
+            for s in streams:
+                s.wait_stream(cur)
+            errs = []
+
+            def work(i, q):
+                try:
+                    for _ in range(3):                       # idempotent: same blocks, same slots
+                        run.retrieve(q, streams[i])
+                except Exception as e:                       # reported below
+                    errs.append(e)
+
+            ts = [threading.Thread(target=work, args=(i, q)) for i, q in enumerate(wl.requests)]
+            for t in ts:
+                t.start()
+            for t in ts:
+                t.join()
+            torch.cuda.synchronize()
+            assert not errs, errs
+            check_full(wl, run, host)
+        finally:
+            run.close()
