@@ -526,6 +526,81 @@ def ablation(args):
                       "steps": args.steps, "warmup": args.warmup, "variants": res}), flush=True)
 
 
+def file_ablation(args):
+    """The paper's ablation (Sec. 5.3) on the storage tier: the staging regions of the workload become
+    file regions, and the same request is retrieved through
+      - passthrough only: the whole request on one O_DIRECT file region, no striping;
+      - orchestrator only: striped 4:4:1:1:1:1 over the host regions and four file regions that are
+        read through the page cache (the file system's path; each file's cached pages are dropped
+        before every retrieve, so the reads are cold);
+      - full: the same striping over O_DIRECT file regions, with the configured weights and with
+        weights the pool measures (files read together).
+    Retrieve ms per call, median of --steps after --warmup; all file regions in --file-dir."""
+    import copy
+    import dataclasses
+
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    torch.cuda.set_device(0)
+    base = workloads.make(args.config)
+    base.regions = [dataclasses.replace(r, kind="file") if r.kind == "staging" else r for r in base.regions]
+    R = workloads.RegionSpec
+
+    def drop_cached(paths):
+        for path in paths:
+            fd = os.open(path, os.O_RDONLY)
+            try:
+                os.fsync(fd)
+                os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+            finally:
+                os.close(fd)
+
+    def variant(name, regions, file_flags=0):
+        wl = copy.deepcopy(base)
+        wl.regions = regions
+        workloads._size_regions(wl.regions, [q.n_present for q in wl.requests], wl.shape.block_bytes)
+        run = WorkloadRun(wl, device=0, file_dir=args.file_dir, file_flags=file_flags)
+        try:
+            run.setup()
+            counts = [int(x) for x in np.bincount(run.maps[wl.requests[0].request_id]["region"].astype(np.int64),
+                                                 minlength=len(regions))]
+            ms = []
+            for i in range(args.warmup + args.steps):
+                if file_flags & K.FILE_BUFFERED:
+                    drop_cached(run.file_paths)
+                torch.cuda.synchronize()
+                t = time.perf_counter()
+                run.retrieve_all()
+                torch.cuda.synchronize()
+                if i >= args.warmup:
+                    ms.append((time.perf_counter() - t) * 1e3)
+            out = {"variant": name, "regions": [(r.kind, r.weight) for r in regions], "blocks": counts,
+                   "ms_median": round(statistics.median(ms), 1), "ms_min": round(min(ms), 1),
+                   "gbps": round(wl.retrieved_bytes / statistics.median(ms) / 1e6, 2)}
+        finally:
+            run.close()
+            torch.cuda.empty_cache()
+        log(json.dumps(out))
+        return out
+
+    import numpy as np
+    res = [variant("passthrough only: one O_DIRECT file region", [R("file", 1)]),
+           variant("orchestrator only: striped, files through the page cache", copy.deepcopy(base.regions),
+                   K.FILE_BUFFERED),
+           variant("full: striped, O_DIRECT files, configured weights", copy.deepcopy(base.regions))]
+    measured = measure_weights(torch, K, base, args.file_dir)
+    res.append(variant("full: striped, O_DIRECT files, measured weights",
+                       [dataclasses.replace(r, weight=int(w)) for r, w in zip(base.regions, measured)]))
+    print(json.dumps({"metric": "retrieval ms of one request by pool organisation, storage tier (ablation)",
+                      "workload": base.name + "-file", "retrieved_bytes": base.retrieved_bytes,
+                      "file_device": "the machine's virtio block device (a VM disk, not an NVMe drive)",
+                      "steps": args.steps, "warmup": args.warmup, "variants": res}), flush=True)
+
+
 def pipeline(args):
     """Layerwise pipelining (the paper's Sec. 2.2.1 and its blocked I/O time):
     layer l of the request is retrieved on one stream while a compute stream,
@@ -835,7 +910,8 @@ def main():
     ap.add_argument("--pipeline", action="store_true",
                     help="instead of the bench line, overlap per-layer retrieval with stand-in compute")
     ap.add_argument("--ablation", action="store_true",
-                    help="instead of the bench line, compare pool organisations on the same request")
+                    help="instead of the bench line, compare pool organisations on the same request "
+                         "(with --file-regions: striping and direct I/O on the storage tier)")
     ap.add_argument("--measured-weights", action="store_true",
                     help="place with Eq. 1 weights measured by the pool (kv_pool_measure_bandwidth, host regions "
                          "sharing one link) instead of the workload's configured weights")
@@ -862,7 +938,7 @@ def main():
         summarize_trace(args.summarize_trace, args.tag, args.bench_args, args.bench_json)
         return
     if args.gpus == 1 and args.ablation:
-        ablation(args)
+        file_ablation(args) if args.file_regions else ablation(args)
         return
     if args.gpus == 1 and args.pipeline:
         pipeline(args)
