@@ -624,7 +624,28 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         fa.cache = static_cast<const uint64_t *>(dev_base);
         LaunchCfg lf = p.launch[KVP_CLASS_HOST][op];
         lf.flags &= ~(KVP_LAUNCH_SDMA | KVP_LAUNCH_UPLOAD);
-        run_file_batches(p, gather, file_batches, spans, fa, lf, p.s_stage);
+        try {
+            run_file_batches(p, gather, file_batches, spans, fa, lf, p.s_stage);
+        } catch (...) {
+            // A file read or write failed.  The kernels of the batches before it are
+            // enqueued on the pool's stream and read this call's work list, so the call
+            // still joins them into the caller's stream and records its completion
+            // events after them (the work-list slot, the requests) before it returns
+            // the error; the cleanup does not throw, so that error is the one reported.
+            (void)hipEventRecord(p.stage_done, p.s_stage);
+            (void)hipStreamWaitEvent(s, p.stage_done, 0);
+            if (slot && hipEventRecord(slot->done, s) != hipSuccess) clear_hip_error();
+            for (RequestRec *rec : touched) {
+                if (rec->busy_rec && rec->busy_stream != s) (void)hipStreamWaitEvent(s, rec->busy, 0);
+                if (hipEventRecord(rec->busy, s) == hipSuccess) {
+                    rec->busy_rec = true;
+                    rec->busy_stream = s;
+                }
+                if (!gather && hipEventRecord(rec->stored, s) == hipSuccess) rec->stored_rec = true;
+            }
+            clear_hip_error();
+            throw;
+        }
         check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
         check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
     }

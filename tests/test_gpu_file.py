@@ -270,3 +270,56 @@ def test_retrieves_from_threads_with_files():
             check_full(wl, run, host)
         finally:
             run.close()
+
+
+def test_read_error_mid_call_then_the_pool_still_works(tmp_path):
+    """The file of a file region loses its second half after the store (truncated from the host), so
+    a retrieve's later batches hit the end of the file: the call reports IO; every destination slot
+    then holds its block's source values or the fill value (the batches before the failure may have
+    landed, nothing else); the request releases, and the same ranges placed, stored and retrieved
+    again come back exact."""
+    L, H, D = 4, 2, 64                                          # chunk 4 KiB, block 32 KiB
+    bb = 2 * L * H * 16 * D * 2
+    n, slots = 64, 80
+    sent = int(np.uint16(SENTINEL).view(np.int16))
+    path = str(tmp_path / "r1.bin")
+    say("case file read error mid-call")
+    with K.KVPool([K.Region("host", 64 * bb), K.Region("file", 64 * bb, path=path)], [1, 1],
+                  K.KVSpec(L, H, D), 0) as p:
+        p.set_file_ring(4 * bb)                                 # 4 blocks a batch: 8 batches from the file
+        g = torch.Generator().manual_seed(77)
+        src = torch.randint(-32768, 32767, (L, 2, slots, H, 16, D), dtype=torch.int16, generator=g).cuda()
+        dst = torch.full_like(src, sent)
+        ks, vs = [src[l, 0].data_ptr() for l in range(L)], [src[l, 1].data_ptr() for l in range(L)]
+        kd, vd = [dst[l, 0].data_ptr() for l in range(L)], [dst[l, 1].data_ptr() for l in range(L)]
+        s = torch.cuda.current_stream().cuda_stream
+        src_tab = list(range(n))
+        dst_tab = [(b * 7 + 3) % slots for b in range(n)]        # 7 is invertible mod 80: distinct slots
+        m = p.place(1, n)
+        assert int((m["region"] == 1).sum()) == n // 2
+        p.store(m, src_tab, slots, ks, vs, s)
+        torch.cuda.synchronize()
+        offs = np.sort(m["offset"][m["region"] == 1])
+        os.truncate(path, int(offs[len(offs) // 2]))            # the file keeps its first 16 blocks
+        with pytest.raises(K.KVPoolError) as ei:
+            p.retrieve(m, dst_tab, slots, kd, vd, s)
+        assert ei.value.name == "IO"
+        torch.cuda.synchronize()
+        landed = 0
+        for b in range(n):
+            got, want = dst[:, :, dst_tab[b]], src[:, :, src_tab[b]]
+            same = bool(torch.equal(got, want))
+            assert same or bool((got == sent).all()), "block %d: neither its values nor the fill value" % b
+            landed += same
+        free = sorted(set(range(slots)) - set(dst_tab))
+        assert bool((dst[:, :, free] == sent).all())
+        say("blocks landed before the failure", landed)
+        p.release(1)
+        m2 = p.place(2, n)                                      # first fit: over the same ranges
+        assert np.array_equal(m2["offset"], m["offset"]) and np.array_equal(m2["region"], m["region"])
+        p.store(m2, src_tab, slots, ks, vs, s)
+        dst.fill_(sent)
+        p.retrieve(m2, dst_tab, slots, kd, vd, s)
+        torch.cuda.synchronize()
+        for b in range(n):
+            assert torch.equal(dst[:, :, dst_tab[b]], src[:, :, src_tab[b]]), "block %d after the error" % b
