@@ -503,151 +503,163 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
                   "hipMemcpyAsync");
         slot->pending = true;  // from here on the slot is in use even if a launch fails
     }
-    if (ahead) {
-        check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
-        check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
-    }
-    if (fork_staging || !batches.empty() || !file_batches.empty())
-        check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
-
-    const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(dev_base) + ptr_bytes);
-    // Staging class forked onto the internal stream first, then the host
-    // class on the caller's stream itself; the caller's stream then waits for
-    // the staging kernel.  One extra stream keeps the pool within the few
-    // hardware queues a process gets, so caller streams (e.g. compute
-    // overlapping a layerwise retrieve) are not serialised behind it.
-    size_t first = 0;
-    CopyArgs args[2] = {geo, geo};
-    for (uint32_t c = 0; c < 2; ++c) {
-        args[c].items = dev_list + first;
-        args[c].cache = static_cast<const uint64_t *>(dev_base);
-        args[c].n_items = static_cast<uint32_t>(items[c].size());
-        first += items[c].size();
-    }
-    TimedCall *tc = p.timing && !noalloc ? &p.timed.back() : nullptr;
-    auto launch = [&](uint32_t c, hipStream_t st) {
-        const LaunchCfg &lc = c == KVP_CLASS_HOST ? lh : p.launch[c][op];
-        if (tc) check_hip(hipEventRecord(tc->t0[c], st), "hipEventRecord");
-        check_hip(launch_chunk_copy(args[c], c, gather, lc.grid, lc.flags, st), "kernel launch");
-        if (tc) {
-            check_hip(hipEventRecord(tc->t1[c], st), "hipEventRecord");
-            tc->ran[c] = true;
-        }
-    };
-    const bool staging = !items[KVP_CLASS_STAGING].empty();
-    if (batches.empty()) {
-        if (fork_staging) {
-            check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
-            launch(KVP_CLASS_STAGING, p.s_stage);
-            check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
-        } else if (staging) {
-            launch(KVP_CLASS_STAGING, s);   // small: in order on the caller's stream
-        }
-        if (host) {
-            take_link();
-            launch(KVP_CLASS_HOST, s);
-            hand_back_link();
-        }
-        if (fork_staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
-    } else {
-        // Copy-engine transport: the host-link copies take the internal
-        // stream (no stream beyond the kernel path's two) and every kernel
-        // runs on the caller's stream -- the staging class first, then one
-        // ring-slot kernel per batch.  A slot is refilled only after its
-        // previous contents were consumed (by any call, either op).
-        if (staging) launch(KVP_CLASS_STAGING, s);
-        const LaunchCfg &lc = p.launch[KVP_CLASS_STAGING][op];
-        const hipMemcpyKind kind = gather ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost;
-        hipStream_t sc = p.s_stage;
-        auto link_copies = [&](const Batch &bt) {
-            char *ring = p.bounce + static_cast<uint64_t>(bt.ring) * p.bounce_slot_bytes;
-            for (size_t i = bt.run0; i < bt.run0 + bt.runs; ++i) {
-                const LinkRun &run = runs[i];
-                char *hmem = static_cast<char *>(p.regions[run.region].host) + run.offset + skip;
-                char *dev = ring + run.slot_offset;
-                void *dst = gather ? static_cast<void *>(dev) : static_cast<void *>(hmem);
-                const void *src = gather ? static_cast<const void *>(hmem) : static_cast<const void *>(dev);
-                if (width == p.block_bytes)
-                    check_hip(hipMemcpyAsync(dst, src, run.blocks * width, kind, sc), "hipMemcpyAsync");
-                else
-                    check_hip(hipMemcpy2DAsync(dst, gather ? width : p.block_bytes, src, gather ? p.block_bytes : width,
-                                               width, run.blocks, kind, sc),
-                              "hipMemcpy2DAsync");
-            }
-        };
-        auto ring_kernel = [&](const Batch &bt) {
-            CopyArgs a = args[KVP_CLASS_HOST];
-            a.items = dev_list + bt.first;
-            a.n_items = bt.n;
-            check_hip(launch_chunk_copy(a, kClassRing, gather, lc.grid, lc.flags, s), "kernel launch");
-        };
-        if (gather) {
-            check_hip(hipStreamWaitEvent(sc, p.fork, 0), "hipStreamWaitEvent");
-            if (tc) check_hip(hipEventRecord(tc->t0[KVP_CLASS_HOST], sc), "hipEventRecord");
-            for (const Batch &bt : batches) {
-                if (p.bounce_free_rec[bt.ring])
-                    check_hip(hipStreamWaitEvent(sc, p.bounce_free[bt.ring], 0), "hipStreamWaitEvent");
-                link_copies(bt);
-                check_hip(hipEventRecord(p.bounce_filled[bt.ring], sc), "hipEventRecord");
-                check_hip(hipStreamWaitEvent(s, p.bounce_filled[bt.ring], 0), "hipStreamWaitEvent");
-                ring_kernel(bt);
-                check_hip(hipEventRecord(p.bounce_free[bt.ring], s), "hipEventRecord");
-                p.bounce_free_rec[bt.ring] = true;
-            }
+    // After a failure once the work list is on its way (a file read or write
+    // that fails, a launch or copy the runtime refuses), whatever was enqueued
+    // still runs and reads the work list.  So the caller's stream joins the
+    // pool's stream, and the work list's and the requests' completion events
+    // are recorded after all of it before the error is returned: a later call
+    // cannot rewrite the list under those kernels, and release waits for them.
+    // Nothing here throws, so the first error is the one reported.
+    auto settle = [&]() noexcept {
+        (void)hipEventRecord(p.stage_done, p.s_stage);
+        (void)hipStreamWaitEvent(s, p.stage_done, 0);
+        if (noalloc) {
+            if (hipEventRecord(sd->free, s) == hipSuccess) sd->free_rec = true;
         } else {
-            if (tc) check_hip(hipEventRecord(tc->t0[KVP_CLASS_HOST], s), "hipEventRecord");
-            for (const Batch &bt : batches) {
-                if (p.bounce_free_rec[bt.ring])
-                    check_hip(hipStreamWaitEvent(s, p.bounce_free[bt.ring], 0), "hipStreamWaitEvent");
-                ring_kernel(bt);
-                check_hip(hipEventRecord(p.bounce_filled[bt.ring], s), "hipEventRecord");
-                check_hip(hipStreamWaitEvent(sc, p.bounce_filled[bt.ring], 0), "hipStreamWaitEvent");
-                link_copies(bt);
-                check_hip(hipEventRecord(p.bounce_free[bt.ring], sc), "hipEventRecord");
-                p.bounce_free_rec[bt.ring] = true;
+            (void)hipEventRecord(slot->done, s);
+        }
+        for (RequestRec *rec : touched) {
+            if (rec->busy_rec && rec->busy_stream != s) (void)hipStreamWaitEvent(s, rec->busy, 0);
+            if (hipEventRecord(rec->busy, s) == hipSuccess) {
+                rec->busy_rec = true;
+                rec->busy_stream = s;
             }
-            check_hip(hipEventRecord(p.stage_done, sc), "hipEventRecord");
+            if (!gather && hipEventRecord(rec->stored, s) == hipSuccess) rec->stored_rec = true;
+        }
+        clear_hip_error();
+    };
+    auto enqueue = [&] {
+        if (ahead) {
+            check_hip(hipEventRecord(p.uploaded, p.s_stage), "hipEventRecord");
+            check_hip(hipStreamWaitEvent(s, p.uploaded, 0), "hipStreamWaitEvent");
+        }
+        if (fork_staging || !batches.empty() || !file_batches.empty())
+            check_hip(hipEventRecord(p.fork, s), "hipEventRecord");
+
+        const CopyItem *dev_list = reinterpret_cast<const CopyItem *>(static_cast<char *>(dev_base) + ptr_bytes);
+        // Staging class forked onto the internal stream first, then the host
+        // class on the caller's stream itself; the caller's stream then waits for
+        // the staging kernel.  One extra stream keeps the pool within the few
+        // hardware queues a process gets, so caller streams (e.g. compute
+        // overlapping a layerwise retrieve) are not serialised behind it.
+        size_t first = 0;
+        CopyArgs args[2] = {geo, geo};
+        for (uint32_t c = 0; c < 2; ++c) {
+            args[c].items = dev_list + first;
+            args[c].cache = static_cast<const uint64_t *>(dev_base);
+            args[c].n_items = static_cast<uint32_t>(items[c].size());
+            first += items[c].size();
+        }
+        TimedCall *tc = p.timing && !noalloc ? &p.timed.back() : nullptr;
+        auto launch = [&](uint32_t c, hipStream_t st) {
+            const LaunchCfg &lc = c == KVP_CLASS_HOST ? lh : p.launch[c][op];
+            if (tc) check_hip(hipEventRecord(tc->t0[c], st), "hipEventRecord");
+            check_hip(launch_chunk_copy(args[c], c, gather, lc.grid, lc.flags, st), "kernel launch");
+            if (tc) {
+                check_hip(hipEventRecord(tc->t1[c], st), "hipEventRecord");
+                tc->ran[c] = true;
+            }
+        };
+        const bool staging = !items[KVP_CLASS_STAGING].empty();
+        if (batches.empty()) {
+            if (fork_staging) {
+                check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
+                launch(KVP_CLASS_STAGING, p.s_stage);
+                check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
+            } else if (staging) {
+                launch(KVP_CLASS_STAGING, s);   // small: in order on the caller's stream
+            }
+            if (host) {
+                take_link();
+                launch(KVP_CLASS_HOST, s);
+                hand_back_link();
+            }
+            if (fork_staging) check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
+        } else {
+            // Copy-engine transport: the host-link copies take the internal
+            // stream (no stream beyond the kernel path's two) and every kernel
+            // runs on the caller's stream -- the staging class first, then one
+            // ring-slot kernel per batch.  A slot is refilled only after its
+            // previous contents were consumed (by any call, either op).
+            if (staging) launch(KVP_CLASS_STAGING, s);
+            const LaunchCfg &lc = p.launch[KVP_CLASS_STAGING][op];
+            const hipMemcpyKind kind = gather ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost;
+            hipStream_t sc = p.s_stage;
+            auto link_copies = [&](const Batch &bt) {
+                char *ring = p.bounce + static_cast<uint64_t>(bt.ring) * p.bounce_slot_bytes;
+                for (size_t i = bt.run0; i < bt.run0 + bt.runs; ++i) {
+                    const LinkRun &run = runs[i];
+                    char *hmem = static_cast<char *>(p.regions[run.region].host) + run.offset + skip;
+                    char *dev = ring + run.slot_offset;
+                    void *dst = gather ? static_cast<void *>(dev) : static_cast<void *>(hmem);
+                    const void *src = gather ? static_cast<const void *>(hmem) : static_cast<const void *>(dev);
+                    if (width == p.block_bytes)
+                        check_hip(hipMemcpyAsync(dst, src, run.blocks * width, kind, sc), "hipMemcpyAsync");
+                    else
+                        check_hip(hipMemcpy2DAsync(dst, gather ? width : p.block_bytes, src, gather ? p.block_bytes : width,
+                                                   width, run.blocks, kind, sc),
+                                  "hipMemcpy2DAsync");
+                }
+            };
+            auto ring_kernel = [&](const Batch &bt) {
+                CopyArgs a = args[KVP_CLASS_HOST];
+                a.items = dev_list + bt.first;
+                a.n_items = bt.n;
+                check_hip(launch_chunk_copy(a, kClassRing, gather, lc.grid, lc.flags, s), "kernel launch");
+            };
+            if (gather) {
+                check_hip(hipStreamWaitEvent(sc, p.fork, 0), "hipStreamWaitEvent");
+                if (tc) check_hip(hipEventRecord(tc->t0[KVP_CLASS_HOST], sc), "hipEventRecord");
+                for (const Batch &bt : batches) {
+                    if (p.bounce_free_rec[bt.ring])
+                        check_hip(hipStreamWaitEvent(sc, p.bounce_free[bt.ring], 0), "hipStreamWaitEvent");
+                    link_copies(bt);
+                    check_hip(hipEventRecord(p.bounce_filled[bt.ring], sc), "hipEventRecord");
+                    check_hip(hipStreamWaitEvent(s, p.bounce_filled[bt.ring], 0), "hipStreamWaitEvent");
+                    ring_kernel(bt);
+                    check_hip(hipEventRecord(p.bounce_free[bt.ring], s), "hipEventRecord");
+                    p.bounce_free_rec[bt.ring] = true;
+                }
+            } else {
+                if (tc) check_hip(hipEventRecord(tc->t0[KVP_CLASS_HOST], s), "hipEventRecord");
+                for (const Batch &bt : batches) {
+                    if (p.bounce_free_rec[bt.ring])
+                        check_hip(hipStreamWaitEvent(s, p.bounce_free[bt.ring], 0), "hipStreamWaitEvent");
+                    ring_kernel(bt);
+                    check_hip(hipEventRecord(p.bounce_filled[bt.ring], s), "hipEventRecord");
+                    check_hip(hipStreamWaitEvent(sc, p.bounce_filled[bt.ring], 0), "hipStreamWaitEvent");
+                    link_copies(bt);
+                    check_hip(hipEventRecord(p.bounce_free[bt.ring], sc), "hipEventRecord");
+                    p.bounce_free_rec[bt.ring] = true;
+                }
+                check_hip(hipEventRecord(p.stage_done, sc), "hipEventRecord");
+                check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
+            }
+            p.bounce_next = static_cast<uint32_t>((p.bounce_next + batches.size()) % kBounceSlots);
+            if (tc) {
+                check_hip(hipEventRecord(tc->t1[KVP_CLASS_HOST], s), "hipEventRecord");
+                tc->ran[KVP_CLASS_HOST] = true;
+            }
+        }
+        if (!file_batches.empty()) {
+            // file-region kernels on the pool's stream, beside the host-class
+            // kernel on the caller's, then joined back into the caller's stream
+            if (!fork_staging && batches.empty()) check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
+            CopyArgs fa = geo;
+            fa.items = dev_list + items[0].size() + items[1].size();
+            fa.cache = static_cast<const uint64_t *>(dev_base);
+            LaunchCfg lf = p.launch[KVP_CLASS_HOST][op];
+            lf.flags &= ~(KVP_LAUNCH_SDMA | KVP_LAUNCH_UPLOAD);
+            run_file_batches(p, gather, file_batches, spans, fa, lf, p.s_stage);
+            check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
             check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
         }
-        p.bounce_next = static_cast<uint32_t>((p.bounce_next + batches.size()) % kBounceSlots);
-        if (tc) {
-            check_hip(hipEventRecord(tc->t1[KVP_CLASS_HOST], s), "hipEventRecord");
-            tc->ran[KVP_CLASS_HOST] = true;
-        }
-    }
-    if (!file_batches.empty()) {
-        // file-region kernels on the pool's stream, beside the host-class
-        // kernel on the caller's, then joined back into the caller's stream
-        if (!fork_staging && batches.empty()) check_hip(hipStreamWaitEvent(p.s_stage, p.fork, 0), "hipStreamWaitEvent");
-        CopyArgs fa = geo;
-        fa.items = dev_list + items[0].size() + items[1].size();
-        fa.cache = static_cast<const uint64_t *>(dev_base);
-        LaunchCfg lf = p.launch[KVP_CLASS_HOST][op];
-        lf.flags &= ~(KVP_LAUNCH_SDMA | KVP_LAUNCH_UPLOAD);
-        try {
-            run_file_batches(p, gather, file_batches, spans, fa, lf, p.s_stage);
-        } catch (...) {
-            // A file read or write failed.  The kernels of the batches before it are
-            // enqueued on the pool's stream and read this call's work list, so the call
-            // still joins them into the caller's stream and records its completion
-            // events after them (the work-list slot, the requests) before it returns
-            // the error; the cleanup does not throw, so that error is the one reported.
-            (void)hipEventRecord(p.stage_done, p.s_stage);
-            (void)hipStreamWaitEvent(s, p.stage_done, 0);
-            if (slot && hipEventRecord(slot->done, s) != hipSuccess) clear_hip_error();
-            for (RequestRec *rec : touched) {
-                if (rec->busy_rec && rec->busy_stream != s) (void)hipStreamWaitEvent(s, rec->busy, 0);
-                if (hipEventRecord(rec->busy, s) == hipSuccess) {
-                    rec->busy_rec = true;
-                    rec->busy_stream = s;
-                }
-                if (!gather && hipEventRecord(rec->stored, s) == hipSuccess) rec->stored_rec = true;
-            }
-            clear_hip_error();
-            throw;
-        }
-        check_hip(hipEventRecord(p.stage_done, p.s_stage), "hipEventRecord");
-        check_hip(hipStreamWaitEvent(s, p.stage_done, 0), "hipStreamWaitEvent");
+    };
+    try {
+        enqueue();
+    } catch (...) {
+        settle();
+        throw;
     }
     if (noalloc) {
         check_hip(hipEventRecord(sd->free, s), "hipEventRecord");
