@@ -1331,8 +1331,8 @@ def main():
                    "retrieved_bytes": wl.retrieved_bytes, "host_link_bytes": host_bytes,
                    "staging_bytes": stage_bytes,
                    "regions": [(r.kind, r.weight) for r in wl.regions],
-                   "weights": ("measured by the pool: kv_pool_measure_bandwidth, 256 MiB per region, host "
-                               "regions sharing one link (MB/s)" + ("; from an earlier run (--weights)" if args.weights
+                   "weights": ("measured by the pool: kv_pool_measure_bandwidth, 256 MiB per region (HBM: 1 GiB), "
+                               "host regions sharing one link (MB/s)" + ("; from an earlier run (--weights)" if args.weights
                                                                     else "")) if measured else "configured",
                    "layout": "head-major chunks" if wl.layout == 0 else "token-major chunks",
                    "dst_slots": wl.dst_num_slots, "seed": wl.seed},

@@ -116,8 +116,9 @@ typedef struct kvp_pool kvp_pool;   /* opaque */
  *   bandwidths[n_regions] positive integer bandwidth weights b_i (any unit,
  *                        e.g. MB/s).  Integers keep floor(p_i * n) exact.
  *                        NULL: measure them (kv_pool_measure_bandwidth with
- *                        256 MiB per region, no flags) and use the result
- *                        (not allowed for placement-only pools).
+ *                        256 MiB per region and KVP_MEASURE_SHARED_LINK |
+ *                        KVP_MEASURE_FILES_TOGETHER) and use the result (not
+ *                        allowed for placement-only pools).
  *   spec                 KV shape; C = H*bs*D*elem_bytes must be a multiple
  *                        of 16 (and, for pool_layout 1, so must D*elem_bytes).
  *   hip_device           GPU ordinal.  -1 creates a placement-only pool: no
@@ -369,6 +370,7 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
 
 #define KVP_MEASURE_SHARED_LINK 1u  /* divide host regions' rate by their count */
 #define KVP_MEASURE_FILES_TOGETHER 2u /* read all file regions at once, as a retrieve does */
+#define KVP_MEASURE_SHARED_HBM  4u  /* divide staging regions' rate by their count */
 
 /*
  * Measure each region's read rate into HBM, the b_i of Eq. 1: the region's
@@ -378,7 +380,12 @@ int kv_pool_counts(const uint64_t *bandwidths, uint32_t n_regions, uint64_t n, u
  * holds the writes of a shorter copy and it would measure above the sustained
  * rate.  Best of 3 timed runs after a warm-up, in MB/s (>= 1).  Host regions are measured one at a time; all of
  * them reach the GPU over the same host link, so KVP_MEASURE_SHARED_LINK
- * divides their figure by the number of host regions.  A file region is read
+ * divides their figure by the number of host regions.  Staging regions are
+ * measured one at a time too; all of them are the one GPU's HBM, and
+ * KVP_MEASURE_SHARED_HBM divides their figure by their number (Eq. 1 then
+ * balances the host link against the whole HBM; on a 128K-token request that
+ * placed about 165 blocks on the host regions instead of 42 and retrieved in
+ * 6.26-6.35 ms against 6.17-6.23, so create does not use it).  A file region is read
  * the way a retrieve reads it: its worker thread reads its file into the
  * pool's pinned ring (min(probe_bytes, its share of the ring) bytes, best of 3
  * after a warm-up; a file the pool created is measured on a probe file

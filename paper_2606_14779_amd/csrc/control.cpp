@@ -146,12 +146,13 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
     try {
         check_hip(hipEventCreate(&e0), "hipEventCreate");
         check_hip(hipEventCreate(&e1), "hipEventCreate");
-        uint32_t n_host = 0;
+        uint32_t n_host = 0, n_staging = 0;
         for (size_t r = 0; r < p.regions.size(); ++r) {
             const Region &reg = p.regions[r];
             if (reg.desc.type == KVP_REGION_FILE) continue;   // below, all file regions together or one by one
             const uint32_t cls = reg.desc.type == KVP_REGION_HOST ? KVP_CLASS_HOST : KVP_CLASS_STAGING;
             n_host += cls == KVP_CLASS_HOST;
+            n_staging += cls == KVP_CLASS_STAGING;
             hipStream_t st = p.s_stage;   // one probe at a time
             const uint64_t n = probe_span(reg, probe_bytes);
             const LaunchCfg &lc = p.launch[cls][KVP_OP_RETRIEVE];
@@ -175,6 +176,10 @@ void measure_regions(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mb
         if ((flags & KVP_MEASURE_SHARED_LINK) && n_host > 1)
             for (size_t r = 0; r < p.regions.size(); ++r)
                 if (p.regions[r].desc.type == KVP_REGION_HOST) mbps[r] = std::max<uint64_t>(1, mbps[r] / n_host);
+        // staging regions are all read from the one GPU's HBM: the same split
+        if ((flags & KVP_MEASURE_SHARED_HBM) && n_staging > 1)
+            for (size_t r = 0; r < p.regions.size(); ++r)
+                if (p.regions[r].desc.type == KVP_REGION_STAGING) mbps[r] = std::max<uint64_t>(1, mbps[r] / n_staging);
     } catch (...) {
         if (e0) (void)hipEventDestroy(e0);
         if (e1) (void)hipEventDestroy(e1);
@@ -190,7 +195,8 @@ void pool_measure(Pool &p, uint64_t probe_bytes, uint32_t flags, uint64_t *mbps_
 {
     if (p.placement_only) fail(KVP_ERR_INVALID, "placement-only pool has no memory to measure");
     if (!mbps_out) fail(KVP_ERR_INVALID, "null output");
-    if (flags & ~(KVP_MEASURE_SHARED_LINK | KVP_MEASURE_FILES_TOGETHER)) fail(KVP_ERR_INVALID, "unknown flags");
+    if (flags & ~(KVP_MEASURE_SHARED_LINK | KVP_MEASURE_FILES_TOGETHER | KVP_MEASURE_SHARED_HBM))
+        fail(KVP_ERR_INVALID, "unknown flags");
     if (probe_bytes < (1u << 16) || probe_bytes > (1ull << 36)) fail(KVP_ERR_INVALID, "probe_bytes outside [64 KiB, 64 GiB]");
     std::lock_guard<std::mutex> lock(p.mu);
     DeviceScope dev(p.device);

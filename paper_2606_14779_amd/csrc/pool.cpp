@@ -486,7 +486,8 @@ Pool *pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths, ui
         if (!bandwidths) {
             // Eq. 1 from measured bandwidths: each region's read rate into HBM
             std::vector<uint64_t> mbps(n_regions);
-            measure_regions(*p, kCreateProbeBytes, 0, mbps.data());
+            measure_regions(*p, kCreateProbeBytes, KVP_MEASURE_SHARED_LINK | KVP_MEASURE_FILES_TOGETHER,
+                            mbps.data());
             for (uint32_t i = 0; i < n_regions; ++i) p->bandwidth[i] = p->regions[i].bandwidth = mbps[i];
         }
     } catch (...) {

@@ -33,6 +33,7 @@ LAUNCH_CHUNK_MAJOR = 64
 LAUNCH_UPLOAD = 128          # no small-call launch: upload the work list, one launch per class
 LAUNCH_TILE = 256            # workgroup-owned tiles of 8 work items x 1 chunk
 MEASURE_SHARED_LINK = 1
+MEASURE_SHARED_HBM = 4       # staging regions share the one GPU's HBM: their rate divided by their count
 MEASURE_FILES_TOGETHER = 2   # file regions read all at once, as a retrieve reads them
 
 LOC_DTYPE = np.dtype([("region", "<u4"), ("gen", "<u4"), ("offset", "<u8")])

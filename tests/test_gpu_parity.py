@@ -578,20 +578,22 @@ def test_store_in_layer_groups_then_retrieve(layout):
 
 def test_measured_bandwidths_drive_placement():
     """Pool organizer from measurement: rates are positive, HBM staging reads
-    beat the host link, the shared-link flag splits the host figure, and a pool
-    created without bandwidths places exactly as the oracle does with the
-    measured weights."""
-    regions = [K.Region("host", 64 << 20, -1), K.Region("host", 64 << 20, -1), K.Region("staging", 64 << 20)]
+    beat the host link, the shared-link flag splits the host figure and the
+    shared-HBM flag the staging figure (each by the number of such regions),
+    and a pool created without bandwidths places exactly as the oracle does
+    with the weights it measured."""
+    regions = [K.Region("host", 64 << 20, -1), K.Region("host", 64 << 20, -1), K.Region("staging", 64 << 20),
+               K.Region("staging", 64 << 20)]
     spec = K.KVSpec(2, 2, 64)
-    with K.KVPool(regions, [1, 1, 1], spec, 0) as p:
+    with K.KVPool(regions, [1, 1, 1, 1], spec, 0) as p:
         alone = p.measure_bandwidth(32 << 20)
-        shared = p.measure_bandwidth(32 << 20, K.MEASURE_SHARED_LINK)
+        shared = p.measure_bandwidth(32 << 20, K.MEASURE_SHARED_LINK | K.MEASURE_SHARED_HBM)
         say("measured MB/s", alone.tolist(), shared.tolist())
-        assert np.all(alone > 1000) and alone[2] > alone[0] and alone[2] > alone[1]
-        for h in (0, 1):
-            assert 0.3 < shared[h] / alone[h] < 0.7
+        assert np.all(alone > 1000) and min(alone[2:]) > max(alone[:2])
+        for r in range(4):
+            assert 0.3 < shared[r] / alone[r] < 0.7
     with K.KVPool(regions, None, spec, 0) as p:
-        bw = [p.region_info(i)["bandwidth"] for i in range(3)]
+        bw = [p.region_info(i)["bandwidth"] for i in range(4)]
         assert all(b > 1000 for b in bw)
         import oracle
         ora = oracle.Pool(bw, [r.capacity_bytes for r in regions], spec.block_bytes)
