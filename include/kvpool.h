@@ -498,8 +498,11 @@ int kv_pool_set_copy_ring(kvp_pool *pool, uint64_t slot_bytes);
 
 /* Bytes per slot of the file regions' 2-slot pinned ring (a multiple of 4096
  * in [64 KiB, 64 GiB]; raised to one block).  The ring is freed after the work
- * on it and allocated again at the new size.  Errors: INVALID (bad size, or
- * the pool has no file region), NOMEM, HIP. */
+ * on it and allocated again at the new size.  If that allocation fails
+ * (NOMEM), the pool has no ring: stores and retrieves with file entries, and
+ * kv_pool_measure_bandwidth on a pool with file regions, return NOMEM until a
+ * later call here succeeds; other transfers are unaffected.  Errors: INVALID
+ * (bad size, or the pool has no file region), NOMEM, HIP. */
 int kv_pool_set_file_ring(kvp_pool *pool, uint64_t slot_bytes);
 
 typedef struct {

@@ -68,6 +68,7 @@ def build(verbose: bool = False, extra: list[str] | None = None) -> str:
         exe = os.path.join(ROOT, "tests", "abi_client", "abi_client")
         cmd = ["g++"] + CXX_FLAGS + ["-I", INCLUDE, client_src, "-o", exe + ".tmp", "-L" + PKG, "-lkvpool",
                                      "-Wl,-rpath,$ORIGIN/../../paper_2606_14779_amd", "-L" + os.path.join(ROCM, "lib"), "-lamdhip64",
+                                     "-Wl,--export-dynamic-symbol=hipHostMalloc",
                                      "-Wl,-rpath," + os.path.join(ROCM, "lib")]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:

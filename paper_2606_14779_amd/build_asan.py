@@ -46,7 +46,7 @@ def build(kernels_obj: str) -> str:
     _run(["g++", "-O1", "-g", "-std=c++17"] + SAN + ["-D__HIP_PLATFORM_AMD__", "-isystem", os.path.join(ROCM, "include"),
          "-I", INCLUDE, os.path.join(ROOT, "tests", "abi_client", "abi_client.cpp"), "-o", exe + ".tmp", "-L" + OUT,
          "-lkvpool", "-Wl,-rpath,$ORIGIN/asan", "-L" + os.path.join(ROCM, "lib"), "-lamdhip64",
-         "-Wl,-rpath," + os.path.join(ROCM, "lib")])
+         "-Wl,-rpath," + os.path.join(ROCM, "lib"), "-Wl,--export-dynamic-symbol=hipHostMalloc"])
     os.replace(exe + ".tmp", exe)
     for o in objs:
         os.remove(o)

@@ -33,6 +33,8 @@ void measure_file_regions(Pool &p, uint64_t probe_bytes, bool together, uint64_t
     for (size_t r = 0; r < p.regions.size(); ++r)
         if (p.regions[r].desc.type == KVP_REGION_FILE) idx.push_back(r);
     if (idx.empty()) return;
+    if (!p.file_ring)   // only after a kv_pool_set_file_ring that could not allocate
+        fail(KVP_ERR_NOMEM, "file-region ring not allocated: set a smaller one with kv_pool_set_file_ring");
     for (uint32_t j = 0; j < kFileSlots; ++j) {   // the ring is idle
         io_drain(p.file_io[j]);
         if (p.file_free_rec[j]) check_hip(hipEventSynchronize(p.file_free[j]), "hipEventSynchronize");

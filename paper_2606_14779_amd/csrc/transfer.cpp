@@ -331,6 +331,8 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
     std::vector<FileSpan> spans;
     std::vector<FileBatch> file_batches;
     if (!file_blocks.empty()) {
+        if (!p.file_ring || p.file_slot_bytes < p.block_bytes)   // only after a kv_pool_set_file_ring that could not allocate
+            fail(KVP_ERR_NOMEM, "file-region ring not allocated: set a smaller one with kv_pool_set_file_ring");
         const FileGeometry fg{p.file_ring_dev, p.file_slot_bytes, kFileSlots, p.file_next, p.block_bytes,
                               p.chunk_bytes};
         plan_file(fg, file_blocks, skip, width, 2 * layer_begin, file_items, spans, file_batches);

@@ -6,11 +6,15 @@
 // slots, in two layer ranges, and checks again.  Last, a second pool made by
 // kv_pool_create_files with a host and a file region (a file created in a
 // temporary directory) stores and retrieves the request through the storage
-// tier and is checked the same way; destroying it removes the file.
+// tier and is checked the same way; a resize of its file ring that cannot
+// allocate (forced below) is reported as NOMEM, file transfers are refused
+// until a later resize succeeds, and then work again; destroying the pool
+// removes the file.
 // With the argument "exit-open" it instead leaves the pool open with a
 // retrieve still enqueued and returns from main: the process must end
 // cleanly (the library registers nothing that runs at exit).
 // Built by the package build step; run by tests/test_abi_client.py (GPU).
+#include <dlfcn.h>
 #include <hip/hip_runtime.h>
 #include <sys/stat.h>
 #include <unistd.h>
@@ -38,6 +42,19 @@
             return 1;                                                                        \
         }                                                                                    \
     } while (0)
+
+// Pinned host allocations larger than this fail (0: none do).  This
+// executable's hipHostMalloc takes the library's references to the runtime's
+// (the build exports it), so a ring resize can be made to fail on any machine.
+static size_t g_fail_pinned_above = 0;
+
+extern "C" hipError_t hipHostMalloc(void **ptr, size_t size, unsigned int flags)
+{
+    using Fn = hipError_t (*)(void **, size_t, unsigned int);
+    static const Fn real = reinterpret_cast<Fn>(dlvsym(RTLD_NEXT, "hipHostMalloc", "hip_4.2"));
+    if (g_fail_pinned_above && size > g_fail_pinned_above) return hipErrorOutOfMemory;
+    return real ? real(ptr, size, flags) : hipErrorNotInitialized;
+}
 
 int main(int argc, char **argv)
 {
@@ -181,6 +198,24 @@ int main(int argc, char **argv)
     if (check()) return 1;
     struct stat st;
     if (on_file == 0 || ::stat(file_path.c_str(), &st) != 0 || uint64_t(st.st_size) != 64 * block_bytes) ++bad;
+    // a ring resize that cannot allocate: NOMEM; file transfers and the file measurement refused with
+    // NOMEM; a resize that fits brings them back
+    g_fail_pinned_above = 64u << 20;
+    if (kv_pool_set_file_ring(fpool, 128u << 20) != KVP_ERR_NOMEM) ++bad;
+    g_fail_pinned_above = 0;
+    if (hipGetLastError() != hipSuccess) ++bad;   // no HIP error left behind
+    if (kv_pool_retrieve(fpool, map.data(), n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream) !=
+        KVP_ERR_NOMEM)
+        ++bad;
+    if (kv_pool_store(fpool, map.data(), n, src_table.data(), slots, k_src.data(), v_src.data(), stream) != KVP_ERR_NOMEM)
+        ++bad;
+    uint64_t mbps[2] = {0, 0};
+    if (kv_pool_measure_bandwidth(fpool, 1u << 20, 0, mbps) != KVP_ERR_NOMEM) ++bad;
+    TRY(kv_pool_set_file_ring(fpool, 2 * block_bytes));
+    for (uint32_t i = 0; i < 2 * L; ++i) HIPTRY(hipMemset(dst[i], 0xA5, layer_bytes));
+    TRY(kv_pool_retrieve(fpool, map.data(), n, dst_table.data(), slots, k_dst.data(), v_dst.data(), stream));
+    HIPTRY(hipStreamSynchronize(stream));
+    if (check()) return 1;
     kv_pool_destroy(fpool);
     if (::stat(file_path.c_str(), &st) == 0) ++bad;     // the pool removes the file it created
     ::rmdir(dir_tmpl);
@@ -191,7 +226,7 @@ int main(int argc, char **argv)
         std::fprintf(stderr, "abi client: %llu mismatching chunks or elements\n", (unsigned long long)bad);
         return 1;
     }
-    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, allocation-free call, copy engines both ways, file region)\n",
+    std::printf("abi client: %u blocks stored and retrieved exactly (small-call launch, upload path, allocation-free call, copy engines both ways, file region, file ring that cannot allocate)\n",
                 n);
     return 0;
 }
