@@ -58,7 +58,11 @@ def test_parity_scaled_workloads(cfg, layout):
                                         (5, K.LAUNCH_TILE | K.LAUNCH_UPLOAD),
                                         (65536, K.LAUNCH_TILE | K.LAUNCH_SPLIT2 | K.LAUNCH_UPLOAD),
                                         (96, K.LAUNCH_TILE | K.LAUNCH_XCD | K.LAUNCH_SPLIT2 | K.LAUNCH_UPLOAD),
-                                        (1, K.LAUNCH_TILE | K.LAUNCH_NT_LOAD | K.LAUNCH_UPLOAD)])
+                                        (1, K.LAUNCH_TILE | K.LAUNCH_NT_LOAD | K.LAUNCH_UPLOAD),
+                                        # one unit per workgroup (the grid capped at the unit count)
+                                        (1 << 20, K.LAUNCH_SPLIT2 | K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE |
+                                         K.LAUNCH_CHUNK_MAJOR | K.LAUNCH_UPLOAD),
+                                        (1 << 20, K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE | K.LAUNCH_UPLOAD)])
 def test_parity_launch_shapes(grid, flags):
     wl = workloads.make(2, max_blocks=45)
     say("case launch", grid, flags)
