@@ -821,8 +821,9 @@ def duplex(args):
     run = WorkloadRun(wl, device=0)
     if args.host_grid or args.host_flags:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, args.host_grid, args.host_flags)
-    if args.store_grid:
-        run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, args.store_grid, K.LAUNCH_NT_STORE)
+    if args.store_grid or args.store_flags >= 0:
+        run.pool.set_launch(K.CLASS_HOST, K.OP_STORE, args.store_grid,
+                            args.store_flags if args.store_flags >= 0 else K.LAUNCH_NT_STORE)
     if args.sdma:
         run.pool.set_launch(K.CLASS_HOST, K.OP_RETRIEVE, 0, K.LAUNCH_SDMA)
     run.setup()
@@ -862,7 +863,8 @@ def duplex(args):
            "link_gbps_both_directions": round(2 * host_bytes / both_ms / 1e6, 2),
            "launch": {"retrieve": "copy engines" if args.sdma else
                       {"grid": args.host_grid or "library default: 12, 48 while a store is in flight"},
-                      "store_grid": args.store_grid or 12}}
+                      "store": "copy engines" if args.store_flags >= 0 and args.store_flags & K.LAUNCH_SDMA else
+                      {"grid": args.store_grid or 12}}}
     print(json.dumps(out), flush=True)
     run.close()
 
