@@ -108,3 +108,77 @@ def test_random_case(seed):
                       shape, layout)
         got = dst.cpu().numpy().view(np.uint16)
         assert np.array_equal(got, expect)
+
+
+# shapes whose chunks pair up into 4096-byte sectors (file regions need 2 x chunk to be a multiple)
+_FILE_SHAPES = [(1, 1, 16, 64), (2, 2, 16, 64), (3, 4, 16, 64), (2, 1, 16, 128), (5, 2, 16, 128),
+                (1, 8, 16, 128), (4, 4, 4, 128), (2, 8, 8, 64)]
+
+
+@pytest.mark.parametrize("seed", list(range(int(os.environ.get("KVP_FUZZ_FILE_SEEDS", "16")))))
+def test_random_case_with_file_regions(seed, tmp_path):
+    """Random cases with some regions as file regions (the storage tier): shapes, region mixes and
+    weights, ring sizes from one block up, launch flags, absent entries; map, pool bytes (read back
+    through the library, i.e. from the files) and destination against the oracle."""
+    rng = np.random.default_rng(50000 + seed)
+    layout = int(rng.integers(0, 2))
+    L, H, bs, D = _FILE_SHAPES[int(rng.integers(0, len(_FILE_SHAPES)))]
+    spec = K.KVSpec(L, H, D, bs, 2, layout)
+    bb = spec.block_bytes
+    N = int(rng.integers(1, 6))
+    kinds = [str(rng.choice(["host", "staging", "file"])) for _ in range(N)]
+    kinds[int(rng.integers(0, N))] = "file"                                  # at least one file region
+    weights = [int(w) for w in rng.integers(1, 6, size=N)]
+    n = int(rng.integers(1, 120))
+    W = sum(weights)
+    caps = [((w * n // W + 1) * bb + 4095) // 4096 * 4096 + int(rng.integers(0, 3)) * 4096 for w in weights]
+    ring_blocks = int(rng.choice([1, 2, 3, 7, 64]))
+    flags = [int(rng.choice([0, K.LAUNCH_NT_LOAD | K.LAUNCH_NT_STORE, K.LAUNCH_UPLOAD])) for _ in range(2)]
+    say("fuzz file", seed, dict(layout=layout, shape=(L, H, bs, D), kinds=kinds, w=weights, n=n,
+                                ring_blocks=ring_blocks, flags=flags))
+    regions = [K.Region(k, c, path=str(tmp_path / ("r%d.bin" % i)) if k == "file" else None)
+               for i, (k, c) in enumerate(zip(kinds, caps))]
+    src_slots_n, dst_slots_n = n + int(rng.integers(0, 5)), n + int(rng.integers(0, 9))
+    src_slots = rng.permutation(src_slots_n)[:n].astype(np.int32)
+    dst_slots = rng.permutation(dst_slots_n)[:n].astype(np.int32)
+    host_src = np.zeros((L, 2, src_slots_n, H, bs, D), np.uint16)
+    kvgen.fill_cache(50000 + seed, 1, np.arange(n, dtype=np.uint64), src_slots, L, H, bs, D,
+                     [host_src[l, 0].ctypes.data for l in range(L)], [host_src[l, 1].ctypes.data for l in range(L)])
+    src = torch.from_numpy(host_src.view(np.int16)).cuda()
+    dst = torch.full((L, 2, dst_slots_n, H, bs, D), int(np.uint16(SENT).view(np.int16)), dtype=torch.int16,
+                     device="cuda")
+    kp = lambda t: [t[l, 0].data_ptr() for l in range(L)]           # noqa: E731
+    vp = lambda t: [t[l, 1].data_ptr() for l in range(L)]           # noqa: E731
+    with K.KVPool(regions, weights, spec, 0) as pool:
+        pool.set_file_ring(max(64 << 10, (ring_blocks * bb + 4095) // 4096 * 4096))
+        for op in (K.OP_RETRIEVE, K.OP_STORE):
+            pool.set_launch(K.CLASS_HOST, op, 0, flags[op] | (K.LAUNCH_NT_STORE if op == K.OP_STORE else 0))
+        m = pool.place(1, n)
+        ora = oracle.Pool(weights, caps, bb)
+        om = ora.place(1, n)
+        assert np.array_equal(m, om)
+        s = torch.cuda.current_stream().cuda_stream
+        pool.store(m, src_slots, src_slots_n, kp(src), vp(src), s)
+        rm = m.copy()
+        absent = rng.random(n) < 0.2
+        rm["region"][absent] = K.ABSENT
+        table = dst_slots.copy()
+        table[absent] = -1
+        pool.retrieve(rm, table, dst_slots_n, kp(dst), vp(dst), s)
+        torch.cuda.synchronize()
+        shape = (L, H, bs, D, 2)
+        oregions = [np.zeros(c, np.uint8) for c in caps]
+        oracle.store(om, src_slots, oregions, [host_src[l, 0] for l in range(L)],
+                     [host_src[l, 1] for l in range(L)], shape, layout)
+        for r in range(len(regions)):
+            offs = om["offset"][om["region"] == r]
+            if len(offs):
+                lo, hi = int(offs.min()), int(offs.max()) + bb
+                assert np.array_equal(pool.region_read(r, lo, hi - lo), oregions[r][lo:hi]), "region %d" % r
+        expect = np.full((L, 2, dst_slots_n, H, bs, D), SENT, np.uint16)
+        orm = om.copy()
+        orm["region"][absent] = oracle.ABSENT
+        oracle.gather(orm, table, oregions, [expect[l, 0] for l in range(L)], [expect[l, 1] for l in range(L)],
+                      shape, layout)
+        got = dst.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, expect)
