@@ -324,48 +324,3 @@ def test_read_error_mid_call_then_the_pool_still_works(tmp_path):
         for b in range(n):
             assert torch.equal(dst[:, :, dst_tab[b]], src[:, :, src_tab[b]]), "block %d after the error" % b
 
-
-def test_file_ring_allocation_failure_is_reported_and_recoverable(tmp_path):
-    """A ring resize that cannot be pinned (2 x 64 GiB on a machine with less memory) fails with NOMEM
-    and leaves no HIP error; file transfers and the file-region measurement are then refused with
-    NOMEM while host-only transfers work; a smaller resize brings the file path back, exact."""
-    psutil = pytest.importorskip("psutil")
-    if psutil.virtual_memory().total >= (128 << 30):
-        pytest.skip("this machine could pin a 128 GiB ring")
-    L, H, D = 4, 2, 64
-    bb = 2 * L * H * 16 * D * 2
-    n, slots = 16, 24
-    path = str(tmp_path / "r1.bin")
-    say("case file ring that cannot be allocated")
-    with K.KVPool([K.Region("host", 32 * bb), K.Region("file", 32 * bb, path=path)], [1, 1],
-                  K.KVSpec(L, H, D), 0) as p:
-        g = torch.Generator().manual_seed(5)
-        src = torch.randint(-32768, 32767, (L, 2, slots, H, 16, D), dtype=torch.int16, generator=g).cuda()
-        dst = torch.zeros_like(src)
-        ks, vs = [src[l, 0].data_ptr() for l in range(L)], [src[l, 1].data_ptr() for l in range(L)]
-        kd, vd = [dst[l, 0].data_ptr() for l in range(L)], [dst[l, 1].data_ptr() for l in range(L)]
-        s = torch.cuda.current_stream().cuda_stream
-        tab = list(range(n))
-        m = p.place(1, n)
-        p.store(m, tab, slots, ks, vs, s)
-        torch.cuda.synchronize()
-        with pytest.raises(K.KVPoolError) as ei:
-            p.set_file_ring(64 << 30)
-        assert ei.value.name == "NOMEM"
-        assert int(torch.full((8,), 2, device="cuda").sum()) == 16    # no HIP error left for the caller
-        for call in (lambda: p.retrieve(m, tab, slots, kd, vd, s), lambda: p.store(m, tab, slots, ks, vs, s),
-                     lambda: p.measure_bandwidth(1 << 20)):
-            with pytest.raises(K.KVPoolError) as ei:
-                call()
-            assert ei.value.name == "NOMEM"
-        host_only = m[m["region"] == 0]
-        host_tab = [b for b in range(n) if m["region"][b] == 0]
-        p.retrieve(host_only, host_tab, slots, kd, vd, s)            # no file entries: unaffected
-        torch.cuda.synchronize()
-        for b in host_tab:
-            assert torch.equal(dst[:, :, b], src[:, :, b])
-        p.set_file_ring(1 << 20)
-        dst.zero_()
-        p.retrieve(m, tab, slots, kd, vd, s)
-        torch.cuda.synchronize()
-        assert torch.equal(dst[:, :, :n], src[:, :, :n])
