@@ -60,8 +60,12 @@ def probes(torch, K, run, nbytes, same_bytes=0):
     sweep's, so that traces and counters tell the two apart."""
     res = {}
     cur = torch.cuda.current_stream()
-    if same_bytes >= (64 << 20):
-        n = same_bytes // 16384 * 16384
+    n = same_bytes // 16384 * 16384
+    free = torch.cuda.mem_get_info()[0] if same_bytes >= (64 << 20) else 0
+    if same_bytes >= (64 << 20) and 2 * n + (1 << 30) > free:
+        # two buffers of the staging side's size do not fit beside the caches and regions
+        res["hbm_copy_same_bytes_skipped"] = "needs 2 x %d B of HBM, %d B free" % (n, free)
+    elif same_bytes >= (64 << 20):
         a = torch.empty(n // 2, dtype=torch.int16, device="cuda")
         b = torch.empty_like(a)
         a.fill_(1)
