@@ -605,6 +605,131 @@ def file_ablation(args):
                       "steps": args.steps, "warmup": args.warmup, "variants": res}), flush=True)
 
 
+def host_staged(args):
+    """The paper's host path on this machine (Sec. 4.3: the KV is read into host memory, then
+    transferred to the GPU), for the host-region part of the request, against the zero-copy kernel on
+    the same blocks.  CPU threads (all the process may use) gather the blocks -- each a contiguous
+    block-sized range of its region -- into a pinned buffer, one slice at a time; each slice goes to
+    HBM by an asynchronous copy as soon as it is gathered, so the next slice's gather overlaps it;
+    then a scatter (torch index_copy_, one per layer and K/V) puts every chunk in its slot of the paged
+    cache.  The HBM staging regions are left out: a CPU cannot read them.  The destination is then
+    compared with the source slots on the GPU."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    from kvgen import workloads
+    from paper_2606_14779_amd import kvpool as K
+    from paper_2606_14779_amd.runner import WorkloadRun
+
+    torch.cuda.set_device(0)
+    wl = workloads.make(args.config, context_tokens=args.context)
+    if wl.layout != 0 or len(wl.requests) != 1:
+        raise SystemExit("--host-staged takes a one-request head-major workload")
+    sh = wl.shape
+    bb, C, L2 = sh.block_bytes, sh.chunk_bytes, 2 * sh.layers
+    run = WorkloadRun(wl, device=0)
+    try:
+        run.setup()
+        q = wl.requests[0]
+        m = run.retrieve_maps[q.request_id]
+        host_idx = [i for i, r in enumerate(wl.regions) if r.kind == "host"]
+        hb = np.nonzero(np.isin(m["region"], host_idx))[0]
+        n = len(hb)
+        base = {r: run.pool.region_info(r)["host_ptr"] for r in host_idx}
+        src_ptr = [base[int(m["region"][b])] + int(m["offset"][b]) for b in hb]
+        pinned = torch.empty(n * bb, dtype=torch.uint8, pin_memory=True)
+        dev = torch.empty(n * bb, dtype=torch.uint8, device="cuda")
+        pin0 = pinned.data_ptr()
+        threads = len(os.sched_getaffinity(0))
+        slices = 8
+        import concurrent.futures as cf
+        pool = cf.ThreadPoolExecutor(max_workers=threads)
+
+        def gather(lo, hi):                        # blocks [lo, hi) into the pinned buffer
+            step = max(1, (hi - lo + threads - 1) // threads)
+
+            def part(a):
+                for i in range(a, min(hi, a + step)):
+                    ctypes.memmove(pin0 + i * bb, src_ptr[i], bb)
+            list(pool.map(part, range(lo, hi, step)))
+
+        bounds = [n * k // slices for k in range(slices + 1)]
+        stream = torch.cuda.Stream()
+        slot_idx = torch.as_tensor(q.dst_slots[hb].astype(np.int64), device="cuda")
+        dst8 = run.dst.view(torch.uint8).view(L2, wl.dst_num_slots, C)
+        buf3 = dev.view(n, L2, C)
+
+        def scatter():
+            with torch.cuda.stream(stream):
+                for c in range(L2):
+                    dst8[c].index_copy_(0, slot_idx, buf3[:, c, :])
+
+        def pipelined():
+            with torch.cuda.stream(stream):
+                for k in range(slices):
+                    lo, hi = bounds[k], bounds[k + 1]
+                    gather(lo, hi)
+                    dev[lo * bb:hi * bb].copy_(pinned[lo * bb:hi * bb], non_blocking=True)
+            scatter()
+            stream.synchronize()
+
+        def wall(fn):
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t) * 1e3
+
+        def h2d():
+            with torch.cuda.stream(stream):
+                dev.copy_(pinned, non_blocking=True)
+            stream.synchronize()
+
+        def scatter_sync():
+            scatter()
+            stream.synchronize()
+
+        res = {"gather": [], "h2d": [], "scatter": [], "pipelined": []}
+        for i in range(args.warmup + args.steps):
+            run.fill_dst()
+            g = wall(lambda: gather(0, n))
+            t = wall(h2d)
+            sc = wall(scatter_sync)
+            run.fill_dst()
+            pl = wall(pipelined)
+            if i >= args.warmup:
+                for k, v in (("gather", g), ("h2d", t), ("scatter", sc), ("pipelined", pl)):
+                    res[k].append(v)
+        # the destination after the last pipelined run: every host block's slot equals its source slot
+        src8 = run.src.view(torch.uint8).view(L2, wl.src_num_slots, C)
+        sidx = torch.as_tensor(q.src_slots[hb].astype(np.int64), device="cuda")
+        ok = all(torch.equal(dst8[c].index_select(0, slot_idx), src8[c].index_select(0, sidx)) for c in range(L2))
+        # the zero-copy kernel on the same blocks
+        mh = m.copy()
+        mh["region"][~np.isin(mh["region"], host_idx)] = K.ABSENT
+        kp, vp = run.layer_ptrs(run.dst)
+        cur = torch.cuda.current_stream()
+        zc = []
+        for i in range(args.warmup + args.steps):
+            t = wall(lambda: run.pool.retrieve(mh, q.dst_slots, wl.dst_num_slots, kp, vp, cur.cuda_stream))
+            if i >= args.warmup:
+                zc.append(t)
+        pool.shutdown()
+        med = {k: round(statistics.median(v), 2) for k, v in res.items()}
+        out = {"metric": "host-region part of one request: the paper's host path (CPU gather into pinned memory, "
+                         "copy to HBM, scatter) against the zero-copy kernel",
+               "workload": wl.name, "blocks": int(n), "bytes": int(n * bb), "cpu_threads": threads,
+               "slices": slices, "cpu_gather_ms": med["gather"], "h2d_ms": med["h2d"],
+               "scatter_ms": med["scatter"], "serial_ms": round(med["gather"] + med["h2d"] + med["scatter"], 2),
+               "pipelined_ms": med["pipelined"], "zero_copy_kernel_ms": round(statistics.median(zc), 2),
+               "verified": bool(ok), "steps": args.steps, "warmup": args.warmup}
+        print(json.dumps(out), flush=True)
+    finally:
+        run.close()
+
+
 def pipeline(args):
     """Layerwise pipelining (the paper's Sec. 2.2.1 and its blocked I/O time):
     layer l of the request is retrieved on one stream while a compute stream,
@@ -915,6 +1040,9 @@ def main():
                     help="with --pipeline: the per-layer compute stand-in (compute-bound GEMM or HBM-bound copy)")
     ap.add_argument("--pipeline", action="store_true",
                     help="instead of the bench line, overlap per-layer retrieval with stand-in compute")
+    ap.add_argument("--host-staged", action="store_true",
+                    help="instead of the bench line, the paper's host path (CPU gather into pinned memory, copy "
+                         "to HBM, scatter) against the zero-copy kernel on the request's host-region blocks")
     ap.add_argument("--ablation", action="store_true",
                     help="instead of the bench line, compare pool organisations on the same request "
                          "(with --file-regions: striping and direct I/O on the storage tier)")
@@ -945,6 +1073,9 @@ def main():
         return
     if args.gpus == 1 and args.ablation:
         file_ablation(args) if args.file_regions else ablation(args)
+        return
+    if args.gpus == 1 and args.host_staged:
+        host_staged(args)
         return
     if args.gpus == 1 and args.pipeline:
         pipeline(args)
