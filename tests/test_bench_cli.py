@@ -29,7 +29,8 @@ def test_help_lists_every_mode():
                  "--pipeline", "--latency", "--duplex", "--ablation", "--layerwise", "--no-cpu-baseline",
                  "--no-probes", "--no-copy-engine", "--host-grid", "--staging-grid", "--store-grid", "--stand-in",
                  "--batch", "--context", "--upload", "--store-flags", "--decode", "--measured-weights",
-                 "--summarize-pmc", "--summarize-trace"):
+                 "--summarize-pmc", "--summarize-trace", "--weights", "--file-regions", "--file-dir",
+                 "--host-staged", "--store-staging-grid", "--store-staging-flags"):
         assert flag in r.stdout, flag
 
 
