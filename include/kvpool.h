@@ -167,7 +167,7 @@ int kv_pool_create(const kvp_region_desc *regions, const uint64_t *bandwidths,
  * and kv_pool_set_timing do not cover them.  A failed file read or write
  * returns KVP_ERR_IO; batches enqueued before it may have reached the engine
  * cache (retrieve) or the file (store).
- * Errors: as kv_pool_create, plus IO (creating or sizing a file).
+ * Errors: as kv_pool_create, plus IO (creating a file or reserving its space).
  */
 int kv_pool_create_files(const kvp_region_desc *regions, const uint64_t *bandwidths,
                          uint32_t n_regions, const kvp_kv_spec *spec, int hip_device,

@@ -293,11 +293,18 @@ void open_file_region(Region &r, const char *path)
             fail(KVP_ERR_INVALID, std::string("cannot create ") + path + ": " + std::strerror(e) +
                                       (e == EINVAL && direct ? " (no O_DIRECT on this file system: KVP_FILE_BUFFERED)" : ""));
         }
-        if (::ftruncate(fd, static_cast<off_t>(r.capacity)) != 0) {
+        // the region's blocks are reserved on the disk now, so a later store cannot run out of
+        // space part-way and writes do not allocate; a file system without fallocate gets a sparse file
+        if (::fallocate(fd, 0, 0, static_cast<off_t>(r.capacity)) != 0) {
             const int e = errno;
-            ::close(fd);
-            ::unlink(path);
-            fail(KVP_ERR_IO, std::string("cannot size ") + path + ": " + std::strerror(e));
+            const bool unsupported = e == EOPNOTSUPP || e == ENOSYS || e == EINVAL;
+            if (!unsupported || ::ftruncate(fd, static_cast<off_t>(r.capacity)) != 0) {
+                const int e2 = unsupported ? errno : e;
+                ::close(fd);
+                ::unlink(path);
+                fail(KVP_ERR_IO, std::string("cannot reserve ") + std::to_string(r.capacity) + " bytes for " + path +
+                                     ": " + std::strerror(e2));
+            }
         }
         r.fd = fd;
         r.file_owned = true;

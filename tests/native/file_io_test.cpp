@@ -262,6 +262,9 @@ static void region_life_cycle(const std::string &dir)
     open_file_region(r, path.c_str());
     struct stat st;
     CHECK(::stat(path.c_str(), &st) == 0 && static_cast<uint64_t>(st.st_size) == r.capacity && r.file_owned);
+    // reserved on the disk where the file system can (st_blocks counts 512-byte units)
+    std::printf("region file: %llu bytes, %llu allocated\n", (unsigned long long)st.st_size,
+                (unsigned long long)st.st_blocks * 512ull);
     // bytes written through the descriptor come back through file_region_read at unaligned ranges
     char *buf = nullptr;
     CHECK(::posix_memalign(reinterpret_cast<void **>(&buf), kSector, r.capacity) == 0);
