@@ -230,6 +230,8 @@ int kv_pool_lookup(kvp_pool *pool, uint64_t request_id, uint32_t n_blocks, kvp_l
  *                        enqueueing.  A later retrieve of these blocks on any
  *                        stream waits for this store.
  * Map entries must be blocks of live placements (else STALE) and distinct.
+ * n_blocks * 4 * L may not exceed 2^31 (INVALID), for this call and for
+ * kv_pool_retrieve and their layerwise forms.
  * Errors: INVALID, STALE, HIP.
  */
 int kv_pool_store(kvp_pool *pool, const kvp_loc *map, uint32_t n_blocks,

@@ -222,7 +222,9 @@ void pool_transfer(Pool &p, const kvp_loc *map, uint32_t n_blocks, const int32_t
         if (!k || !v || (k & 15) || (v & 15))
             fail(KVP_ERR_INVALID, "layer " + std::to_string(l) + ": null or unaligned cache pointer");
     }
-    if (static_cast<uint64_t>(n_blocks) * 4 * L >= (1ull << 32)) fail(KVP_ERR_INVALID, "request too large");
+    // a kernel's units (blocks x 2L chunks x at most 2 parts) and its workgroup stride (at most 2^20)
+    // are summed in 32 bits: at most 2^31 units keeps that sum from wrapping
+    if (static_cast<uint64_t>(n_blocks) * 4 * L > (1ull << 31)) fail(KVP_ERR_INVALID, "request too large");
 
     std::lock_guard<std::mutex> lock(p.mu);
     DeviceScope dev(p.device);

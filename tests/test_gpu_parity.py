@@ -1038,3 +1038,30 @@ def test_hundreds_of_requests_in_one_call(sdma):
         check_tags(tags, dst.cpu().numpy(), src_slots, dst_slots, sentinel)
         for i in range(len(sizes)):
             pool.release(1000 + i)
+
+
+def test_request_size_limit():
+    """n_blocks * 4 * L may reach 2^31 and no more: a kernel's units and its workgroup stride are summed
+    in 32 bits.  At the limit, a map of absent entries is accepted (and moves nothing); one block more
+    is refused with INVALID before anything is read or launched."""
+    L = 32
+    spec = K.KVSpec(L, 1, 8)                                   # 256-byte chunks
+    cache = torch.zeros(L, 2, 4, 16, 8, dtype=torch.int16, device="cuda")
+    ks = [cache[l, 0].data_ptr() for l in range(L)]
+    vs = [cache[l, 1].data_ptr() for l in range(L)]
+    s = torch.cuda.current_stream().cuda_stream
+    limit = (1 << 31) // (4 * L)
+    with K.KVPool([K.Region("staging", 1 << 20)], [1], spec, 0) as p:
+        for n, ok in ((limit, True), (limit + 1, False)):
+            m = np.zeros(n, dtype=K.LOC_DTYPE)
+            m["region"] = K.ABSENT
+            table = np.full(n, -1, np.int32)
+            if ok:
+                p.retrieve(m, table, 4, ks, vs, s)
+            else:
+                with pytest.raises(K.KVPoolError) as ei:
+                    p.retrieve(m, table, 4, ks, vs, s)
+                assert ei.value.name == "INVALID" and "too large" in str(ei.value)
+            del m, table
+    torch.cuda.synchronize()
+    assert int(cache.abs().sum()) == 0
