@@ -187,14 +187,18 @@ void FileWorkers::shutdown()
 
 void FileWorkers::submit(size_t worker, const IoJob &job)
 {
+    Worker &w = *w_.at(worker);
     {
         std::lock_guard<std::mutex> g(job.group->mu);
         ++job.group->pending;
     }
-    Worker &w = *w_.at(worker);
-    {
+    try {
         std::lock_guard<std::mutex> lock(w.mu);
         w.q.push_back(job);
+    } catch (...) {   // not queued: take it back off the count, or a wait on the group never ends
+        std::lock_guard<std::mutex> g(job.group->mu);
+        if (--job.group->pending == 0) job.group->cv.notify_all();
+        throw;
     }
     w.cv.notify_one();
 }
