@@ -182,3 +182,12 @@ def test_random_case_with_file_regions(seed, tmp_path):
                       shape, layout)
         got = dst.cpu().numpy().view(np.uint16)
         assert np.array_equal(got, expect)
+        # a random layer range into a fresh destination: file spans narrower than a block
+        lo = int(rng.integers(0, L))
+        hi = int(rng.integers(lo + 1, L + 1))
+        dst.fill_(int(np.uint16(SENT).view(np.int16)))
+        pool.retrieve_layers(rm, table, dst_slots_n, lo, hi, kp(dst), vp(dst), s)
+        torch.cuda.synchronize()
+        got = dst.cpu().numpy().view(np.uint16)
+        assert np.array_equal(got[lo:hi], expect[lo:hi]), "layers [%d, %d)" % (lo, hi)
+        assert np.all(got[:lo] == SENT) and np.all(got[hi:] == SENT)
