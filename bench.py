@@ -135,8 +135,8 @@ def probes(torch, K, run, nbytes, same_bytes=0):
 
 
 # rocprofv3 counter passes behind the PMC summaries in profiles/.  Each pass is one run of
-#   rocprofv3 --pmc <counters> --output-format csv -d gpurun_out/pmc_<tag>/<pass> -o <pass> -- python3 bench.py <args>
-# (at most 4 TCC counters per pass on gfx950); then `python3 bench.py --summarize-pmc gpurun_out/pmc_<tag>
+#   rocprofv3 --pmc <counters> --output-format csv -d <dir>/<pass> -o <pass> -- python3 bench.py <args>
+# (at most 4 TCC counters per pass on gfx950); then `python3 bench.py --summarize-pmc <dir>
 # --tag <tag> --bench-args "<args>"` writes profiles/retrieve_<tag>_pmc.txt.
 PMC_PASSES = [
     ("fetch", ["FETCH_SIZE"]),
@@ -195,11 +195,12 @@ def summarize_pmc(d, tag, bench_args, out_dir=None):
              "TCC_EA0_WRREQ_WRITE_IO_32B_sum": "wr_io", "TCC_EA0_WRREQ_WRITE_GMI_32B_sum": "wr_gmi"}
     lines = ["# rocprofv3 PMC summary: KV store / retrieve kernels, %s" % tag,
              "# passes (repository root on the MI355X machine, after `cd /tmp && export TMPDIR=/tmp`), one run each:"]
+    dn = os.path.normpath(d)   # the commands name the directory the passes were written to
     for name, counters in PMC_PASSES:
-        lines.append("#   rocprofv3 --pmc %s --output-format csv -d gpurun_out/pmc_%s/%s -o %s -- python3 bench.py %s"
-                     % (" ".join(counters), tag, name, name, bench_args))
-    lines += ["# then: python3 bench.py --summarize-pmc gpurun_out/pmc_%s --tag %s --bench-args \"%s\""
-              % (tag, tag, bench_args),
+        lines.append("#   rocprofv3 --pmc %s --output-format csv -d %s/%s -o %s -- python3 bench.py %s"
+                     % (" ".join(counters), dn, name, name, bench_args))
+    lines += ["# then: python3 bench.py --summarize-pmc %s --tag %s --bench-args \"%s\""
+              % (dn, tag, bench_args),
               "# Values are means per dispatch.  *_bytes = 32 x the 32-byte request counters, per destination",
               "# (dram: HBM; io: the host link; gmi: another die), unscaled.  fetch_bytes / write_bytes =",
               "# FETCH_SIZE / WRITE_SIZE x 1024 x the scale that makes the 4 GiB probe copy read / write 4 GiB.",
@@ -243,10 +244,10 @@ def summarize_trace(d, tag, bench_args, bench_json):
         per[(t["Kernel_Name"], gx // max(1, wx))].append((int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e6)
     out = ["# Kernel trace summary: %s" % tag, "",
            "Command (repository root on the MI355X machine, after `cd /tmp && export TMPDIR=/tmp`):", "",
-           "    rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/kt_%s -o kt -- python3 bench.py %s"
-           % (tag, bench_args), "",
-           "then `python3 bench.py --summarize-trace gpurun_out/kt_%s --tag %s --bench-args \"%s\" --bench-json <its "
-           "JSON line>`." % (tag, tag, bench_args), "",
+           "    rocprofv3 --kernel-trace --stats --output-format csv -d %s -o kt -- python3 bench.py %s"
+           % (os.path.normpath(d), bench_args), "",
+           "then `python3 bench.py --summarize-trace %s --tag %s --bench-args \"%s\" --bench-json <its "
+           "JSON line>`." % (os.path.normpath(d), tag, bench_args), "",
            "kernels.hip sha256: `%s`" % kernels_sha(), "", "## rocprofv3 --stats", "",
            "| Kernel | Calls | Avg ms | Min ms | Max ms | % |", "|---|---:|---:|---:|---:|---:|"]
     for r in stats[:16]:
