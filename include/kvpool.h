@@ -24,9 +24,11 @@
  *     calling thread's last failure.
  *   - All arguments are checked before any GPU work is enqueued.  A call
  *     that fails (its checks, or the library's host memory running out) has
- *     no side effects, with one exception: a HIP runtime error
- *     (KVP_ERR_HIP) met while a store or retrieve enqueues its work may
- *     leave part of that work enqueued.
+ *     no side effects, with two exceptions: a HIP runtime error (KVP_ERR_HIP)
+ *     met while a store or retrieve enqueues its work, and a failed read or
+ *     write of a file region (KVP_ERR_IO), may leave part of that work
+ *     enqueued or done.  The call still orders what it enqueued before later
+ *     work on its stream and before a release of the requests it touched.
  *   - "stream" is a hipStream_t passed as void* (NULL = the null stream).
  *   - Host arrays passed in (maps, block tables, pointer tables) may be freed
  *     as soon as the call returns: the library copies what it keeps.
