@@ -1449,9 +1449,12 @@ def main():
     store_roof = None
     if store and host_blocks:
         a = host_bytes / (store["host_kernel_ms_avg"] / 1e3) / 1e9
+        trw = pmc_traffic(wl.name, "host_region_copy<false, %d," % kform)
         store_roof = {"bound": "pcie", "kernel": "host_region_copy<false,...> (zero-copy store to pinned host regions)",
                       "achieved": round(a, 2), "peak": PCIE5_X16_GBPS, "unit": "GB/s",
                       "frac": round(a / PCIE5_X16_GBPS, 4),
+                      "traffic": round(trw["fetch_bytes"] + trw["write_bytes"]) if trw else None,
+                      "traffic_detail": traffic_detail(trw, host_bytes, host_bytes),
                       "measured_peak": pr["d2h_peak_gbps"] if pr else None,
                       "frac_measured": round(a / pr["d2h_peak_gbps"], 4) if pr else None}
 
