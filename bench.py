@@ -244,8 +244,9 @@ def summarize_trace(d, tag, bench_args, bench_json):
         per[(t["Kernel_Name"], gx // max(1, wx))].append((int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e6)
     out = ["# Kernel trace summary: %s" % tag, "",
            "Command (repository root on the MI355X machine, after `cd /tmp && export TMPDIR=/tmp`):", "",
-           "    rocprofv3 --kernel-trace --stats --output-format csv -d %s -o kt -- python3 bench.py %s"
-           % (os.path.normpath(d), bench_args), "",
+           "    rocprofv3 --kernel-trace%s --stats --output-format csv -d %s -o kt -- python3 bench.py %s"
+           % (" --memory-copy-trace" if os.path.exists(os.path.join(d, "kt_memory_copy_stats.csv")) else "",
+              os.path.normpath(d), bench_args), "",
            "then `python3 bench.py --summarize-trace %s --tag %s --bench-args \"%s\" --bench-json <its "
            "JSON line>`." % (os.path.normpath(d), tag, bench_args), "",
            "kernels.hip sha256: `%s`" % kernels_sha(), "", "## rocprofv3 --stats", "",
@@ -259,14 +260,29 @@ def summarize_trace(d, tag, bench_args, bench_json):
     for (name, wg), ds in sorted(per.items(), key=lambda kv: -sum(kv[1]))[:16]:
         out.append("| `%s` | %d | %d | %.3f | %.3f |" % (name.split("(")[0].replace("void ", "")[:90], wg, len(ds),
                                                          sum(ds) / len(ds), min(ds)))
+    mc_stats = os.path.join(d, "kt_memory_copy_stats.csv")
+    if os.path.exists(mc_stats):   # a run with --memory-copy-trace as well
+        out += ["", "## rocprofv3 --stats: memory copies", "", "| Direction | Calls | Avg ms | Min ms | Max ms |",
+                "|---|---:|---:|---:|---:|"]
+        for r in csv.DictReader(open(mc_stats)):
+            out.append("| `%s` | %s | %.3f | %.3f | %.3f |" % (r["Name"], r["Calls"], float(r["AverageNs"]) / 1e6,
+                                                           float(r["MinNs"]) / 1e6, float(r["MaxNs"]) / 1e6))
+        mc = [(int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e6
+              for t in csv.DictReader(open(os.path.join(d, "kt_memory_copy_trace.csv")))]
+        longc = sorted(x for x in mc if x >= 10.0)
+        if longc:   # in a copy-engine run these are the whole ring slots (the trace records no sizes)
+            out += ["", "Copies of at least 10 ms: %d, median %.3f ms." % (len(longc), longc[len(longc) // 2])]
     if bench_json and os.path.exists(bench_json):
         b = json.loads(open(bench_json).read().strip().splitlines()[-1])
-        rf = b.get("roofline") or {}
-        ms = (rf.get("bytes_per_launch") or 0) / (rf.get("achieved") or 1) / 1e6
-        out += ["", "## Bench line of the same run", "",
-                "    value %.2f GB/s, ms_per_step %.3f; dominant kernel %s: %.3f ms per launch (HIP events), "
-                "%s %s = %.4f of %s" % (b["value"], b["ms_per_step"], rf.get("kernel", "?").split(" ")[0], ms,
-                                        rf.get("achieved"), rf.get("unit"), rf.get("frac") or 0, rf.get("peak"))]
+        if "value" in b and "roofline" in b:
+            rf = b.get("roofline") or {}
+            ms = (rf.get("bytes_per_launch") or 0) / (rf.get("achieved") or 1) / 1e6
+            out += ["", "## Bench line of the same run", "",
+                    "    value %.2f GB/s, ms_per_step %.3f; dominant kernel %s: %.3f ms per launch (HIP events), "
+                    "%s %s = %.4f of %s" % (b["value"], b["ms_per_step"], rf.get("kernel", "?").split(" ")[0], ms,
+                                            rf.get("achieved"), rf.get("unit"), rf.get("frac") or 0, rf.get("peak"))]
+        else:   # another mode's line (latency, duplex, ...): as printed
+            out += ["", "## JSON line of the same run", "", "    " + json.dumps(b)]
     path = os.path.join(ROOT, "profiles", "retrieve_%s_kernel_trace.md" % tag)
     open(path, "w").write("\n".join(out) + "\n")
     print("\n".join(out))
