@@ -234,6 +234,13 @@ def test_file_region_rules():
             assert bw[0] > 0 and bw[1] > 0
             assert p.region_info(0)["type"] == K.REGION_FILE and p.region_info(0)["host_ptr"] is None
         assert not os.path.exists(path), "the pool removes the file it created"
+        # measured together, each file region is credited with its probe bytes over the group's time:
+        # two regions of one size get the same rate, whatever the disk did meanwhile
+        paths2 = [os.path.join(d, "g%d.bin" % i) for i in range(2)]
+        with K.KVPool([K.Region("file", 8 << 20, path=q) for q in paths2], [1, 1], spec, 0) as p:
+            tog = p.measure_bandwidth(4 << 20, K.MEASURE_FILES_TOGETHER)
+            say("file regions together MB/s", tog.tolist())
+            assert tog[0] == tog[1] and tog[0] > 0
 
 
 def test_retrieves_from_threads_with_files():
